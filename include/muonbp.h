@@ -1,0 +1,177 @@
+/*
+ * muonbp.h -- C ABI of the MI355X (gfx950) MuonBP optimizer step.
+ *
+ * MuonBP (Khaled et al., arXiv 2510.16981, Sec. 3.2, Algorithm 1) keeps a
+ * heavy-ball momentum buffer per matrix, orthogonalizes it with K quintic
+ * Newton-Schulz iterations (Appendix B, Algorithm 2) either per block of an
+ * r x c shard grid (block steps) or over the whole matrix (full steps, when
+ * t mod P = 0), and applies the update with one of two stepsizes.
+ *
+ * Conventions for every function below:
+ *  - All entry points are plain C, never throw and never abort; they return a
+ *    muonbp_status.  A non-OK status from argument or shape validation leaves
+ *    the context usable; MUONBP_E_HIP poisons it (every later call that would
+ *    touch the GPU returns MUONBP_E_STATE).  muonbp_last_error() gives text.
+ *  - Matrices are row-major and contiguous (leading dimension = cols).
+ *    Pointers named "device" are HIP device pointers on the device that was
+ *    current at muonbp_create; they must be 16-byte aligned for full speed
+ *    (any element-aligned pointer is accepted).
+ *  - GPU work is enqueued on the context's stream and the call returns
+ *    without synchronising, unless stated otherwise.  The caller keeps every
+ *    pointer valid until that work completes (muonbp_synchronize).
+ *  - A context is not thread-safe; use one context per stream.
+ */
+#ifndef MUONBP_H
+#define MUONBP_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct muonbp_ctx muonbp_ctx; /* opaque, owned by the library */
+
+typedef enum {
+  MUONBP_OK = 0,
+  MUONBP_E_INVALID = 1, /* bad argument: NULL pointer, bad count, bad option  */
+  MUONBP_E_SHAPE = 2,   /* non-positive size, or grid does not divide matrix  */
+  MUONBP_E_DTYPE = 3,   /* unsupported dtype or dtype combination             */
+  MUONBP_E_NOMEM = 4,   /* device or host allocation failed                   */
+  MUONBP_E_HIP = 5,     /* a HIP runtime call or kernel launch failed         */
+  MUONBP_E_STATE = 6    /* context poisoned by an earlier MUONBP_E_HIP        */
+} muonbp_status;
+
+typedef enum { MUONBP_F32 = 0, MUONBP_BF16 = 1 } muonbp_dtype;
+
+/* One weight matrix W (rows x cols) and its shard grid (Sec. 3, "How blocks
+ * align with model-parallel shards"): block (i, j) holds rows
+ * [i*rows/grid_rows, (i+1)*rows/grid_rows) and columns
+ * [j*cols/grid_cols, (j+1)*cols/grid_cols).  grid_rows must divide rows and
+ * grid_cols must divide cols (MUONBP_E_SHAPE otherwise). */
+typedef struct {
+  int64_t rows, cols;
+  int32_t grid_rows, grid_cols;
+} muonbp_matrix;
+
+/* Options.  Defaults (muonbp_options_default) follow Algorithm 2:
+ * K = 5, (a, b, c) = (2, -1.5, 0.5), eps = 1e-7, no Nesterov, no RMS scaling,
+ * bf16 params, momentum and NS operands. */
+typedef struct {
+  int32_t ns_steps;         /* K >= 0, Newton-Schulz iterations (Alg. 2)       */
+  float a, b, c;            /* quintic coefficients (Alg. 2)                   */
+  float eps;                /* X <- G / (||G||_F + eps) (Alg. 2)               */
+  int32_t nesterov;         /* 1: NS input is G + mu*M instead of M (not in
+                               the paper; off by default)                      */
+  int32_t scale_mode;       /* 0: U as is (Alg. 1); 1: U * rms_beta *
+                               sqrt(max(p, q)), p x q = block shape on block
+                               steps, matrix shape on full steps (Sec. 3.2,
+                               "AdamW learning rate transfer")                 */
+  float rms_beta;           /* beta of scale_mode 1                            */
+  muonbp_dtype param_dtype; /* dtype of params and grads                       */
+  muonbp_dtype state_dtype; /* dtype of the momentum buffer                    */
+  muonbp_dtype ns_dtype;    /* dtype of NS operands (fp32 accumulate always)   */
+} muonbp_options;
+
+/* Fill *opt with the defaults above.  NULL is ignored. */
+void muonbp_options_default(muonbp_options* opt);
+
+/* Create a context for n_mats matrices (Algorithm 1 setup).
+ *  mats        host array of n_mats shapes and grids (copied).
+ *  period      P >= 1; 0 means P = infinity (BlockMuon: never a full step).
+ *  lr_block    eta_block, used on block steps (Sec. 3.2).
+ *  lr_full     eta_full, used on full steps (Sec. 3.2).
+ *  momentum    mu in M_t = mu M_{t-1} + G_t (eq. NTR).
+ *  weight_decay lambda: X <- X - eta_t (lambda X + s U) (decoupled).
+ *  opt         NULL for defaults.
+ *  hip_stream  hipStream_t to enqueue on (NULL = the null stream).
+ *  out         receives the context; *out is NULL on error.
+ * Allocates the momentum buffers (zeroed, Algorithm 1's M_{-1} = 0), the NS
+ * workspace and the plan tables on the current device; enqueues no compute.
+ * Errors: E_INVALID, E_SHAPE, E_DTYPE (before any HIP call), E_NOMEM, E_HIP. */
+muonbp_status muonbp_create(const muonbp_matrix* mats, int32_t n_mats,
+                            int64_t period, float lr_block, float lr_full,
+                            float momentum, float weight_decay,
+                            const muonbp_options* opt, void* hip_stream,
+                            muonbp_ctx** out);
+
+/* One iteration t = step of Algorithm 1 for every matrix.
+ *  params  host array of n_mats device pointers (param_dtype, rows x cols),
+ *          updated in place.
+ *  grads   host array of n_mats device pointers (param_dtype), read only.
+ *  step    t >= 0.  Full step iff period > 0 and step % period == 0.
+ * Enqueues: momentum (+ per-segment sum of squares), per-unit scale,
+ * operand pack, K x (Gram, polynomial, apply) grouped MFMA launches, update.
+ * Errors: E_INVALID (NULL ctx/arrays/pointers, step < 0), E_STATE, E_HIP. */
+muonbp_status muonbp_step(muonbp_ctx* ctx, void* const* params,
+                          const void* const* grads, int64_t step);
+
+/* Change eta_block and eta_full for later steps (learning-rate schedules). */
+muonbp_status muonbp_set_lr(muonbp_ctx* ctx, float lr_block, float lr_full);
+
+/* Change the stream used by later calls. */
+muonbp_status muonbp_set_stream(muonbp_ctx* ctx, void* hip_stream);
+
+/* Copy matrix `mat`'s momentum (state_dtype, rows x cols) to / from device
+ * memory `dst` / `src` (checkpoint and resume).  Asynchronous on the stream. */
+muonbp_status muonbp_get_momentum(muonbp_ctx* ctx, int32_t mat, void* dst);
+muonbp_status muonbp_set_momentum(muonbp_ctx* ctx, int32_t mat, const void* src);
+
+/* Copy the orthogonalized update U_t of matrix `mat` from the last step
+ * (ns_dtype, rows x cols, before RMS scaling) to device memory `dst`.
+ * E_STATE if no step has run yet. */
+muonbp_status muonbp_get_update(muonbp_ctx* ctx, int32_t mat, void* dst);
+
+/* Wait for all work enqueued by this context. */
+muonbp_status muonbp_synchronize(muonbp_ctx* ctx);
+
+/* Static description of one of the two plans (full = 0: block plan, 1: full
+ * plan).  Host-only; makes no HIP call. */
+typedef struct {
+  int64_t n_problems;      /* orthogonalized units (blocks or matrices)     */
+  int64_t n_elements;      /* parameters covered                            */
+  int64_t gemm_tiles[3];   /* workgroup tiles per NS iteration: Gram, poly,
+                              apply                                         */
+  double ns_flops;         /* algorithmic NS flops per step: per S x L unit
+                              and iteration S(S+1)L + S^2(S+1) + 2S^2 L
+                              (symmetric products counted once)             */
+  double ns_dense_flops;   /* Sec. 2.2 cost 2K(2 L S^2 + S^3), S <= L        */
+  double elementwise_bytes;/* algorithmic HBM bytes of the non-NS kernels    */
+  int64_t workspace_bytes; /* NS workspace this plan needs                  */
+} muonbp_plan_info;
+
+/* Plan description for a set of matrices without creating a context
+ * (E_INVALID / E_SHAPE / E_DTYPE as muonbp_create). */
+muonbp_status muonbp_describe_plan(const muonbp_matrix* mats, int32_t n_mats,
+                                   const muonbp_options* opt, int32_t full,
+                                   muonbp_plan_info* out);
+
+/* Per-kernel timing.  While enabled, every launch of the context is
+ * bracketed by HIP events on its stream; muonbp_profile_read synchronises,
+ * accumulates the elapsed times per kernel kind and resets the records.
+ * Kinds: 0 momentum, 1 scale, 2 pack, 3 gram, 4 poly, 5 apply, 6 update. */
+#define MUONBP_N_KERNEL_KINDS 7
+typedef struct {
+  double ms[MUONBP_N_KERNEL_KINDS];       /* summed kernel time             */
+  int64_t launches[MUONBP_N_KERNEL_KINDS];
+} muonbp_profile;
+
+muonbp_status muonbp_profile_enable(muonbp_ctx* ctx, int32_t enable);
+muonbp_status muonbp_profile_read(muonbp_ctx* ctx, muonbp_profile* out);
+
+/* Static text for a status code. */
+const char* muonbp_status_string(muonbp_status s);
+
+/* Detail of the last error on ctx ("" if none; static text if ctx is NULL).
+ * Owned by the context, valid until its next call. */
+const char* muonbp_last_error(const muonbp_ctx* ctx);
+
+/* Free everything the context owns (waits for its stream first).
+ * NULL is a no-op. */
+void muonbp_destroy(muonbp_ctx* ctx);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MUONBP_H */

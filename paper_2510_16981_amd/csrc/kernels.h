@@ -1,0 +1,43 @@
+// Launchers of the MuonBP HIP kernels (gfx950).  Each returns the launch
+// status; tables are device pointers built by the planner.
+#pragma once
+#include <hip/hip_runtime_api.h>
+
+#include "device_types.h"
+
+namespace muonbp {
+
+enum class DType { F32 = 0, BF16 = 1 };
+
+// M <- mu M + G over every block segment (eq. NTR); partials[seg] = sum of
+// squares of the NS input of that segment (M, or G + mu M with Nesterov).
+hipError_t launch_momentum(DType grad_t, DType mom_t, bool vec, int n_segs,
+                           const SegDesc* segs, const BlockDesc* blocks,
+                           const MatPtrs* mats, void* mom, float mu,
+                           int nesterov, float* partials, hipStream_t s);
+
+// scales[p] = 1 / (sqrt(sum of its partials) + eps)  (Algorithm 2, first line).
+hipError_t launch_scale(int n_probs, const ScaleDesc* sd, const float* partials,
+                        float* scales, float eps, hipStream_t s);
+
+// Z0 = s_p Y_p written straight and transposed into the NS workspace.
+hipError_t launch_pack(DType mom_t, DType grad_t, DType ns_t, int n_tiles,
+                       const TileRef* tiles, const PackDesc* pd,
+                       const MatPtrs* mats, const void* mom,
+                       const float* scales, float mu, int nesterov,
+                       hipStream_t s);
+
+// Grouped C = alpha X Y^T + beta D (+ transposed copy) over a tile list.
+// sym: problems are symmetric, the list holds upper tiles and the mirror
+// write (Ct = C) is skipped on diagonal tiles.
+hipError_t launch_ns_gemm(DType ns_t, int n_tiles, const GemmDesc* probs,
+                          const TileRef* tiles, float alpha, float beta,
+                          int sym, hipStream_t s);
+
+// X <- X (1 - eta lambda) - eta s_b U_b over every block segment.
+hipError_t launch_update(DType param_t, DType ns_t, bool vec, int n_segs,
+                         const SegDesc* segs, const BlockDesc* blocks,
+                         const MatPtrs* mats, const UpdDesc* upd, float eta,
+                         float lambda, hipStream_t s);
+
+}  // namespace muonbp

@@ -1,0 +1,643 @@
+// C ABI of the MuonBP optimizer step (declared in include/muonbp.h).
+//
+// The host side of Algorithm 1 (Sec. 3.2): it owns the momentum buffers and
+// the NS workspace, picks the block or the full plan by step mod P, and
+// enqueues the kernels of kernels.hip on the caller's stream.
+#include <hip/hip_runtime_api.h>
+
+#include <cmath>
+#include <cstring>
+#include <new>
+#include <string>
+#include <utility>
+#include <vector>
+
+#include "../../include/muonbp.h"
+#include "kernels.h"
+#include "plan.h"
+
+using namespace muonbp;
+
+namespace {
+
+constexpr int kPtrRing = 8;  // staging slots for per-step pointer tables
+
+size_t dtype_size(muonbp_dtype d) { return d == MUONBP_F32 ? 4 : 2; }
+DType dt(muonbp_dtype d) { return d == MUONBP_F32 ? DType::F32 : DType::BF16; }
+bool dtype_ok(muonbp_dtype d) { return d == MUONBP_F32 || d == MUONBP_BF16; }
+
+struct PlanDev {
+  ScaleDesc* scale = nullptr;
+  PackDesc* pack = nullptr;
+  TileRef* pack_tiles = nullptr;
+  GemmDesc* gram[2] = {nullptr, nullptr};
+  GemmDesc* poly = nullptr;
+  GemmDesc* apply[2] = {nullptr, nullptr};
+  TileRef* gram_tiles = nullptr;
+  TileRef* poly_tiles = nullptr;
+  TileRef* apply_tiles = nullptr;
+  UpdDesc* upd = nullptr;
+  std::vector<UpdDesc> upd_host;  // for muonbp_get_update
+};
+
+struct ProfRec {
+  int kind;
+  hipEvent_t start, stop;
+};
+
+}  // namespace
+
+struct muonbp_ctx {
+  Layout lay;
+  muonbp_options opt{};
+  int64_t period = 0;
+  float lr_block = 0, lr_full = 0, mu = 0, wd = 0;
+  hipStream_t stream = nullptr;
+  int device = 0;
+
+  void* mom = nullptr;
+  void* ws = nullptr;
+  float* partials = nullptr;
+  float* scales = nullptr;
+  SegDesc* segs = nullptr;
+  BlockDesc* blocks = nullptr;
+  PlanDev pd[2];
+  std::vector<void*> allocs;
+
+  MatPtrs* ptr_dev[kPtrRing] = {};
+  MatPtrs* ptr_host[kPtrRing] = {};  // pinned
+  hipEvent_t ptr_ev[kPtrRing] = {};
+  bool ptr_ev_used[kPtrRing] = {};
+  int ptr_slot = -1;
+  std::vector<MatPtrs> last_ptrs;
+  bool ptrs_valid = false;
+
+  bool vec_layout = false;
+  int last_plan = -1;
+  bool poisoned = false;
+  std::string err;
+
+  bool prof = false;
+  std::vector<ProfRec> prof_recs;
+  std::vector<hipEvent_t> ev_pool;
+  double prof_ms[MUONBP_N_KERNEL_KINDS] = {};
+  int64_t prof_n[MUONBP_N_KERNEL_KINDS] = {};
+};
+
+namespace {
+
+muonbp_status fail(muonbp_ctx* c, muonbp_status s, const std::string& msg) {
+  if (c) c->err = msg;
+  return s;
+}
+
+muonbp_status hip_fail(muonbp_ctx* c, hipError_t e, const char* what) {
+  if (c) {
+    c->poisoned = true;
+    c->err = std::string(what) + ": " + hipGetErrorString(e);
+  }
+  return MUONBP_E_HIP;
+}
+
+std::string validate_opts(const muonbp_options& o) {
+  if (o.ns_steps < 0 || o.ns_steps > 1000) return "ns_steps must be in [0, 1000]";
+  if (!(o.eps >= 0.f) || !std::isfinite(o.eps)) return "eps must be finite and >= 0";
+  if (!std::isfinite(o.a) || !std::isfinite(o.b) || !std::isfinite(o.c))
+    return "NS coefficients must be finite";
+  if (o.nesterov != 0 && o.nesterov != 1) return "nesterov must be 0 or 1";
+  if (o.scale_mode != 0 && o.scale_mode != 1) return "scale_mode must be 0 or 1";
+  if (!std::isfinite(o.rms_beta)) return "rms_beta must be finite";
+  return "";
+}
+
+template <typename T>
+hipError_t upload(muonbp_ctx* c, T** dst, const std::vector<T>& src) {
+  *dst = nullptr;
+  if (src.empty()) return hipSuccess;
+  void* p = nullptr;
+  hipError_t e = hipMalloc(&p, src.size() * sizeof(T));
+  if (e != hipSuccess) return e;
+  c->allocs.push_back(p);
+  *dst = static_cast<T*>(p);
+  return hipMemcpy(p, src.data(), src.size() * sizeof(T), hipMemcpyHostToDevice);
+}
+
+hipError_t dev_alloc(muonbp_ctx* c, void** p, size_t bytes) {
+  *p = nullptr;
+  if (bytes == 0) bytes = 256;
+  hipError_t e = hipMalloc(p, bytes);
+  if (e == hipSuccess) c->allocs.push_back(*p);
+  return e;
+}
+
+// Device tables of one plan (needs c->ws allocated).
+hipError_t build_plan_tables(muonbp_ctx* c, int full) {
+  const Plan& plan = c->lay.plan[full];
+  PlanDev& pd = c->pd[full];
+  const size_t es = dtype_size(c->opt.ns_dtype);
+  char* ws = static_cast<char*>(c->ws);
+  auto at = [&](int64_t off) { return static_cast<void*>(ws + off * int64_t(es)); };
+  const muonbp_options& o = c->opt;
+
+  std::vector<ScaleDesc> sd;
+  std::vector<PackDesc> pk;
+  std::vector<GemmDesc> gram[2], poly, apply[2];
+  for (const Problem& p : plan.probs) {
+    sd.push_back(ScaleDesc{p.seg_begin, p.seg_end});
+    const MatrixShape& m = c->lay.mats[p.mat];
+    PackDesc d{};
+    d.in_mat_off = p.row0 * m.cols + p.col0;
+    d.mom_off = c->lay.mat_off[p.mat] + d.in_mat_off;
+    d.ld = m.cols;
+    d.mat = p.mat;
+    d.rows = int32_t(p.rows);
+    d.cols = int32_t(p.cols);
+    d.tiles_c = int32_t((p.cols + kPackTile - 1) / kPackTile);
+    // Z = Y (S = rows) or Y^T (S = cols); Z^T the other way round.
+    if (!p.trans) {
+      d.dst_s = at(p.off_z[0]);
+      d.ld_s = p.Lp;
+      d.dst_t = at(p.off_zt[0]);
+      d.ld_t = p.Sp;
+    } else {
+      d.dst_s = at(p.off_zt[0]);
+      d.ld_s = p.Sp;
+      d.dst_t = at(p.off_z[0]);
+      d.ld_t = p.Lp;
+    }
+    pk.push_back(d);
+    const int32_t S = int32_t(p.S), Lr = int32_t(p.L), Sp = int32_t(p.Sp), Lp = int32_t(p.Lp);
+    for (int q = 0; q < 2; ++q) {
+      // A = Z_q Z_q^T
+      gram[q].push_back(GemmDesc{at(p.off_z[q]), at(p.off_z[q]), nullptr, at(p.off_a), at(p.off_a),
+                                 S, S, Lr, Lp, Lp, 0, Sp, Sp});
+      // Z_{1-q} = a Z_q + B Z_q, also stored transposed.
+      apply[q].push_back(GemmDesc{at(p.off_b), at(p.off_zt[q]), at(p.off_z[q]), at(p.off_z[1 - q]),
+                                  at(p.off_zt[1 - q]), S, Lr, S, Sp, Sp, Lp, Lp, Sp});
+    }
+    // B = c A A^T + b A  (A symmetric)
+    poly.push_back(GemmDesc{at(p.off_a), at(p.off_a), at(p.off_a), at(p.off_b), at(p.off_b), S, S, S,
+                            Sp, Sp, Sp, Sp, Sp});
+  }
+  // Update table: U of every block after K iterations (buffer K mod 2).
+  const int fin = o.ns_steps & 1;
+  pd.upd_host.clear();
+  for (const Problem& p : plan.probs) {
+    const MatrixShape& m = c->lay.mats[p.mat];
+    float s = 1.f;
+    if (o.scale_mode == 1) s = o.rms_beta * std::sqrt(float(std::max(p.rows, p.cols)));
+    const int64_t base = p.trans ? p.off_zt[fin] : p.off_z[fin];
+    const int64_t ldu = p.trans ? p.Sp : p.Lp;
+    (void)m;
+    for (int32_t b = p.first_block; b < p.first_block + p.n_blocks; ++b) {
+      const BlockPlan& bp = c->lay.blocks[b];
+      const int64_t off = base + (bp.row0 - p.row0) * ldu + (bp.col0 - p.col0);
+      pd.upd_host.push_back(UpdDesc{at(off), ldu, s, 0});
+    }
+  }
+  hipError_t e;
+  if ((e = upload(c, &pd.scale, sd)) != hipSuccess) return e;
+  if ((e = upload(c, &pd.pack, pk)) != hipSuccess) return e;
+  if ((e = upload(c, &pd.pack_tiles, plan.pack_tiles)) != hipSuccess) return e;
+  for (int q = 0; q < 2; ++q) {
+    if ((e = upload(c, &pd.gram[q], gram[q])) != hipSuccess) return e;
+    if ((e = upload(c, &pd.apply[q], apply[q])) != hipSuccess) return e;
+  }
+  if ((e = upload(c, &pd.poly, poly)) != hipSuccess) return e;
+  if ((e = upload(c, &pd.gram_tiles, plan.gram_tiles)) != hipSuccess) return e;
+  if ((e = upload(c, &pd.poly_tiles, plan.poly_tiles)) != hipSuccess) return e;
+  if ((e = upload(c, &pd.apply_tiles, plan.apply_tiles)) != hipSuccess) return e;
+  if ((e = upload(c, &pd.upd, pd.upd_host)) != hipSuccess) return e;
+  return hipSuccess;
+}
+
+void free_ctx(muonbp_ctx* c) {
+  if (!c) return;
+  for (void* p : c->allocs) (void)hipFree(p);
+  for (int i = 0; i < kPtrRing; ++i) {
+    if (c->ptr_host[i]) (void)hipHostFree(c->ptr_host[i]);
+    if (c->ptr_ev[i]) (void)hipEventDestroy(c->ptr_ev[i]);
+  }
+  for (auto& r : c->prof_recs) {
+    (void)hipEventDestroy(r.start);
+    (void)hipEventDestroy(r.stop);
+  }
+  for (hipEvent_t e : c->ev_pool) (void)hipEventDestroy(e);
+  delete c;
+}
+
+std::string check_mats(const muonbp_matrix* mats, int32_t n_mats, std::vector<MatrixShape>* out) {
+  if (!mats) return "mats is NULL";
+  if (n_mats <= 0) return "n_mats must be > 0";
+  out->clear();
+  for (int32_t i = 0; i < n_mats; ++i)
+    out->push_back(MatrixShape{mats[i].rows, mats[i].cols, mats[i].grid_rows, mats[i].grid_cols});
+  return "";
+}
+
+// Profiling helpers: bracket a launch with events when enabled.
+hipEvent_t take_event(muonbp_ctx* c) {
+  if (!c->ev_pool.empty()) {
+    hipEvent_t e = c->ev_pool.back();
+    c->ev_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+template <typename F>
+hipError_t timed(muonbp_ctx* c, int kind, F&& launch) {
+  if (!c->prof) return launch();
+  hipEvent_t a = take_event(c), b = take_event(c);
+  if (!a || !b) return hipErrorOutOfMemory;
+  hipError_t e = hipEventRecord(a, c->stream);
+  if (e != hipSuccess) return e;
+  e = launch();
+  if (e != hipSuccess) return e;
+  e = hipEventRecord(b, c->stream);
+  if (e != hipSuccess) return e;
+  c->prof_recs.push_back(ProfRec{kind, a, b});
+  return hipSuccess;
+}
+
+// Make the device pointer table for this step current (uploads only when
+// the caller's pointers changed since the last step).
+hipError_t stage_pointers(muonbp_ctx* c, void* const* params, const void* const* grads) {
+  const size_t n = c->lay.mats.size();
+  bool same = c->ptrs_valid;
+  for (size_t i = 0; same && i < n; ++i)
+    same = c->last_ptrs[i].param == params[i] && c->last_ptrs[i].grad == grads[i];
+  if (same) return hipSuccess;
+  const int slot = (c->ptr_slot + 1) % kPtrRing;
+  hipError_t e;
+  if (c->ptr_ev_used[slot] && (e = hipEventSynchronize(c->ptr_ev[slot])) != hipSuccess) return e;
+  for (size_t i = 0; i < n; ++i) c->ptr_host[slot][i] = MatPtrs{params[i], grads[i]};
+  e = hipMemcpyAsync(c->ptr_dev[slot], c->ptr_host[slot], n * sizeof(MatPtrs), hipMemcpyHostToDevice,
+                     c->stream);
+  if (e != hipSuccess) return e;
+  if ((e = hipEventRecord(c->ptr_ev[slot], c->stream)) != hipSuccess) return e;
+  c->ptr_ev_used[slot] = true;
+  c->ptr_slot = slot;
+  c->last_ptrs.assign(c->ptr_host[slot], c->ptr_host[slot] + n);
+  c->ptrs_valid = true;
+  return hipSuccess;
+}
+
+}  // namespace
+
+extern "C" {
+
+void muonbp_options_default(muonbp_options* o) {
+  if (!o) return;
+  std::memset(o, 0, sizeof(*o));
+  o->ns_steps = 5;
+  o->a = 2.0f;
+  o->b = -1.5f;
+  o->c = 0.5f;
+  o->eps = 1e-7f;
+  o->nesterov = 0;
+  o->scale_mode = 0;
+  o->rms_beta = 1.0f;
+  o->param_dtype = MUONBP_BF16;
+  o->state_dtype = MUONBP_BF16;
+  o->ns_dtype = MUONBP_BF16;
+}
+
+const char* muonbp_status_string(muonbp_status s) {
+  switch (s) {
+    case MUONBP_OK: return "ok";
+    case MUONBP_E_INVALID: return "invalid argument";
+    case MUONBP_E_SHAPE: return "invalid shape or grid";
+    case MUONBP_E_DTYPE: return "unsupported dtype";
+    case MUONBP_E_NOMEM: return "out of memory";
+    case MUONBP_E_HIP: return "HIP error";
+    case MUONBP_E_STATE: return "context unusable after an earlier HIP error";
+  }
+  return "unknown status";
+}
+
+const char* muonbp_last_error(const muonbp_ctx* c) {
+  if (!c) return "no context";
+  return c->err.c_str();
+}
+
+muonbp_status muonbp_describe_plan(const muonbp_matrix* mats, int32_t n_mats,
+                                   const muonbp_options* opt, int32_t full,
+                                   muonbp_plan_info* out) {
+  if (!out || (full != 0 && full != 1)) return MUONBP_E_INVALID;
+  muonbp_options o;
+  muonbp_options_default(&o);
+  if (opt) o = *opt;
+  if (!validate_opts(o).empty()) return MUONBP_E_INVALID;
+  if (!dtype_ok(o.param_dtype) || !dtype_ok(o.state_dtype) || !dtype_ok(o.ns_dtype))
+    return MUONBP_E_DTYPE;
+  std::vector<MatrixShape> shapes;
+  if (!check_mats(mats, n_mats, &shapes).empty()) return MUONBP_E_INVALID;
+  Layout lay;
+  bool shape_err = false;
+  try {
+    if (!build_layout(shapes.data(), n_mats, int(dtype_size(o.ns_dtype)), o.ns_steps, &lay,
+                      &shape_err)
+             .empty())
+      return shape_err ? MUONBP_E_SHAPE : MUONBP_E_INVALID;
+  } catch (const std::bad_alloc&) {
+    return MUONBP_E_NOMEM;
+  }
+  const Plan& p = lay.plan[full];
+  std::memset(out, 0, sizeof(*out));
+  out->n_problems = int64_t(p.probs.size());
+  out->n_elements = lay.total_elems;
+  out->gemm_tiles[0] = int64_t(p.gram_tiles.size());
+  out->gemm_tiles[1] = int64_t(p.poly_tiles.size());
+  out->gemm_tiles[2] = int64_t(p.apply_tiles.size());
+  out->ns_flops = p.ns_flops;
+  out->ns_dense_flops = p.ns_dense_flops;
+  const double pb = double(dtype_size(o.param_dtype)), sb = double(dtype_size(o.state_dtype)),
+               nb = double(dtype_size(o.ns_dtype));
+  // momentum: read G, M, write M; update: read X, U, write X.
+  out->elementwise_bytes = double(lay.total_elems) * ((pb + 2 * sb) + (2 * pb + nb));
+  out->workspace_bytes = p.ws_elems * int64_t(nb);
+  return MUONBP_OK;
+}
+
+muonbp_status muonbp_create(const muonbp_matrix* mats, int32_t n_mats, int64_t period,
+                            float lr_block, float lr_full, float momentum, float weight_decay,
+                            const muonbp_options* opt, void* hip_stream, muonbp_ctx** out) {
+  if (!out) return MUONBP_E_INVALID;
+  *out = nullptr;
+  muonbp_options o;
+  muonbp_options_default(&o);
+  if (opt) o = *opt;
+  if (period < 0) return MUONBP_E_INVALID;
+  if (!std::isfinite(lr_block) || !std::isfinite(lr_full) || !std::isfinite(momentum) ||
+      !std::isfinite(weight_decay))
+    return MUONBP_E_INVALID;
+  if (!validate_opts(o).empty()) return MUONBP_E_INVALID;
+  if (!dtype_ok(o.param_dtype) || !dtype_ok(o.state_dtype) || !dtype_ok(o.ns_dtype))
+    return MUONBP_E_DTYPE;
+  std::vector<MatrixShape> shapes;
+  if (!check_mats(mats, n_mats, &shapes).empty()) return MUONBP_E_INVALID;
+
+  muonbp_ctx* c = new (std::nothrow) muonbp_ctx();
+  if (!c) return MUONBP_E_NOMEM;
+  try {
+    bool shape_err = false;
+    std::string msg = build_layout(shapes.data(), n_mats, int(dtype_size(o.ns_dtype)), o.ns_steps,
+                                   &c->lay, &shape_err);
+    if (!msg.empty()) {
+      free_ctx(c);
+      return shape_err ? MUONBP_E_SHAPE : MUONBP_E_INVALID;
+    }
+  } catch (const std::bad_alloc&) {
+    free_ctx(c);
+    return MUONBP_E_NOMEM;
+  }
+  c->opt = o;
+  c->period = period;
+  c->lr_block = lr_block;
+  c->lr_full = lr_full;
+  c->mu = momentum;
+  c->wd = weight_decay;
+  c->stream = static_cast<hipStream_t>(hip_stream);
+
+  // 16-byte vector paths need 8-element aligned windows and strides.
+  bool vec = true;
+  for (const BlockPlan& b : c->lay.blocks) {
+    const MatrixShape& m = c->lay.mats[b.mat];
+    vec = vec && b.cols % 8 == 0 && b.col0 % 8 == 0 && m.cols % 8 == 0 && c->lay.mat_off[b.mat] % 8 == 0;
+  }
+  c->vec_layout = vec;
+
+  hipError_t e = hipGetDevice(&c->device);
+  if (e != hipSuccess) {
+    hip_fail(c, e, "hipGetDevice");
+    free_ctx(c);
+    return MUONBP_E_HIP;
+  }
+  auto bail = [&](hipError_t err, const char* what) {
+    const muonbp_status st = (err == hipErrorOutOfMemory) ? MUONBP_E_NOMEM : MUONBP_E_HIP;
+    free_ctx(c);
+    (void)what;
+    return st;
+  };
+  const size_t sb = dtype_size(o.state_dtype), nb = dtype_size(o.ns_dtype);
+  const int64_t ws_elems = std::max(c->lay.plan[0].ws_elems, c->lay.plan[1].ws_elems);
+  const size_t n_probs = std::max(c->lay.plan[0].probs.size(), c->lay.plan[1].probs.size());
+  if ((e = dev_alloc(c, &c->mom, size_t(c->lay.total_elems) * sb)) != hipSuccess) return bail(e, "momentum");
+  if ((e = dev_alloc(c, &c->ws, size_t(ws_elems) * nb)) != hipSuccess) return bail(e, "workspace");
+  void* p = nullptr;
+  if ((e = dev_alloc(c, &p, c->lay.segs.size() * sizeof(float))) != hipSuccess) return bail(e, "partials");
+  c->partials = static_cast<float*>(p);
+  if ((e = dev_alloc(c, &p, n_probs * sizeof(float))) != hipSuccess) return bail(e, "scales");
+  c->scales = static_cast<float*>(p);
+  if ((e = upload(c, &c->segs, c->lay.segs)) != hipSuccess) return bail(e, "segments");
+  std::vector<BlockDesc> bd;
+  for (const BlockPlan& b : c->lay.blocks) {
+    const MatrixShape& m = c->lay.mats[b.mat];
+    BlockDesc d{};
+    d.in_mat_off = b.row0 * m.cols + b.col0;
+    d.mom_off = c->lay.mat_off[b.mat] + d.in_mat_off;
+    d.ld = m.cols;
+    d.mat = b.mat;
+    d.cols = int32_t(b.cols);
+    bd.push_back(d);
+  }
+  if ((e = upload(c, &c->blocks, bd)) != hipSuccess) return bail(e, "blocks");
+  for (int full = 0; full < 2; ++full)
+    if ((e = build_plan_tables(c, full)) != hipSuccess) return bail(e, "plan tables");
+  for (int i = 0; i < kPtrRing; ++i) {
+    if ((e = dev_alloc(c, &p, shapes.size() * sizeof(MatPtrs))) != hipSuccess) return bail(e, "pointer table");
+    c->ptr_dev[i] = static_cast<MatPtrs*>(p);
+    void* h = nullptr;
+    if ((e = hipHostMalloc(&h, shapes.size() * sizeof(MatPtrs), 0)) != hipSuccess) return bail(e, "pinned table");
+    c->ptr_host[i] = static_cast<MatPtrs*>(h);
+    if ((e = hipEventCreateWithFlags(&c->ptr_ev[i], hipEventDisableTiming)) != hipSuccess)
+      return bail(e, "event");
+  }
+  // Algorithm 1: M_{-1} = 0.
+  if ((e = hipMemset(c->mom, 0, size_t(c->lay.total_elems) * sb)) != hipSuccess) return bail(e, "memset");
+  if ((e = hipDeviceSynchronize()) != hipSuccess) return bail(e, "sync");
+  *out = c;
+  return MUONBP_OK;
+}
+
+muonbp_status muonbp_step(muonbp_ctx* c, void* const* params, const void* const* grads, int64_t step) {
+  if (!c) return MUONBP_E_INVALID;
+  if (c->poisoned) return fail(c, MUONBP_E_STATE, "context poisoned: " + c->err);
+  if (!params || !grads) return fail(c, MUONBP_E_INVALID, "params and grads must not be NULL");
+  if (step < 0) return fail(c, MUONBP_E_INVALID, "step must be >= 0");
+  const size_t n = c->lay.mats.size();
+  const size_t pb = dtype_size(c->opt.param_dtype);
+  bool aligned = c->vec_layout;
+  for (size_t i = 0; i < n; ++i) {
+    if (!params[i] || !grads[i]) return fail(c, MUONBP_E_INVALID, "NULL param or grad pointer");
+    if (reinterpret_cast<uintptr_t>(params[i]) % pb || reinterpret_cast<uintptr_t>(grads[i]) % pb)
+      return fail(c, MUONBP_E_INVALID, "param or grad pointer not element-aligned");
+    aligned = aligned && reinterpret_cast<uintptr_t>(params[i]) % 16 == 0 &&
+              reinterpret_cast<uintptr_t>(grads[i]) % 16 == 0;
+  }
+  hipError_t e = stage_pointers(c, params, grads);
+  if (e != hipSuccess) return hip_fail(c, e, "pointer upload");
+  const MatPtrs* mats = c->ptr_dev[c->ptr_slot];
+
+  // Algorithm 1: full orthogonalization iff t mod P = 0 (P = 0 means infinity).
+  const int full = (c->period > 0 && step % c->period == 0) ? 1 : 0;
+  const Plan& plan = c->lay.plan[full];
+  const PlanDev& pd = c->pd[full];
+  const muonbp_options& o = c->opt;
+  const DType tp = dt(o.param_dtype), tm = dt(o.state_dtype), tn = dt(o.ns_dtype);
+  const int nsegs = int(c->lay.segs.size());
+  const hipStream_t s = c->stream;
+
+  e = timed(c, 0, [&] {
+    return launch_momentum(tp, tm, aligned, nsegs, c->segs, c->blocks, mats, c->mom, c->mu,
+                           o.nesterov, c->partials, s);
+  });
+  if (e != hipSuccess) return hip_fail(c, e, "momentum");
+  e = timed(c, 1, [&] {
+    return launch_scale(int(plan.probs.size()), pd.scale, c->partials, c->scales, o.eps, s);
+  });
+  if (e != hipSuccess) return hip_fail(c, e, "scale");
+  e = timed(c, 2, [&] {
+    return launch_pack(tm, tp, tn, int(plan.pack_tiles.size()), pd.pack_tiles, pd.pack, mats, c->mom,
+                       c->scales, c->mu, o.nesterov, s);
+  });
+  if (e != hipSuccess) return hip_fail(c, e, "pack");
+  for (int k = 0; k < o.ns_steps; ++k) {
+    const int q = k & 1;
+    e = timed(c, 3, [&] {
+      return launch_ns_gemm(tn, int(plan.gram_tiles.size()), pd.gram[q], pd.gram_tiles, 1.f, 0.f, 1, s);
+    });
+    if (e != hipSuccess) return hip_fail(c, e, "gram");
+    e = timed(c, 4, [&] {
+      return launch_ns_gemm(tn, int(plan.poly_tiles.size()), pd.poly, pd.poly_tiles, o.c, o.b, 1, s);
+    });
+    if (e != hipSuccess) return hip_fail(c, e, "poly");
+    e = timed(c, 5, [&] {
+      return launch_ns_gemm(tn, int(plan.apply_tiles.size()), pd.apply[q], pd.apply_tiles, 1.f, o.a, 0, s);
+    });
+    if (e != hipSuccess) return hip_fail(c, e, "apply");
+  }
+  const float eta = full ? c->lr_full : c->lr_block;
+  bool upd_vec = aligned;
+  e = timed(c, 6, [&] {
+    return launch_update(tp, tn, upd_vec, nsegs, c->segs, c->blocks, mats, pd.upd, eta, c->wd, s);
+  });
+  if (e != hipSuccess) return hip_fail(c, e, "update");
+  c->last_plan = full;
+  return MUONBP_OK;
+}
+
+muonbp_status muonbp_set_lr(muonbp_ctx* c, float lr_block, float lr_full) {
+  if (!c) return MUONBP_E_INVALID;
+  if (!std::isfinite(lr_block) || !std::isfinite(lr_full))
+    return fail(c, MUONBP_E_INVALID, "learning rates must be finite");
+  c->lr_block = lr_block;
+  c->lr_full = lr_full;
+  return MUONBP_OK;
+}
+
+muonbp_status muonbp_set_stream(muonbp_ctx* c, void* hip_stream) {
+  if (!c) return MUONBP_E_INVALID;
+  if (c->poisoned) return fail(c, MUONBP_E_STATE, "context poisoned: " + c->err);
+  // Order the new stream after everything enqueued so far.
+  hipError_t e = hipStreamSynchronize(c->stream);
+  if (e != hipSuccess) return hip_fail(c, e, "hipStreamSynchronize");
+  c->stream = static_cast<hipStream_t>(hip_stream);
+  c->ptrs_valid = false;
+  return MUONBP_OK;
+}
+
+static muonbp_status momentum_copy(muonbp_ctx* c, int32_t mat, void* dst, const void* src) {
+  if (!c) return MUONBP_E_INVALID;
+  if (c->poisoned) return fail(c, MUONBP_E_STATE, "context poisoned: " + c->err);
+  if (mat < 0 || size_t(mat) >= c->lay.mats.size()) return fail(c, MUONBP_E_INVALID, "bad matrix index");
+  if (!dst && !src) return fail(c, MUONBP_E_INVALID, "NULL pointer");
+  const MatrixShape& m = c->lay.mats[mat];
+  const size_t sb = dtype_size(c->opt.state_dtype);
+  char* mom = static_cast<char*>(c->mom) + c->lay.mat_off[mat] * int64_t(sb);
+  const size_t bytes = size_t(m.rows * m.cols) * sb;
+  hipError_t e = dst ? hipMemcpyAsync(dst, mom, bytes, hipMemcpyDeviceToDevice, c->stream)
+                     : hipMemcpyAsync(mom, src, bytes, hipMemcpyDeviceToDevice, c->stream);
+  if (e != hipSuccess) return hip_fail(c, e, "momentum copy");
+  return MUONBP_OK;
+}
+
+muonbp_status muonbp_get_momentum(muonbp_ctx* c, int32_t mat, void* dst) {
+  if (c && !dst) return fail(c, MUONBP_E_INVALID, "dst is NULL");
+  return momentum_copy(c, mat, dst, nullptr);
+}
+
+muonbp_status muonbp_set_momentum(muonbp_ctx* c, int32_t mat, const void* src) {
+  if (c && !src) return fail(c, MUONBP_E_INVALID, "src is NULL");
+  return momentum_copy(c, mat, nullptr, src);
+}
+
+muonbp_status muonbp_get_update(muonbp_ctx* c, int32_t mat, void* dst) {
+  if (!c) return MUONBP_E_INVALID;
+  if (c->poisoned) return fail(c, MUONBP_E_STATE, "context poisoned: " + c->err);
+  if (mat < 0 || size_t(mat) >= c->lay.mats.size()) return fail(c, MUONBP_E_INVALID, "bad matrix index");
+  if (!dst) return fail(c, MUONBP_E_INVALID, "dst is NULL");
+  if (c->last_plan < 0) return fail(c, MUONBP_E_STATE, "no step has run yet");
+  const MatrixShape& m = c->lay.mats[mat];
+  const size_t es = dtype_size(c->opt.ns_dtype);
+  const PlanDev& pd = c->pd[c->last_plan];
+  for (size_t b = 0; b < c->lay.blocks.size(); ++b) {
+    const BlockPlan& bp = c->lay.blocks[b];
+    if (bp.mat != mat) continue;
+    const UpdDesc& u = pd.upd_host[b];
+    char* d = static_cast<char*>(dst) + (bp.row0 * m.cols + bp.col0) * int64_t(es);
+    hipError_t e = hipMemcpy2DAsync(d, size_t(m.cols) * es, u.u, size_t(u.ldu) * es, size_t(bp.cols) * es,
+                                    size_t(bp.rows), hipMemcpyDeviceToDevice, c->stream);
+    if (e != hipSuccess) return hip_fail(c, e, "update copy");
+  }
+  return MUONBP_OK;
+}
+
+muonbp_status muonbp_synchronize(muonbp_ctx* c) {
+  if (!c) return MUONBP_E_INVALID;
+  if (c->poisoned) return fail(c, MUONBP_E_STATE, "context poisoned: " + c->err);
+  hipError_t e = hipStreamSynchronize(c->stream);
+  if (e != hipSuccess) return hip_fail(c, e, "hipStreamSynchronize");
+  return MUONBP_OK;
+}
+
+muonbp_status muonbp_profile_enable(muonbp_ctx* c, int32_t enable) {
+  if (!c) return MUONBP_E_INVALID;
+  c->prof = enable != 0;
+  return MUONBP_OK;
+}
+
+muonbp_status muonbp_profile_read(muonbp_ctx* c, muonbp_profile* out) {
+  if (!c || !out) return MUONBP_E_INVALID;
+  if (c->poisoned) return fail(c, MUONBP_E_STATE, "context poisoned: " + c->err);
+  for (ProfRec& r : c->prof_recs) {
+    hipError_t e = hipEventSynchronize(r.stop);
+    if (e != hipSuccess) return hip_fail(c, e, "hipEventSynchronize");
+    float ms = 0.f;
+    e = hipEventElapsedTime(&ms, r.start, r.stop);
+    if (e != hipSuccess) return hip_fail(c, e, "hipEventElapsedTime");
+    c->prof_ms[r.kind] += ms;
+    c->prof_n[r.kind] += 1;
+    c->ev_pool.push_back(r.start);
+    c->ev_pool.push_back(r.stop);
+  }
+  c->prof_recs.clear();
+  for (int k = 0; k < MUONBP_N_KERNEL_KINDS; ++k) {
+    out->ms[k] = c->prof_ms[k];
+    out->launches[k] = c->prof_n[k];
+    c->prof_ms[k] = 0;
+    c->prof_n[k] = 0;
+  }
+  return MUONBP_OK;
+}
+
+void muonbp_destroy(muonbp_ctx* c) {
+  if (!c) return;
+  (void)hipStreamSynchronize(c->stream);
+  free_ctx(c);
+}
+
+}  // extern "C"

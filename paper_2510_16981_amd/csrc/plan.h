@@ -1,0 +1,77 @@
+// Host-side planner of the MuonBP step: block table, elementwise segments,
+// the two orthogonalization plans (blocks / whole matrices) with their NS
+// workspace layout and the tile lists of every grouped launch.  Pure C++ with
+// no HIP call, so it runs (and is tested) without a GPU.
+#pragma once
+#include <stdint.h>
+
+#include <string>
+#include <vector>
+
+#include "device_types.h"
+
+namespace muonbp {
+
+constexpr int kGemmTile = 128;          // square workgroup tile of the NS GEMMs
+constexpr int kPackTile = 64;           // square tile of the pack kernel
+constexpr int64_t kSegTarget = 16384;   // elements per elementwise workgroup
+constexpr int64_t kWsAlignBytes = 256;  // alignment of every workspace buffer
+
+struct MatrixShape {
+  int64_t rows, cols;
+  int32_t grid_rows, grid_cols;
+};
+
+struct BlockPlan {
+  int32_t mat;
+  int64_t row0, col0, rows, cols;  // window inside the matrix
+  int32_t seg_begin, seg_end;
+};
+
+// One orthogonalized unit: a block (block plan) or a whole matrix (full
+// plan).  NS runs on the S x L matrix Z = Y (or Y^T when rows > cols).
+struct Problem {
+  int32_t mat;
+  int64_t row0, col0, rows, cols;
+  bool trans;
+  int64_t S, L;    // S = min(rows, cols), L = max(rows, cols)
+  int64_t Sp, Lp;  // leading dimensions (multiples of 8 elements)
+  // Element offsets inside the NS workspace arena.
+  int64_t off_z[2];   // Z (S x Lp), ping-pong
+  int64_t off_zt[2];  // Z^T (L x Sp), ping-pong
+  int64_t off_a;      // A = Z Z^T (S x Sp)
+  int64_t off_b;      // B = b A + c A^2 (S x Sp)
+  int32_t seg_begin, seg_end;
+  int32_t first_block, n_blocks;
+};
+
+struct Plan {
+  bool full = false;
+  std::vector<Problem> probs;
+  int64_t ws_elems = 0;
+  std::vector<TileRef> pack_tiles;
+  std::vector<TileRef> gram_tiles, poly_tiles, apply_tiles;
+  double ns_flops = 0, ns_dense_flops = 0;
+};
+
+struct Layout {
+  std::vector<MatrixShape> mats;
+  std::vector<int64_t> mat_off;  // element offset of each matrix (momentum arena)
+  std::vector<BlockPlan> blocks;
+  std::vector<SegDesc> segs;
+  int64_t total_elems = 0;
+  Plan plan[2];  // [0] block plan, [1] full plan
+};
+
+// Validates shapes and builds every table.  ns_elem_bytes sizes the
+// workspace alignment; ns_steps only feeds the flop counts.  Returns "" on
+// success, else a message (with *shape_error telling shape vs. argument).
+std::string build_layout(const MatrixShape* mats, int32_t n_mats,
+                         int ns_elem_bytes, int ns_steps, Layout* out,
+                         bool* shape_error);
+
+// Per-step flops of NS on one S x L unit for K iterations.
+double ns_unit_flops(int64_t S, int64_t L, int K);        // symmetric-aware
+double ns_unit_dense_flops(int64_t S, int64_t L, int K);  // Sec. 2.2 model
+
+}  // namespace muonbp

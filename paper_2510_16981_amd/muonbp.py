@@ -1,0 +1,240 @@
+"""ctypes binding of ``libmuonbp.so`` (C ABI in ``include/muonbp.h``).
+
+Argument marshalling only: every step of the optimizer runs in the HIP
+library.  torch supplies device memory (``data_ptr``) and the current HIP
+stream.  There is no fallback: if the library is missing, loading raises.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import List, Optional, Sequence, Tuple
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libmuonbp.so")
+
+F32, BF16 = 0, 1
+KERNEL_KINDS = ("momentum", "scale", "pack", "gram", "poly", "apply", "update")
+
+STATUS = {0: "MUONBP_OK", 1: "MUONBP_E_INVALID", 2: "MUONBP_E_SHAPE",
+          3: "MUONBP_E_DTYPE", 4: "MUONBP_E_NOMEM", 5: "MUONBP_E_HIP",
+          6: "MUONBP_E_STATE"}
+
+
+class MuonBPError(RuntimeError):
+    def __init__(self, status: int, detail: str = ""):
+        self.status = status
+        super().__init__(f"{STATUS.get(status, status)}: {detail}")
+
+
+class Matrix(ctypes.Structure):
+    _fields_ = [("rows", ctypes.c_int64), ("cols", ctypes.c_int64),
+                ("grid_rows", ctypes.c_int32), ("grid_cols", ctypes.c_int32)]
+
+
+class Options(ctypes.Structure):
+    _fields_ = [("ns_steps", ctypes.c_int32), ("a", ctypes.c_float),
+                ("b", ctypes.c_float), ("c", ctypes.c_float),
+                ("eps", ctypes.c_float), ("nesterov", ctypes.c_int32),
+                ("scale_mode", ctypes.c_int32), ("rms_beta", ctypes.c_float),
+                ("param_dtype", ctypes.c_int), ("state_dtype", ctypes.c_int),
+                ("ns_dtype", ctypes.c_int)]
+
+
+class PlanInfo(ctypes.Structure):
+    _fields_ = [("n_problems", ctypes.c_int64), ("n_elements", ctypes.c_int64),
+                ("gemm_tiles", ctypes.c_int64 * 3), ("ns_flops", ctypes.c_double),
+                ("ns_dense_flops", ctypes.c_double),
+                ("elementwise_bytes", ctypes.c_double),
+                ("workspace_bytes", ctypes.c_int64)]
+
+
+class Profile(ctypes.Structure):
+    _fields_ = [("ms", ctypes.c_double * 7), ("launches", ctypes.c_int64 * 7)]
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load the HIP library (raises when it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(
+            f"{path} is missing: build it with `python -m paper_2510_16981_amd.build`")
+    lib = ctypes.CDLL(path)
+    P, I32, I64, F = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float
+    sig = {
+        "muonbp_options_default": (None, [ctypes.POINTER(Options)]),
+        "muonbp_create": (ctypes.c_int, [ctypes.POINTER(Matrix), I32, I64, F, F, F, F,
+                                         ctypes.POINTER(Options), P, ctypes.POINTER(P)]),
+        "muonbp_step": (ctypes.c_int, [P, ctypes.POINTER(P), ctypes.POINTER(P), I64]),
+        "muonbp_set_lr": (ctypes.c_int, [P, F, F]),
+        "muonbp_set_stream": (ctypes.c_int, [P, P]),
+        "muonbp_get_momentum": (ctypes.c_int, [P, I32, P]),
+        "muonbp_set_momentum": (ctypes.c_int, [P, I32, P]),
+        "muonbp_get_update": (ctypes.c_int, [P, I32, P]),
+        "muonbp_synchronize": (ctypes.c_int, [P]),
+        "muonbp_describe_plan": (ctypes.c_int, [ctypes.POINTER(Matrix), I32,
+                                                ctypes.POINTER(Options), I32,
+                                                ctypes.POINTER(PlanInfo)]),
+        "muonbp_profile_enable": (ctypes.c_int, [P, I32]),
+        "muonbp_profile_read": (ctypes.c_int, [P, ctypes.POINTER(Profile)]),
+        "muonbp_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+        "muonbp_last_error": (ctypes.c_char_p, [P]),
+        "muonbp_destroy": (None, [P]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def options_default(**overrides) -> Options:
+    o = Options()
+    load_library().muonbp_options_default(ctypes.byref(o))
+    for k, v in overrides.items():
+        if not hasattr(o, k):
+            raise AttributeError(k)
+        setattr(o, k, v)
+    return o
+
+
+def _mats(mats: Sequence[Tuple[int, int, int, int]]):
+    arr = (Matrix * len(mats))()
+    for i, (r, c, gr, gc) in enumerate(mats):
+        arr[i] = Matrix(r, c, gr, gc)
+    return arr
+
+
+def describe_plan(mats, full: bool, options: Optional[Options] = None) -> PlanInfo:
+    """Host-only description of the block (full=False) or full plan."""
+    lib = load_library()
+    info = PlanInfo()
+    st = lib.muonbp_describe_plan(_mats(mats), len(mats),
+                                  ctypes.byref(options) if options else None,
+                                  int(bool(full)), ctypes.byref(info))
+    if st:
+        raise MuonBPError(st, "describe_plan")
+    return info
+
+
+def _torch_dtype(code: int):
+    import torch
+    return {F32: torch.float32, BF16: torch.bfloat16}[code]
+
+
+class MuonBP:
+    """One optimizer context over a fixed list of matrices (Algorithm 1)."""
+
+    def __init__(self, mats: Sequence[Tuple[int, int, int, int]], period: int,
+                 lr_block: float, lr_full: float, momentum: float,
+                 weight_decay: float = 0.0, options: Optional[Options] = None,
+                 stream=None):
+        import torch
+        self.lib = load_library()
+        self.mats = [tuple(int(v) for v in m) for m in mats]
+        self.options = options if options is not None else options_default()
+        if stream is None:
+            stream = torch.cuda.current_stream()
+        self._stream = stream
+        ctx = ctypes.c_void_p()
+        st = self.lib.muonbp_create(_mats(self.mats), len(self.mats), int(period),
+                                    float(lr_block), float(lr_full), float(momentum),
+                                    float(weight_decay), ctypes.byref(self.options),
+                                    ctypes.c_void_p(stream.cuda_stream), ctypes.byref(ctx))
+        if st:
+            raise MuonBPError(st, "muonbp_create")
+        self.ctx = ctx
+        self.period = int(period)
+        self._ptrs = (ctypes.c_void_p * len(self.mats))()
+        self._gptrs = (ctypes.c_void_p * len(self.mats))()
+
+    # -- helpers
+    def _check(self, st: int, what: str):
+        if st:
+            detail = self.lib.muonbp_last_error(self.ctx)
+            raise MuonBPError(st, f"{what}: {detail.decode() if detail else ''}")
+
+    def _check_tensor(self, t, i, dtype_code):
+        import torch
+        r, c = self.mats[i][:2]
+        if not (t.is_cuda and t.is_contiguous() and t.dtype == _torch_dtype(dtype_code)
+                and tuple(t.shape) == (r, c)):
+            raise ValueError(f"matrix {i}: need a contiguous {_torch_dtype(dtype_code)} "
+                             f"CUDA tensor of shape {(r, c)}, got {t.dtype} {tuple(t.shape)}")
+
+    def is_full(self, t: int) -> bool:
+        return self.period > 0 and t % self.period == 0
+
+    # -- API
+    def step(self, params: List, grads: List, t: int) -> None:
+        n = len(self.mats)
+        if len(params) != n or len(grads) != n:
+            raise ValueError("one param and one grad per matrix")
+        for i in range(n):
+            self._check_tensor(params[i], i, self.options.param_dtype)
+            self._check_tensor(grads[i], i, self.options.param_dtype)
+            self._ptrs[i] = params[i].data_ptr()
+            self._gptrs[i] = grads[i].data_ptr()
+        self._check(self.lib.muonbp_step(self.ctx, self._ptrs, self._gptrs, int(t)), "step")
+
+    def set_lr(self, lr_block: float, lr_full: float) -> None:
+        self._check(self.lib.muonbp_set_lr(self.ctx, float(lr_block), float(lr_full)), "set_lr")
+
+    def set_stream(self, stream) -> None:
+        self._check(self.lib.muonbp_set_stream(self.ctx, ctypes.c_void_p(stream.cuda_stream)),
+                    "set_stream")
+        self._stream = stream
+
+    def get_momentum(self, i: int, out=None):
+        import torch
+        r, c = self.mats[i][:2]
+        if out is None:
+            out = torch.empty((r, c), dtype=_torch_dtype(self.options.state_dtype), device="cuda")
+        self._check_tensor(out, i, self.options.state_dtype)
+        self._check(self.lib.muonbp_get_momentum(self.ctx, i, ctypes.c_void_p(out.data_ptr())),
+                    "get_momentum")
+        return out
+
+    def set_momentum(self, i: int, src) -> None:
+        self._check_tensor(src, i, self.options.state_dtype)
+        self._check(self.lib.muonbp_set_momentum(self.ctx, i, ctypes.c_void_p(src.data_ptr())),
+                    "set_momentum")
+
+    def get_update(self, i: int, out=None):
+        import torch
+        r, c = self.mats[i][:2]
+        if out is None:
+            out = torch.empty((r, c), dtype=_torch_dtype(self.options.ns_dtype), device="cuda")
+        self._check_tensor(out, i, self.options.ns_dtype)
+        self._check(self.lib.muonbp_get_update(self.ctx, i, ctypes.c_void_p(out.data_ptr())),
+                    "get_update")
+        return out
+
+    def synchronize(self) -> None:
+        self._check(self.lib.muonbp_synchronize(self.ctx), "synchronize")
+
+    def profile_enable(self, on: bool = True) -> None:
+        self._check(self.lib.muonbp_profile_enable(self.ctx, int(bool(on))), "profile_enable")
+
+    def profile_read(self) -> dict:
+        p = Profile()
+        self._check(self.lib.muonbp_profile_read(self.ctx, ctypes.byref(p)), "profile_read")
+        return {k: (p.ms[i], p.launches[i]) for i, k in enumerate(KERNEL_KINDS)}
+
+    def close(self) -> None:
+        if getattr(self, "ctx", None):
+            self.lib.muonbp_destroy(self.ctx)
+            self.ctx = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

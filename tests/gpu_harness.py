@@ -1,0 +1,141 @@
+"""Shared driver of the GPU parity tests: runs the HIP library and the CPU
+oracle in lockstep on the same seeded inputs and reports relative Frobenius
+errors.  Imported by the GPU tests only."""
+
+from __future__ import annotations
+
+import sys
+from dataclasses import dataclass, field
+from typing import Dict, List, Optional, Sequence
+
+import numpy as np
+
+from oracle import muonbp_oracle as O
+from paper_2510_16981_amd import workload as W
+
+DT = {"f32": 0, "bf16": 1}
+
+
+def rel(a: np.ndarray, b: np.ndarray) -> float:
+    nb = np.linalg.norm(b)
+    if nb == 0.0:
+        return float(np.linalg.norm(a))
+    return float(np.linalg.norm(a - b) / nb)
+
+
+def announce(msg: str) -> None:
+    print(f"[gpu-case] {msg}", flush=True)
+    sys.stdout.flush()
+
+
+@dataclass
+class Case:
+    mats: Sequence[tuple]
+    period: int = 5
+    steps: int = 6
+    lr_block: float = 0.013
+    lr_full: float = 0.02
+    momentum: float = 0.95
+    weight_decay: float = 0.1
+    ns_steps: int = 5
+    nesterov: int = 0
+    scale_mode: int = 0
+    rms_beta: float = 1.0
+    param: str = "bf16"
+    state: str = "bf16"
+    ns: str = "bf16"
+    rank: int = 16
+    seed: int = 0
+    zero_mats: Sequence[int] = ()
+    check_steps: Optional[Sequence[int]] = None  # None = every step
+
+
+@dataclass
+class Result:
+    u_err: List[float] = field(default_factory=list)      # teacher-forced U
+    u_free_err: List[float] = field(default_factory=list)  # U vs free-running oracle
+    m_err: List[float] = field(default_factory=list)
+    x_err: List[float] = field(default_factory=list)
+    fulls: List[bool] = field(default_factory=list)
+    final_params: List[np.ndarray] = field(default_factory=list)
+    final_mom: List[np.ndarray] = field(default_factory=list)
+    updates: Dict[int, List[np.ndarray]] = field(default_factory=dict)
+
+    def worst(self) -> Dict[str, float]:
+        f = lambda v: max(v) if v else 0.0
+        return dict(u=f(self.u_err), u_free=f(self.u_free_err), m=f(self.m_err), x=f(self.x_err))
+
+
+def make_inputs(case: Case):
+    """Seeded params and per-step grads (float64 values of the storage dtype)."""
+    grads = []
+    bases = [W.lowrank_basis(r, c, case.rank, case.seed, k) for k, (r, c, _, _) in enumerate(case.mats)]
+    for t in range(case.steps):
+        gt = []
+        for k, (r, c, _, _) in enumerate(case.mats):
+            if k in case.zero_mats:
+                gt.append(W.quantize(np.zeros((r, c)), case.param))
+            else:
+                gt.append(W.quantize(W.lowrank_grad(r, c, case.rank, case.seed, k, t,
+                                                    basis=bases[k]), case.param))
+        grads.append(gt)
+    params = [W.quantize(W.init_param(r, c, case.seed, k), case.param)
+              for k, (r, c, _, _) in enumerate(case.mats)]
+    return params, grads
+
+
+def run_case(case: Case, keep_updates: bool = False) -> Result:
+    import torch
+    from paper_2510_16981_amd import muonbp as mb
+
+    opts = mb.options_default(ns_steps=case.ns_steps, nesterov=case.nesterov,
+                              scale_mode=case.scale_mode, rms_beta=case.rms_beta,
+                              param_dtype=DT[case.param], state_dtype=DT[case.state],
+                              ns_dtype=DT[case.ns])
+    opt = mb.MuonBP(case.mats, case.period, case.lr_block, case.lr_full, case.momentum,
+                    case.weight_decay, options=opts)
+    orc = O.MuonBPOracle([O.MatrixSpec(*m) for m in case.mats],
+                         O.OracleConfig(period=case.period, lr_block=case.lr_block,
+                                        lr_full=case.lr_full, momentum=case.momentum,
+                                        weight_decay=case.weight_decay, ns_steps=case.ns_steps,
+                                        nesterov=bool(case.nesterov), scale_mode=case.scale_mode,
+                                        rms_beta=case.rms_beta))
+    params_h, grads_h = make_inputs(case)
+    params = [p.cuda() for p in params_h]
+    x_ref = [p.double().numpy() for p in params_h]
+    res = Result()
+    for t in range(case.steps):
+        g_dev = [g.cuda() for g in grads_h[t]]
+        opt.step(params, g_dev, t)
+        full = opt.is_full(t)
+        res.fulls.append(full)
+        g64 = [g.double().numpy() for g in grads_h[t]]
+        x_ref, rec = orc.step(x_ref, g64, t, record=True)
+        check = case.check_steps is None or t in case.check_steps
+        if not check and t != case.steps - 1:
+            continue
+        torch.cuda.synchronize()
+        for k, (r, c, gr, gc) in enumerate(case.mats):
+            m_gpu = opt.get_momentum(k).double().cpu().numpy()
+            u_gpu = opt.get_update(k).double().cpu().numpy()
+            torch.cuda.synchronize()
+            # Teacher forcing: the oracle orthogonalizes the GPU's own state.
+            y = g64[k] + case.momentum * m_gpu if case.nesterov else m_gpu
+            ns = dict(K=case.ns_steps)
+            u_tf = O.orthogonalize_via_ns(y, **ns) if full else \
+                O.orthogonalize_blockwise(y, (gr, gc), **ns)
+            res.u_err.append(rel(u_gpu, u_tf))
+            u_free = rec.U[k]
+            if case.scale_mode == 1:
+                p, q = (r, c) if full else (r // gr, c // gc)
+                u_free = u_free / O.rms_scale(p, q, case.rms_beta)
+            res.u_free_err.append(rel(u_gpu, u_free))
+            res.m_err.append(rel(m_gpu, rec.M[k]))
+            res.x_err.append(rel(params[k].double().cpu().numpy(), x_ref[k]))
+            if keep_updates:
+                res.updates.setdefault(t, []).append(u_gpu)
+    torch.cuda.synchronize()
+    res.final_params = [p.double().cpu().numpy() for p in params]
+    res.final_mom = [opt.get_momentum(k).double().cpu().numpy() for k in range(len(case.mats))]
+    opt.close()
+    return res

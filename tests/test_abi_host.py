@@ -1,0 +1,141 @@
+"""Host-side checks of the C-ABI library (no GPU needed, no compute call).
+
+The library must load, export every function declared in include/muonbp.h,
+reject bad arguments before touching the GPU, and describe its plans.
+"""
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import muonbp_oracle as O
+from paper_2510_16981_amd import muonbp as mb
+from paper_2510_16981_amd import workload as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "muonbp.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(mb.LIB_PATH):
+        from paper_2510_16981_amd import build
+        build.build()
+    return mb.load_library()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(muonbp_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_api():
+    names = declared_functions()
+    for required in ["muonbp_create", "muonbp_step", "muonbp_destroy",
+                     "muonbp_get_update", "muonbp_get_momentum", "muonbp_set_momentum"]:
+        assert required in names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    missing = [n for n in declared_functions() if not hasattr(lib, n)]
+    assert not missing, missing
+
+
+def test_options_default(lib):
+    o = mb.options_default()
+    assert o.ns_steps == 5
+    assert (o.a, o.b, o.c) == (2.0, -1.5, 0.5)
+    assert abs(o.eps - 1e-7) < 1e-12
+    assert (o.nesterov, o.scale_mode, o.rms_beta) == (0, 0, 1.0)
+    assert (o.param_dtype, o.state_dtype, o.ns_dtype) == (mb.BF16, mb.BF16, mb.BF16)
+
+
+def test_status_strings(lib):
+    for code in range(7):
+        assert lib.muonbp_status_string(code)
+    assert lib.muonbp_last_error(None) == b"no context"
+    lib.muonbp_destroy(None)  # NULL-safe
+
+
+def _create(lib, mats, period=5, opt=None, out=True):
+    ctx = ctypes.c_void_p()
+    arr = mb._mats(mats) if mats is not None else None
+    n = len(mats) if mats is not None else 0
+    return lib.muonbp_create(arr, n, period, 0.01, 0.02, 0.95, 0.1,
+                             ctypes.byref(opt) if opt else None, None,
+                             ctypes.byref(ctx) if out else None), ctx
+
+
+def test_create_rejects_bad_arguments_before_gpu(lib):
+    assert _create(lib, None)[0] == 1
+    assert _create(lib, [])[0] == 1
+    assert _create(lib, [(8, 8, 1, 1)], out=False)[0] == 1
+    assert _create(lib, [(8, 8, 1, 1)], period=-1)[0] == 1
+    st, ctx = _create(lib, [(10, 8, 3, 1)])
+    assert st == 2 and not ctx.value
+    assert _create(lib, [(0, 8, 1, 1)])[0] == 2
+    assert _create(lib, [(8, 8, 0, 1)])[0] == 2
+    assert _create(lib, [(8, 8, 1, 1)], opt=mb.options_default(param_dtype=7))[0] == 3
+    assert _create(lib, [(8, 8, 1, 1)], opt=mb.options_default(ns_steps=-1))[0] == 1
+    assert _create(lib, [(8, 8, 1, 1)], opt=mb.options_default(scale_mode=3))[0] == 1
+
+
+def test_null_context_calls(lib):
+    assert lib.muonbp_step(None, None, None, 0) == 1
+    assert lib.muonbp_set_lr(None, 0.1, 0.1) == 1
+    assert lib.muonbp_synchronize(None) == 1
+    assert lib.muonbp_get_update(None, 0, None) == 1
+
+
+def _unit_counts(mats, full):
+    units = []
+    for r, c, gr, gc in mats:
+        if full:
+            units.append((r, c))
+        else:
+            units += [(r // gr, c // gc)] * (gr * gc)
+    return units
+
+
+@pytest.mark.parametrize("name", list(W.WORKLOADS))
+def test_describe_plan_counts_and_flops(lib, name):
+    mats = W.workload_matrices(name)
+    for full in (False, True):
+        info = mb.describe_plan(mats, full)
+        units = _unit_counts(mats, full)
+        assert info.n_problems == len(units)
+        assert info.n_elements == sum(r * c for r, c, _, _ in mats)
+        dense = sum(O.ns_dense_flops(p, q, 5) for p, q in units)
+        assert abs(info.ns_dense_flops - dense) <= 1e-9 * dense
+        sym = 0.0
+        gram = apply = 0
+        for p, q in units:
+            S, L = min(p, q), max(p, q)
+            sym += 5 * (S * (S + 1) * L + S * S * (S + 1) + 2 * S * S * L)
+            ts, tl = -(-S // 128), -(-L // 128)
+            gram += ts * (ts + 1) // 2
+            apply += ts * tl
+        assert abs(info.ns_flops - sym) <= 1e-9 * sym
+        assert info.gemm_tiles[0] == gram and info.gemm_tiles[1] == gram
+        assert info.gemm_tiles[2] == apply
+        assert info.workspace_bytes > 0
+
+
+def test_describe_plan_qkv_numbers(lib):
+    """2048 x 6144 with 8 column shards of 2048 x 768 (transposed: S = 768)."""
+    mats = W.workload_matrices("qkv-2048x6144-bf16")
+    blk = mb.describe_plan(mats, False)
+    full = mb.describe_plan(mats, True)
+    assert abs(blk.ns_dense_flops / 1e12 - 0.2295) < 5e-4
+    assert abs(full.ns_dense_flops / 1e12 - 0.6013) < 5e-4
+    assert abs(blk.ns_flops / 1e12 - 0.1632) < 5e-4
+    assert abs(full.ns_flops / 1e12 - 0.4296) < 5e-4
+
+
+def test_describe_plan_rejects_bad_grid(lib):
+    with pytest.raises(mb.MuonBPError):
+        mb.describe_plan([(10, 10, 3, 1)], False)

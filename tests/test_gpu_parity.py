@@ -1,0 +1,220 @@
+"""GPU parity: the HIP library against the CPU oracle on seeded inputs.
+
+Bars: relative Frobenius error <= 1e-4 when every stage is fp32, <= 2e-2
+when any of params, momentum or NS operands is bf16.  U is compared
+teacher-forced (the oracle orthogonalizes the GPU's own momentum) so that
+the NS error is isolated; momentum and params are compared against the
+free-running fp64 oracle.
+"""
+
+import numpy as np
+import pytest
+
+from tests.gpu_harness import Case, announce, rel, run_case
+
+pytestmark = pytest.mark.gpu
+
+BF16_TOL = 2e-2
+F32_TOL = 1e-4
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a ROCm device"
+    from paper_2510_16981_amd import muonbp as mb
+    mb.load_library()  # fails loudly if the HIP library is missing
+
+
+def _check(res, tol, free_u_tol=None):
+    w = res.worst()
+    announce(f"worst errors {w}")
+    assert w["u"] <= tol, w
+    assert w["m"] <= tol, w
+    assert w["x"] <= tol, w
+    if free_u_tol is not None:
+        assert w["u_free"] <= free_u_tol, w
+
+
+def test_single_256x512_fp32_ten_steps():
+    """fp32 path: 256 x 512, two 256 x 256 column blocks, rank-32 gradients,
+    mu = 0.95, K = 5, P = 5, 10 steps."""
+    case = Case(mats=[(256, 512, 1, 2)], period=5, steps=10, rank=32,
+                param="f32", state="f32", ns="f32")
+    announce("single-256x512-f32")
+    res = run_case(case)
+    assert res.fulls == [t % 5 == 0 for t in range(10)]
+    _check(res, F32_TOL, free_u_tol=F32_TOL)
+    # The cumulative update X_T - X_0 agrees as well (fp32 storage).
+    from tests.gpu_harness import make_inputs
+    from oracle import muonbp_oracle as O
+    params_h, grads_h = make_inputs(case)
+    x0 = params_h[0].double().numpy()
+    orc = O.MuonBPOracle([O.MatrixSpec(256, 512, 1, 2)],
+                         O.OracleConfig(period=5, lr_block=case.lr_block, lr_full=case.lr_full,
+                                        momentum=case.momentum, weight_decay=case.weight_decay))
+    x = [x0]
+    for t in range(10):
+        x = orc.step(x, [grads_h[t][0].double().numpy()], t)
+    assert rel(res.final_params[0] - x0, x[0] - x0) <= F32_TOL
+
+
+RAGGED = [(272, 528, 2, 2), (528, 272, 2, 2), (129, 1000, 1, 1), (8, 40, 1, 1)]
+SCALAR = [(300, 520, 2, 4), (520, 300, 4, 2), (64, 12, 1, 12), (1, 40, 1, 1), (3, 5, 1, 1)]
+
+
+@pytest.mark.parametrize("mats", [RAGGED, SCALAR], ids=["vector-paths", "scalar-paths"])
+def test_ragged_shapes_bf16(mats):
+    """Several tiles with ragged tails, tall (transposed) units, column
+    normalisation blocks (m x 1), single-row matrices."""
+    announce(f"ragged bf16 {mats}")
+    res = run_case(Case(mats=mats, period=3, steps=4))
+    _check(res, BF16_TOL)
+
+
+@pytest.mark.parametrize("mats", [RAGGED, SCALAR], ids=["vector-paths", "scalar-paths"])
+def test_ragged_shapes_fp32(mats):
+    announce(f"ragged f32 {mats}")
+    res = run_case(Case(mats=mats, period=3, steps=4, param="f32", state="f32", ns="f32"))
+    _check(res, F32_TOL, free_u_tol=F32_TOL)
+
+
+@pytest.mark.parametrize("param,state,ns", [("bf16", "f32", "bf16"), ("f32", "f32", "bf16"),
+                                            ("f32", "bf16", "f32"), ("bf16", "bf16", "f32")])
+def test_dtype_combinations(param, state, ns):
+    announce(f"dtypes param={param} state={state} ns={ns}")
+    res = run_case(Case(mats=RAGGED[:2], period=2, steps=3, param=param, state=state, ns=ns))
+    _check(res, BF16_TOL)
+
+
+def test_nesterov_rms_scaling_and_zero_gradient():
+    """Options off the paper's default path plus a zero-gradient matrix
+    (U = 0 there, so X only decays)."""
+    announce("nesterov + rms + zero matrix")
+    res = run_case(Case(mats=RAGGED[:2] + [(64, 128, 2, 2)], period=2, steps=3, nesterov=1,
+                        scale_mode=1, rms_beta=0.2, zero_mats=(2,), param="f32", state="f32",
+                        ns="f32"))
+    _check(res, F32_TOL, free_u_tol=F32_TOL)
+
+
+def test_zero_ns_steps_gives_normalised_momentum():
+    announce("K = 0")
+    res = run_case(Case(mats=RAGGED[:2], ns_steps=0, period=2, steps=2, param="f32", state="f32",
+                        ns="f32"))
+    _check(res, F32_TOL, free_u_tol=F32_TOL)
+
+
+@pytest.mark.parametrize("period", [1, 0], ids=["muon", "blockmuon"])
+def test_period_extremes(period):
+    """P = 1 is Muon (every step full), P = infinity is BlockMuon."""
+    announce(f"period {period}")
+    res = run_case(Case(mats=[(256, 384, 2, 3)], period=period, steps=3, param="f32",
+                        state="f32", ns="f32"))
+    assert res.fulls == [period == 1] * 3
+    _check(res, F32_TOL, free_u_tol=F32_TOL)
+
+
+def test_qkv_2048x6144_bf16_full_size():
+    """The benchmarked workload at full size: 2048 x 6144 bf16, eight
+    2048 x 768 column shards, rank-128 gradients, P = 5.  Steps 0 and 5 are
+    full, 1..4 blockwise."""
+    announce("qkv-2048x6144-bf16 full size")
+    res = run_case(Case(mats=[(2048, 6144, 1, 8)], period=5, steps=6, rank=128,
+                        check_steps=(0, 1, 5)))
+    assert res.fulls == [True, False, False, False, False, True]
+    _check(res, BF16_TOL)
+
+
+def test_deterministic():
+    announce("determinism")
+    c = Case(mats=RAGGED, period=2, steps=3)
+    a, b = run_case(c), run_case(c)
+    for x, y in zip(a.final_params, b.final_params):
+        assert np.array_equal(x, y)
+
+
+def test_blocks_match_independent_shards():
+    """Each block of a sharded matrix is what a device holding only that
+    shard computes: one context over a 2 x 3 grid equals six single-block
+    contexts, bit for bit (BlockMuon, P = infinity)."""
+    import torch
+    from paper_2510_16981_amd import muonbp as mb
+    from paper_2510_16981_amd import workload as W
+    announce("sharding equivalence")
+    m, n, gr, gc = 256, 384, 2, 3
+    bm, bn = m // gr, n // gc
+    G = [W.quantize(W.lowrank_grad(m, n, 16, 0, 0, t), "bf16").cuda() for t in range(3)]
+    X0 = W.quantize(W.init_param(m, n, 0, 0), "bf16").cuda()
+    whole = mb.MuonBP([(m, n, gr, gc)], 0, 0.01, 0.02, 0.9, 0.1)
+    X = X0.clone()
+    for t in range(3):
+        whole.step([X], [G[t]], t)
+    parts = []
+    for i in range(gr):
+        for j in range(gc):
+            ctx = mb.MuonBP([(bm, bn, 1, 1)], 0, 0.01, 0.02, 0.9, 0.1)
+            Xb = X0[i * bm:(i + 1) * bm, j * bn:(j + 1) * bn].contiguous()
+            for t in range(3):
+                Gb = G[t][i * bm:(i + 1) * bm, j * bn:(j + 1) * bn].contiguous()
+                ctx.step([Xb], [Gb], t)
+            torch.cuda.synchronize()
+            parts.append((i, j, Xb))
+            ctx.close()
+    torch.cuda.synchronize()
+    for i, j, Xb in parts:
+        assert torch.equal(X[i * bm:(i + 1) * bm, j * bn:(j + 1) * bn], Xb)
+    whole.close()
+
+
+def test_resume_from_momentum_checkpoint():
+    """get_momentum after step 2, restore into a fresh context, continue:
+    identical to the uninterrupted run."""
+    import torch
+    from paper_2510_16981_amd import muonbp as mb
+    from paper_2510_16981_amd import workload as W
+    announce("resume")
+    mats = [(272, 528, 2, 2)]
+    G = [W.quantize(W.lowrank_grad(272, 528, 16, 0, 0, t), "bf16").cuda() for t in range(6)]
+    X0 = W.quantize(W.init_param(272, 528, 0, 0), "bf16").cuda()
+    a = mb.MuonBP(mats, 3, 0.01, 0.02, 0.9, 0.1)
+    Xa = X0.clone()
+    for t in range(6):
+        a.step([Xa], [G[t]], t)
+    b = mb.MuonBP(mats, 3, 0.01, 0.02, 0.9, 0.1)
+    Xb = X0.clone()
+    for t in range(3):
+        b.step([Xb], [G[t]], t)
+    M = b.get_momentum(0)
+    torch.cuda.synchronize()
+    b.close()
+    c = mb.MuonBP(mats, 3, 0.01, 0.02, 0.9, 0.1)
+    c.set_momentum(0, M)
+    for t in range(3, 6):
+        c.step([Xb], [G[t]], t)
+    torch.cuda.synchronize()
+    assert torch.equal(Xa, Xb)
+    a.close()
+    c.close()
+
+
+def test_errors_on_device():
+    """Errors are reported as status codes; the context stays usable."""
+    import torch
+    from paper_2510_16981_amd import muonbp as mb
+    announce("error paths")
+    ctx = mb.MuonBP([(64, 64, 1, 1)], 2, 0.01, 0.02, 0.9, 0.0)
+    with pytest.raises(mb.MuonBPError):
+        ctx.get_update(0)  # no step yet
+    X = torch.zeros(64, 64, dtype=torch.bfloat16, device="cuda")
+    G = torch.ones(64, 64, dtype=torch.bfloat16, device="cuda")
+    import ctypes
+    ptrs = (ctypes.c_void_p * 1)(X.data_ptr())
+    assert ctx.lib.muonbp_step(ctx.ctx, ptrs, ptrs, -1) == 1
+    nul = (ctypes.c_void_p * 1)(None)
+    assert ctx.lib.muonbp_step(ctx.ctx, nul, ptrs, 0) == 1
+    ctx.step([X], [G], 0)
+    ctx.synchronize()
+    U = ctx.get_update(0).float()
+    torch.cuda.synchronize()
+    assert torch.isfinite(U).all()
+    ctx.close()
