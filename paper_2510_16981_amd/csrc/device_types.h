@@ -49,15 +49,17 @@ struct PackDesc {
 
 // One product of a grouped NS launch, all row-major with K contiguous:
 //   C[i][j] = alpha * sum_k X[i][k] Y[j][k] + beta * D[i][j]
-// and, when Ct is set, Ct[j][i] = the same value.
+// and, when Ct is set, Ct[j][i] = alpha * sum_k X[i][k] Y[j][k] + beta * Dt[j][i]
+// where Dt holds D transposed (the same values, so Ct = C^T).
 struct GemmDesc {
   const void* X;
   const void* Y;
   const void* D;
+  const void* Dt;
   void* C;
   void* Ct;
   int32_t M, N, K;
-  int32_t ldx, ldy, ldd, ldc, ldct;
+  int32_t ldx, ldy, ldd, lddt, ldc, ldct;
 };
 
 // One workgroup tile of a grouped launch: problem index and packed

@@ -211,22 +211,74 @@ template <> struct Mfma<float> {
   }
 };
 
-// 16-byte slice of row `row` starting at column k, zero outside
-// [0, nrows) x [0, K).
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(1))) const u32x4_t gu32x4_t;
+
+// 16-byte load through the global address space (global_load rather than
+// flat_load: flat loads also count against the LDS wait counter, so every
+// LDS wait in the K loop would also wait for the prefetch).  The integer
+// round trip makes the compiler emit an address-space-1 access.
+__device__ __forceinline__ uint4 gld16(const void* p) {
+  const u32x4_t v = *(gu32x4_t*)(reinterpret_cast<uintptr_t>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+// Zero the elements of a 16-byte slice at positions >= nv (nv in [0, EPV]).
 template <typename T>
-__device__ __forceinline__ uint4 load_slice(const T* base, int row, int nrows, int ld, int k, int K) {
-  constexpr int EPV = 16 / sizeof(T);
-  uint4 z = make_uint4(0, 0, 0, 0);
-  if (row >= nrows || k >= K) return z;
-  const T* p = base + int64_t(row) * ld + k;
-  if (k + EPV <= K) return *reinterpret_cast<const uint4*>(p);
-  union {
-    T e[EPV];
-    uint4 v;
-  } u;
+__device__ __forceinline__ uint4 mask_tail(uint4 v, int nv) {
+  if (sizeof(T) == 2) {
+    v.x &= (nv > 0 ? 0xffffu : 0u) | (nv > 1 ? 0xffff0000u : 0u);
+    v.y &= (nv > 2 ? 0xffffu : 0u) | (nv > 3 ? 0xffff0000u : 0u);
+    v.z &= (nv > 4 ? 0xffffu : 0u) | (nv > 5 ? 0xffff0000u : 0u);
+    v.w &= (nv > 6 ? 0xffffu : 0u) | (nv > 7 ? 0xffff0000u : 0u);
+  } else {
+    v.x = nv > 0 ? v.x : 0u;
+    v.y = nv > 1 ? v.y : 0u;
+    v.z = nv > 2 ? v.z : 0u;
+    v.w = nv > 3 ? v.w : 0u;
+  }
+  return v;
+}
+
+constexpr int kStPitch = kTile + 1;  // fp32 staging row pitch (floats)
+static_assert(kTile * kStPitch * 4 <= 4 * kLdsOp, "staging tile must fit in LDS");
+
+// Writes one 128 x 128 output tile from the fp32 staging tile st.
+// Output element (r, c) of the tile goes to out[(r0 + r) * ldo + c0 + c] with
+// value st(r, c) + beta * add[(r0 + r) * lda + c0 + c]; with `transposed`,
+// st(r, c) is read at st[c * kStPitch + r] (the tile's transpose).
+template <typename T>
+__device__ __forceinline__ void store_tile(const float* st, void* outp, int ldo, const void* addp,
+                                           int lda, float beta, int r0, int c0, int nr, int nc,
+                                           bool transposed) {
+  T* out = static_cast<T*>(outp);
+  const T* add = static_cast<const T*>(addp);
+  constexpr int kChunks = kTile * kTile / 8;
+#pragma unroll 2
+  for (int q = threadIdx.x; q < kChunks; q += kThreads) {
+    const int r = q >> 4, c = (q & 15) * 8;
+    const int gr = r0 + r, gc = c0 + c;
+    if (gr >= nr || gc >= nc) continue;
+    float f[8];
 #pragma unroll
-  for (int i = 0; i < EPV; ++i) u.e[i] = (k + i < K) ? p[i] : from_f<T>(0.f);
-  return u.v;
+    for (int e = 0; e < 8; ++e) f[e] = transposed ? st[(c + e) * kStPitch + r] : st[r * kStPitch + c + e];
+    const int64_t oo = int64_t(gr) * ldo + gc, oa = int64_t(gr) * lda + gc;
+    if (gc + 8 <= nc) {
+      if (add) {
+        float a8[8];
+        load8(add + oa, a8);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) f[e] = fmaf(beta, a8[e], f[e]);
+      }
+      store8(out + oo, f);
+    } else {
+      for (int e = 0; e < nc - gc; ++e) {
+        float v = f[e];
+        if (add) v = fmaf(beta, to_f<T>(add[oa + e]), v);
+        out[oo + e] = from_f<T>(v);
+      }
+    }
+  }
 }
 
 template <typename T>
@@ -243,17 +295,35 @@ __global__ __launch_bounds__(kThreads) void k_ns_gemm(const GemmDesc* __restrict
   const int m0 = ti * kTile, n0 = tj * kTile;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
-  const T* X = static_cast<const T*>(d.X);
-  const T* Y = static_cast<const T*>(d.Y);
-
+  // Rows beyond M (N) are clamped to a valid row: they only feed output rows
+  // (columns) that are never stored.  Columns at or beyond K are masked to
+  // zero in the last K slice, which may straddle K (rows are padded to a
+  // multiple of 8 elements, so the 16-byte read stays inside the row).
+  const int kc = (tid & 7) * EPV;  // this thread's column inside a K slice
+  const T* xrow[4];
+  const T* yrow[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int row = (tid + kThreads * q) >> 3;
+    xrow[q] = static_cast<const T*>(d.X) + int64_t(min(m0 + row, d.M - 1)) * d.ldx;
+    yrow[q] = static_cast<const T*>(d.Y) + int64_t(min(n0 + row, d.N - 1)) * d.ldy;
+  }
   uint4 rx[4], ry[4];
   auto gload = [&](int k0) {
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const int v = tid + kThreads * q;
-      const int row = v >> 3, kk = k0 + (v & 7) * EPV;
-      rx[q] = load_slice<T>(X, m0 + row, d.M, d.ldx, kk, d.K);
-      ry[q] = load_slice<T>(Y, n0 + row, d.N, d.ldy, kk, d.K);
+      rx[q] = gld16(xrow[q] + k0 + kc);
+      ry[q] = gld16(yrow[q] + k0 + kc);
+    }
+  };
+  auto gload_tail = [&](int k0) {
+    const int kk = k0 + kc;
+    const int nv = max(0, min(d.K - kk, EPV));
+    const int o = nv > 0 ? kk : 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      rx[q] = mask_tail<T>(gld16(xrow[q] + o), nv);
+      ry[q] = mask_tail<T>(gld16(yrow[q] + o), nv);
     }
   };
   auto lstore = [&](int buf) {
@@ -275,12 +345,14 @@ __global__ __launch_bounds__(kThreads) void k_ns_gemm(const GemmDesc* __restrict
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
   const int nk = (d.K + BK - 1) / BK;
-  gload(0);
+  if (BK <= d.K) gload(0); else gload_tail(0);
   lstore(0);
   __syncthreads();
   for (int kt = 0; kt < nk; ++kt) {
     const int buf = kt & 1;
-    if (kt + 1 < nk) gload((kt + 1) * BK);
+    if (kt + 1 < nk) {
+      if ((kt + 2) * BK <= d.K) gload((kt + 1) * BK); else gload_tail((kt + 1) * BK);
+    }
     const unsigned char* As = lds + (2 * buf) * kLdsOp;
     const unsigned char* Bs = lds + (2 * buf + 1) * kLdsOp;
 #pragma unroll
@@ -303,29 +375,25 @@ __global__ __launch_bounds__(kThreads) void k_ns_gemm(const GemmDesc* __restrict
   }
 
   // Epilogue.  32x32 accumulator layout: lane l holds column l % 32 and, for
-  // register v, row 8 (v / 4) + 4 (l / 32) + v % 4.
-  const T* D = static_cast<const T*>(d.D);
-  T* C = static_cast<T*>(d.C);
-  T* Ct = static_cast<T*>(d.Ct);
-  const bool mirror = Ct != nullptr && !(sym && ti == tj);
+  // register v, row 8 (v / 4) + 4 (l / 32) + v % 4.  alpha * acc is staged
+  // in LDS as fp32 (odd row pitch: conflict-light row and column reads), then
+  // every thread writes 8-element (16-byte) chunks of C rows and, for the
+  // transposed copy, of Ct rows, adding beta * D (or beta * Dt) in fp32.
+  float* st = reinterpret_cast<float*>(lds);
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
-      const int col = n0 + wn * 64 + j * 32 + (lane & 31);
-      const int rbase = m0 + wm * 64 + i * 32 + 4 * (lane >> 5);
+      const int col = wn * 64 + j * 32 + (lane & 31);
+      const int rbase = wm * 64 + i * 32 + 4 * (lane >> 5);
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int row = rbase + 8 * (v >> 2) + (v & 3);
-        if (row < d.M && col < d.N) {
-          float val = alpha * acc[i][j][v];
-          if (D) val = fmaf(beta, to_f<T>(D[int64_t(row) * d.ldd + col]), val);
-          const T o = from_f<T>(val);
-          C[int64_t(row) * d.ldc + col] = o;
-          if (mirror) Ct[int64_t(col) * d.ldct + row] = o;
-        }
-      }
+      for (int v = 0; v < 16; ++v)
+        st[(rbase + 8 * (v >> 2) + (v & 3)) * kStPitch + col] = alpha * acc[i][j][v];
     }
+  __syncthreads();
+  store_tile<T>(st, d.C, d.ldc, d.D, d.ldd, beta, m0, n0, d.M, d.N, false);
+  if (d.Ct != nullptr && !(sym && ti == tj))
+    store_tile<T>(st, d.Ct, d.ldct, d.Dt, d.lddt, beta, n0, m0, d.N, d.M, true);
 }
 
 // ---------------------------------------------------------------- update

@@ -169,15 +169,16 @@ hipError_t build_plan_tables(muonbp_ctx* c, int full) {
     const int32_t S = int32_t(p.S), Lr = int32_t(p.L), Sp = int32_t(p.Sp), Lp = int32_t(p.Lp);
     for (int q = 0; q < 2; ++q) {
       // A = Z_q Z_q^T
-      gram[q].push_back(GemmDesc{at(p.off_z[q]), at(p.off_z[q]), nullptr, at(p.off_a), at(p.off_a),
-                                 S, S, Lr, Lp, Lp, 0, Sp, Sp});
+      gram[q].push_back(GemmDesc{at(p.off_z[q]), at(p.off_z[q]), nullptr, nullptr, at(p.off_a),
+                                 at(p.off_a), S, S, Lr, Lp, Lp, 0, 0, Sp, Sp});
       // Z_{1-q} = a Z_q + B Z_q, also stored transposed.
-      apply[q].push_back(GemmDesc{at(p.off_b), at(p.off_zt[q]), at(p.off_z[q]), at(p.off_z[1 - q]),
-                                  at(p.off_zt[1 - q]), S, Lr, S, Sp, Sp, Lp, Lp, Sp});
+      apply[q].push_back(GemmDesc{at(p.off_b), at(p.off_zt[q]), at(p.off_z[q]), at(p.off_zt[q]),
+                                  at(p.off_z[1 - q]), at(p.off_zt[1 - q]), S, Lr, S, Sp, Sp, Lp,
+                                  Sp, Lp, Sp});
     }
     // B = c A A^T + b A  (A symmetric)
-    poly.push_back(GemmDesc{at(p.off_a), at(p.off_a), at(p.off_a), at(p.off_b), at(p.off_b), S, S, S,
-                            Sp, Sp, Sp, Sp, Sp});
+    poly.push_back(GemmDesc{at(p.off_a), at(p.off_a), at(p.off_a), at(p.off_a), at(p.off_b),
+                            at(p.off_b), S, S, S, Sp, Sp, Sp, Sp, Sp, Sp});
   }
   // Update table: U of every block after K iterations (buffer K mod 2).
   const int fin = o.ns_steps & 1;
