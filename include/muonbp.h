@@ -56,7 +56,7 @@ typedef struct {
 
 /* Options.  Defaults (muonbp_options_default) follow Algorithm 2:
  * K = 5, (a, b, c) = (2, -1.5, 0.5), eps = 1e-7, no Nesterov, no RMS scaling,
- * bf16 params, momentum and NS operands. */
+ * bf16 params, momentum and NS operands, automatic tile shapes. */
 typedef struct {
   int32_t ns_steps;         /* K >= 0, Newton-Schulz iterations (Alg. 2)       */
   float a, b, c;            /* quintic coefficients (Alg. 2)                   */
@@ -71,6 +71,10 @@ typedef struct {
   muonbp_dtype param_dtype; /* dtype of params and grads                       */
   muonbp_dtype state_dtype; /* dtype of the momentum buffer                    */
   muonbp_dtype ns_dtype;    /* dtype of NS operands (fp32 accumulate always)   */
+  int32_t tile_policy;      /* NS GEMM workgroup tile: 0 = chosen per launch
+                               from its tile counts; 1 = 128x128,
+                               2 = 256x128, 3 = 256x256 (the symmetric
+                               products fall back to 128x128 for 2)           */
 } muonbp_options;
 
 /* Fill *opt with the defaults above.  NULL is ignored. */
@@ -132,6 +136,7 @@ typedef struct {
   int64_t n_elements;      /* parameters covered                            */
   int64_t gemm_tiles[3];   /* workgroup tiles per NS iteration: Gram, poly,
                               apply                                         */
+  int32_t gemm_tile_rows[3], gemm_tile_cols[3]; /* their tile shapes         */
   double ns_flops;         /* algorithmic NS flops per step: per S x L unit
                               and iteration S(S+1)L + S^2(S+1) + 2S^2 L
                               (symmetric products counted once)             */

@@ -62,6 +62,11 @@ struct GemmDesc {
   int32_t ldx, ldy, ldd, lddt, ldc, ldct;
 };
 
+// Workgroup tile shapes of the NS GEMM (rows x columns of C per workgroup).
+enum GemmVariant : int32_t { kGemm128x128 = 0, kGemm256x128 = 1, kGemm256x256 = 2 };
+constexpr int kGemmTileRows[3] = {128, 256, 256};
+constexpr int kGemmTileCols[3] = {128, 128, 256};
+
 // One workgroup tile of a grouped launch: problem index and packed
 // (tile row << 16 | tile column).
 struct TileRef {

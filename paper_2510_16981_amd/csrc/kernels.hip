@@ -182,17 +182,17 @@ __global__ __launch_bounds__(kThreads) void k_pack(
 
 // ---------------------------------------------------------------- NS GEMM
 //
-// Workgroup tile 128 x 128, 4 waves in a 2 x 2 layout, 64 x 64 per wave as
-// 2 x 2 MFMA 32x32 tiles.  The K loop stages 128-byte K slices of X and Y
-// rows through double-buffered LDS (row pitch 144 B to spread banks); each
-// 16-byte LDS read feeds one v_mfma_f32_32x32x16_bf16 (bf16) or four
-// v_mfma_f32_32x32x2f32 (fp32).  Lanes 0-31 take the even 16-byte chunk of a
-// 32-byte K step, lanes 32-63 the odd one, identically for both operands, so
-// every k is summed exactly once.
+// Grouped C = alpha X Y^T + beta D over a tile list, both operands row-major
+// with K contiguous.  Workgroup tile BM x BN, 256 threads = 4 waves in a
+// 2 x 2 layout, (BM/2) x (BN/2) per wave as TM x TN MFMA 32x32 tiles.  The K
+// loop stages 128-byte K slices of X and Y rows through double-buffered LDS
+// (row pitch 144 B to spread banks); global loads for slice k+1 are issued
+// before the MFMAs of slice k.  Each 16-byte LDS read feeds one
+// v_mfma_f32_32x32x16_bf16 (bf16) or four v_mfma_f32_32x32x2f32 (fp32).
+// Lanes 0-31 take the even 16-byte chunk of a 32-byte K step, lanes 32-63 the
+// odd one, identically for both operands, so every k is summed exactly once.
 
-constexpr int kTile = 128;
 constexpr int kLdsRow = 144;
-constexpr int kLdsOp = kTile * kLdsRow;
 
 template <typename T> struct Mfma;
 template <> struct Mfma<bf16> {
@@ -240,28 +240,22 @@ __device__ __forceinline__ uint4 mask_tail(uint4 v, int nv) {
   return v;
 }
 
-constexpr int kStPitch = kTile + 1;  // fp32 staging row pitch (floats)
-static_assert(kTile * kStPitch * 4 <= 4 * kLdsOp, "staging tile must fit in LDS");
-
-// Writes one 128 x 128 output tile from the fp32 staging tile st.
-// Output element (r, c) of the tile goes to out[(r0 + r) * ldo + c0 + c] with
-// value st(r, c) + beta * add[(r0 + r) * lda + c0 + c]; with `transposed`,
-// st(r, c) is read at st[c * kStPitch + r] (the tile's transpose).
+// Writes nrows x (8 * nchunk) of one wave's staged fp32 rows to out,
+// adding beta * add; `st` row pitch `pitch` floats.  Output row r, chunk c
+// of the staged block is element (r0 + r, c0 + 8c) of out; with `transposed`
+// the staged value is read at st[(8c + e) * pitch + r].
 template <typename T>
-__device__ __forceinline__ void store_tile(const float* st, void* outp, int ldo, const void* addp,
-                                           int lda, float beta, int r0, int c0, int nr, int nc,
-                                           bool transposed) {
-  T* out = static_cast<T*>(outp);
-  const T* add = static_cast<const T*>(addp);
-  constexpr int kChunks = kTile * kTile / 8;
-#pragma unroll 2
-  for (int q = threadIdx.x; q < kChunks; q += kThreads) {
-    const int r = q >> 4, c = (q & 15) * 8;
+__device__ __forceinline__ void store_rows(const float* st, int pitch, int nrows, int nchunk,
+                                           T* out, int ldo, const T* add, int lda, float beta,
+                                           int r0, int c0, int nr, int nc, bool transposed,
+                                           int lane) {
+  for (int q = lane; q < nrows * nchunk; q += 64) {
+    const int r = q / nchunk, c = (q - r * nchunk) * 8;
     const int gr = r0 + r, gc = c0 + c;
     if (gr >= nr || gc >= nc) continue;
     float f[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) f[e] = transposed ? st[(c + e) * kStPitch + r] : st[r * kStPitch + c + e];
+    for (int e = 0; e < 8; ++e) f[e] = transposed ? st[(c + e) * pitch + r] : st[r * pitch + c + e];
     const int64_t oo = int64_t(gr) * ldo + gc, oa = int64_t(gr) * lda + gc;
     if (gc + 8 <= nc) {
       if (add) {
@@ -281,66 +275,81 @@ __device__ __forceinline__ void store_tile(const float* st, void* outp, int ldo,
   }
 }
 
-template <typename T>
+template <typename T, int BM, int BN>
+struct GemmShape {
+  static constexpr int EPV = 16 / sizeof(T);  // elements per 16-byte slice
+  static constexpr int BK = 8 * EPV;          // elements per 128-byte K slice
+  static constexpr int TM = BM / 64;          // MFMA tiles per wave, rows
+  static constexpr int TN = BN / 64;          // MFMA tiles per wave, columns
+  static constexpr int QX = BM * 8 / 256;     // 16-byte X slices per thread per stage
+  static constexpr int QY = BN * 8 / 256;
+  static constexpr int LDS_X = BM * kLdsRow;
+  static constexpr int LDS_STAGE = (BM + BN) * kLdsRow;
+  static constexpr int ST_PITCH = 32 * TN + 1;  // epilogue staging pitch (floats)
+  static constexpr int LDS_EPI = 4 * 32 * ST_PITCH * 4;
+  static constexpr int LDS_BYTES = 2 * LDS_STAGE > LDS_EPI ? 2 * LDS_STAGE : LDS_EPI;
+};
+
+template <typename T, int BM, int BN>
 __global__ __launch_bounds__(kThreads) void k_ns_gemm(const GemmDesc* __restrict__ probs,
                                                       const TileRef* __restrict__ tiles,
                                                       float alpha, float beta, int sym) {
-  constexpr int EPV = 16 / sizeof(T);
-  constexpr int BK = 8 * EPV;  // elements per 128-byte K slice
-  __shared__ __attribute__((aligned(16))) unsigned char lds[4 * kLdsOp];
+  using G = GemmShape<T, BM, BN>;
+  constexpr int EPV = G::EPV, BK = G::BK, TM = G::TM, TN = G::TN, QX = G::QX, QY = G::QY;
+  __shared__ __attribute__((aligned(16))) unsigned char lds[G::LDS_BYTES];
 
   const TileRef t = tiles[blockIdx.x];
   const GemmDesc d = probs[t.prob];
   const int ti = t.ij >> 16, tj = t.ij & 0xffff;
-  const int m0 = ti * kTile, n0 = tj * kTile;
+  const int m0 = ti * BM, n0 = tj * BN;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
+
   // Rows beyond M (N) are clamped to a valid row: they only feed output rows
   // (columns) that are never stored.  Columns at or beyond K are masked to
   // zero in the last K slice, which may straddle K (rows are padded to a
   // multiple of 8 elements, so the 16-byte read stays inside the row).
   const int kc = (tid & 7) * EPV;  // this thread's column inside a K slice
-  const T* xrow[4];
-  const T* yrow[4];
+  const T* xrow[QX];
+  const T* yrow[QY];
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int row = (tid + kThreads * q) >> 3;
-    xrow[q] = static_cast<const T*>(d.X) + int64_t(min(m0 + row, d.M - 1)) * d.ldx;
-    yrow[q] = static_cast<const T*>(d.Y) + int64_t(min(n0 + row, d.N - 1)) * d.ldy;
-  }
-  uint4 rx[4], ry[4];
+  for (int q = 0; q < QX; ++q)
+    xrow[q] = static_cast<const T*>(d.X) + int64_t(min(m0 + ((tid + kThreads * q) >> 3), d.M - 1)) * d.ldx;
+#pragma unroll
+  for (int q = 0; q < QY; ++q)
+    yrow[q] = static_cast<const T*>(d.Y) + int64_t(min(n0 + ((tid + kThreads * q) >> 3), d.N - 1)) * d.ldy;
+  uint4 rx[QX], ry[QY];
   auto gload = [&](int k0) {
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      rx[q] = gld16(xrow[q] + k0 + kc);
-      ry[q] = gld16(yrow[q] + k0 + kc);
-    }
+    for (int q = 0; q < QX; ++q) rx[q] = gld16(xrow[q] + k0 + kc);
+#pragma unroll
+    for (int q = 0; q < QY; ++q) ry[q] = gld16(yrow[q] + k0 + kc);
   };
   auto gload_tail = [&](int k0) {
     const int kk = k0 + kc;
     const int nv = max(0, min(d.K - kk, EPV));
     const int o = nv > 0 ? kk : 0;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      rx[q] = mask_tail<T>(gld16(xrow[q] + o), nv);
-      ry[q] = mask_tail<T>(gld16(yrow[q] + o), nv);
-    }
+    for (int q = 0; q < QX; ++q) rx[q] = mask_tail<T>(gld16(xrow[q] + o), nv);
+#pragma unroll
+    for (int q = 0; q < QY; ++q) ry[q] = mask_tail<T>(gld16(yrow[q] + o), nv);
   };
   auto lstore = [&](int buf) {
+    unsigned char* base = lds + buf * G::LDS_STAGE;
+    const int off = (tid >> 3) * kLdsRow + (tid & 7) * 16;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int v = tid + kThreads * q;
-      const int off = (v >> 3) * kLdsRow + (v & 7) * 16;
-      *reinterpret_cast<uint4*>(lds + (2 * buf) * kLdsOp + off) = rx[q];
-      *reinterpret_cast<uint4*>(lds + (2 * buf + 1) * kLdsOp + off) = ry[q];
-    }
+    for (int q = 0; q < QX; ++q)
+      *reinterpret_cast<uint4*>(base + off + q * 32 * kLdsRow) = rx[q];
+#pragma unroll
+    for (int q = 0; q < QY; ++q)
+      *reinterpret_cast<uint4*>(base + G::LDS_X + off + q * 32 * kLdsRow) = ry[q];
   };
 
-  f32x16_t acc[2][2];
+  f32x16_t acc[TM][TN];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < TM; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < TN; ++j)
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
@@ -348,52 +357,58 @@ __global__ __launch_bounds__(kThreads) void k_ns_gemm(const GemmDesc* __restrict
   if (BK <= d.K) gload(0); else gload_tail(0);
   lstore(0);
   __syncthreads();
+  const int xoff = (wm * 32 * TM + (lane & 31)) * kLdsRow;
+  const int yoff = G::LDS_X + (wn * 32 * TN + (lane & 31)) * kLdsRow;
   for (int kt = 0; kt < nk; ++kt) {
     const int buf = kt & 1;
     if (kt + 1 < nk) {
       if ((kt + 2) * BK <= d.K) gload((kt + 1) * BK); else gload_tail((kt + 1) * BK);
     }
-    const unsigned char* As = lds + (2 * buf) * kLdsOp;
-    const unsigned char* Bs = lds + (2 * buf + 1) * kLdsOp;
+    const unsigned char* S = lds + buf * G::LDS_STAGE;
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
       const int koff = (2 * s + (lane >> 5)) * 16;
-      uint4 a[2], b[2];
+      uint4 a[TM], b[TN];
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
-        a[i] = *reinterpret_cast<const uint4*>(As + (wm * 64 + i * 32 + (lane & 31)) * kLdsRow + koff);
+      for (int i = 0; i < TM; ++i)
+        a[i] = *reinterpret_cast<const uint4*>(S + xoff + i * 32 * kLdsRow + koff);
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
-        b[j] = *reinterpret_cast<const uint4*>(Bs + (wn * 64 + j * 32 + (lane & 31)) * kLdsRow + koff);
+      for (int j = 0; j < TN; ++j)
+        b[j] = *reinterpret_cast<const uint4*>(S + yoff + j * 32 * kLdsRow + koff);
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j) acc[i][j] = Mfma<T>::step(a[i], b[j], acc[i][j]);
+        for (int j = 0; j < TN; ++j) acc[i][j] = Mfma<T>::step(a[i], b[j], acc[i][j]);
     }
     if (kt + 1 < nk) lstore(buf ^ 1);
     __syncthreads();
   }
 
-  // Epilogue.  32x32 accumulator layout: lane l holds column l % 32 and, for
-  // register v, row 8 (v / 4) + 4 (l / 32) + v % 4.  alpha * acc is staged
-  // in LDS as fp32 (odd row pitch: conflict-light row and column reads), then
-  // every thread writes 8-element (16-byte) chunks of C rows and, for the
-  // transposed copy, of Ct rows, adding beta * D (or beta * Dt) in fp32.
-  float* st = reinterpret_cast<float*>(lds);
+  // Epilogue, one MFMA row of the wave's sub-tile at a time.  32x32
+  // accumulator layout: lane l holds column l % 32 and, for register v, row
+  // 8 (v / 4) + 4 (l / 32) + v % 4.  alpha * acc is staged in a wave-private
+  // LDS block (32 rows x 32 TN columns, odd pitch), then written as 16-byte
+  // chunks of C rows and, for the transposed copy, of Ct rows, adding
+  // beta * D (or beta * Dt) in fp32.
+  constexpr int P = G::ST_PITCH;
+  float* st = reinterpret_cast<float*>(lds) + wave * 32 * P;
+  const bool mirror = d.Ct != nullptr && !(sym && ti == tj);
+  const int wr0 = m0 + wm * 32 * TM, wc0 = n0 + wn * 32 * TN;
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < TM; ++i) {
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int col = wn * 64 + j * 32 + (lane & 31);
-      const int rbase = wm * 64 + i * 32 + 4 * (lane >> 5);
+    for (int j = 0; j < TN; ++j)
 #pragma unroll
       for (int v = 0; v < 16; ++v)
-        st[(rbase + 8 * (v >> 2) + (v & 3)) * kStPitch + col] = alpha * acc[i][j][v];
-    }
-  __syncthreads();
-  store_tile<T>(st, d.C, d.ldc, d.D, d.ldd, beta, m0, n0, d.M, d.N, false);
-  if (d.Ct != nullptr && !(sym && ti == tj))
-    store_tile<T>(st, d.Ct, d.ldct, d.Dt, d.lddt, beta, n0, m0, d.N, d.M, true);
+        st[(8 * (v >> 2) + 4 * (lane >> 5) + (v & 3)) * P + j * 32 + (lane & 31)] = alpha * acc[i][j][v];
+    __syncthreads();
+    store_rows<T>(st, P, 32, 4 * TN, static_cast<T*>(d.C), d.ldc, static_cast<const T*>(d.D), d.ldd,
+                  beta, wr0 + 32 * i, wc0, d.M, d.N, false, lane);
+    if (mirror)
+      store_rows<T>(st, P, 32 * TN, 4, static_cast<T*>(d.Ct), d.ldct, static_cast<const T*>(d.Dt),
+                    d.lddt, beta, wc0, wr0 + 32 * i, d.N, d.M, true, lane);
+    __syncthreads();
+  }
 }
 
 // ---------------------------------------------------------------- update
@@ -488,13 +503,27 @@ hipError_t launch_pack(DType mom_t, DType grad_t, DType ns_t, int n_tiles, const
   });
 }
 
-hipError_t launch_ns_gemm(DType ns_t, int n_tiles, const GemmDesc* probs, const TileRef* tiles,
-                          float alpha, float beta, int sym, hipStream_t s) {
+hipError_t launch_ns_gemm(DType ns_t, int variant, int n_tiles, const GemmDesc* probs,
+                          const TileRef* tiles, float alpha, float beta, int sym, hipStream_t s) {
   if (n_tiles <= 0) return hipSuccess;
   return dispatch1(ns_t, [&](auto n) {
     using TN = decltype(n);
-    hipLaunchKernelGGL((k_ns_gemm<TN>), dim3(n_tiles), dim3(kThreads), 0, s, probs, tiles, alpha,
-                       beta, sym);
+    switch (variant) {
+      case kGemm128x128:
+        hipLaunchKernelGGL((k_ns_gemm<TN, 128, 128>), dim3(n_tiles), dim3(kThreads), 0, s, probs,
+                           tiles, alpha, beta, sym);
+        break;
+      case kGemm256x128:
+        hipLaunchKernelGGL((k_ns_gemm<TN, 256, 128>), dim3(n_tiles), dim3(kThreads), 0, s, probs,
+                           tiles, alpha, beta, sym);
+        break;
+      case kGemm256x256:
+        hipLaunchKernelGGL((k_ns_gemm<TN, 256, 256>), dim3(n_tiles), dim3(kThreads), 0, s, probs,
+                           tiles, alpha, beta, sym);
+        break;
+      default:
+        return hipErrorInvalidValue;
+    }
     return hipGetLastError();
   });
 }

@@ -33,9 +33,7 @@ struct PlanDev {
   GemmDesc* gram[2] = {nullptr, nullptr};
   GemmDesc* poly = nullptr;
   GemmDesc* apply[2] = {nullptr, nullptr};
-  TileRef* gram_tiles = nullptr;
-  TileRef* poly_tiles = nullptr;
-  TileRef* apply_tiles = nullptr;
+  TileRef* tiles[3] = {nullptr, nullptr, nullptr};  // per GemmKind
   UpdDesc* upd = nullptr;
   std::vector<UpdDesc> upd_host;  // for muonbp_get_update
 };
@@ -107,6 +105,7 @@ std::string validate_opts(const muonbp_options& o) {
   if (o.nesterov != 0 && o.nesterov != 1) return "nesterov must be 0 or 1";
   if (o.scale_mode != 0 && o.scale_mode != 1) return "scale_mode must be 0 or 1";
   if (!std::isfinite(o.rms_beta)) return "rms_beta must be finite";
+  if (o.tile_policy < 0 || o.tile_policy > 3) return "tile_policy must be in [0, 3]";
   return "";
 }
 
@@ -205,9 +204,8 @@ hipError_t build_plan_tables(muonbp_ctx* c, int full) {
     if ((e = upload(c, &pd.apply[q], apply[q])) != hipSuccess) return e;
   }
   if ((e = upload(c, &pd.poly, poly)) != hipSuccess) return e;
-  if ((e = upload(c, &pd.gram_tiles, plan.gram_tiles)) != hipSuccess) return e;
-  if ((e = upload(c, &pd.poly_tiles, plan.poly_tiles)) != hipSuccess) return e;
-  if ((e = upload(c, &pd.apply_tiles, plan.apply_tiles)) != hipSuccess) return e;
+  for (int k = 0; k < 3; ++k)
+    if ((e = upload(c, &pd.tiles[k], plan.tiles[k])) != hipSuccess) return e;
   if ((e = upload(c, &pd.upd, pd.upd_host)) != hipSuccess) return e;
   return hipSuccess;
 }
@@ -304,6 +302,7 @@ void muonbp_options_default(muonbp_options* o) {
   o->param_dtype = MUONBP_BF16;
   o->state_dtype = MUONBP_BF16;
   o->ns_dtype = MUONBP_BF16;
+  o->tile_policy = 0;
 }
 
 const char* muonbp_status_string(muonbp_status s) {
@@ -339,8 +338,8 @@ muonbp_status muonbp_describe_plan(const muonbp_matrix* mats, int32_t n_mats,
   Layout lay;
   bool shape_err = false;
   try {
-    if (!build_layout(shapes.data(), n_mats, int(dtype_size(o.ns_dtype)), o.ns_steps, &lay,
-                      &shape_err)
+    if (!build_layout(shapes.data(), n_mats, int(dtype_size(o.ns_dtype)), o.ns_steps,
+                      o.tile_policy, &lay, &shape_err)
              .empty())
       return shape_err ? MUONBP_E_SHAPE : MUONBP_E_INVALID;
   } catch (const std::bad_alloc&) {
@@ -350,9 +349,11 @@ muonbp_status muonbp_describe_plan(const muonbp_matrix* mats, int32_t n_mats,
   std::memset(out, 0, sizeof(*out));
   out->n_problems = int64_t(p.probs.size());
   out->n_elements = lay.total_elems;
-  out->gemm_tiles[0] = int64_t(p.gram_tiles.size());
-  out->gemm_tiles[1] = int64_t(p.poly_tiles.size());
-  out->gemm_tiles[2] = int64_t(p.apply_tiles.size());
+  for (int k = 0; k < 3; ++k) {
+    out->gemm_tiles[k] = int64_t(p.tiles[k].size());
+    out->gemm_tile_rows[k] = kGemmTileRows[p.variant[k]];
+    out->gemm_tile_cols[k] = kGemmTileCols[p.variant[k]];
+  }
   out->ns_flops = p.ns_flops;
   out->ns_dense_flops = p.ns_dense_flops;
   const double pb = double(dtype_size(o.param_dtype)), sb = double(dtype_size(o.state_dtype)),
@@ -386,7 +387,7 @@ muonbp_status muonbp_create(const muonbp_matrix* mats, int32_t n_mats, int64_t p
   try {
     bool shape_err = false;
     std::string msg = build_layout(shapes.data(), n_mats, int(dtype_size(o.ns_dtype)), o.ns_steps,
-                                   &c->lay, &shape_err);
+                                   o.tile_policy, &c->lay, &shape_err);
     if (!msg.empty()) {
       free_ctx(c);
       return shape_err ? MUONBP_E_SHAPE : MUONBP_E_INVALID;
@@ -509,15 +510,18 @@ muonbp_status muonbp_step(muonbp_ctx* c, void* const* params, const void* const*
   for (int k = 0; k < o.ns_steps; ++k) {
     const int q = k & 1;
     e = timed(c, 3, [&] {
-      return launch_ns_gemm(tn, int(plan.gram_tiles.size()), pd.gram[q], pd.gram_tiles, 1.f, 0.f, 1, s);
+      return launch_ns_gemm(tn, plan.variant[kGram], int(plan.tiles[kGram].size()), pd.gram[q],
+                            pd.tiles[kGram], 1.f, 0.f, 1, s);
     });
     if (e != hipSuccess) return hip_fail(c, e, "gram");
     e = timed(c, 4, [&] {
-      return launch_ns_gemm(tn, int(plan.poly_tiles.size()), pd.poly, pd.poly_tiles, o.c, o.b, 1, s);
+      return launch_ns_gemm(tn, plan.variant[kPoly], int(plan.tiles[kPoly].size()), pd.poly,
+                            pd.tiles[kPoly], o.c, o.b, 1, s);
     });
     if (e != hipSuccess) return hip_fail(c, e, "poly");
     e = timed(c, 5, [&] {
-      return launch_ns_gemm(tn, int(plan.apply_tiles.size()), pd.apply[q], pd.apply_tiles, 1.f, o.a, 0, s);
+      return launch_ns_gemm(tn, plan.variant[kApply], int(plan.tiles[kApply].size()), pd.apply[q],
+                            pd.tiles[kApply], 1.f, o.a, 0, s);
     });
     if (e != hipSuccess) return hip_fail(c, e, "apply");
   }

@@ -33,25 +33,86 @@ bool place_problem(Problem* p, int64_t* cursor, int64_t align_elems) {
   return *cursor > 0 && *cursor < (int64_t(1) << 46);
 }
 
-void add_tiles(Plan* plan, int32_t prob) {
+void add_pack_tiles(Plan* plan, int32_t prob) {
   const Problem& p = plan->probs[prob];
-  const int64_t ts = ceil_div(p.S, kGemmTile), tl = ceil_div(p.L, kGemmTile);
-  for (int64_t i = 0; i < ts; ++i)
-    for (int64_t j = i; j < ts; ++j) {
-      TileRef t{prob, int32_t((i << 16) | j)};
-      plan->gram_tiles.push_back(t);
-      plan->poly_tiles.push_back(t);
-    }
-  for (int64_t i = 0; i < ts; ++i)
-    for (int64_t j = 0; j < tl; ++j)
-      plan->apply_tiles.push_back(TileRef{prob, int32_t((i << 16) | j)});
   const int64_t pr = ceil_div(p.rows, kPackTile), pc = ceil_div(p.cols, kPackTile);
   for (int64_t i = 0; i < pr; ++i)
     for (int64_t j = 0; j < pc; ++j)
       plan->pack_tiles.push_back(TileRef{prob, int32_t((i << 16) | j)});
 }
 
+// Rows x columns of C for one product of problem p.
+void gemm_dims(const Problem& p, GemmKind kind, int64_t* m, int64_t* n, int64_t* k) {
+  *m = p.S;
+  *n = kind == kApply ? p.L : p.S;
+  *k = kind == kGram ? p.L : p.S;
+}
+
+int64_t count_tiles(const std::vector<Problem>& probs, GemmKind kind, int v) {
+  int64_t n = 0;
+  for (const Problem& p : probs) {
+    int64_t m, c, k;
+    gemm_dims(p, kind, &m, &c, &k);
+    const int64_t tm = ceil_div(m, kGemmTileRows[v]), tn = ceil_div(c, kGemmTileCols[v]);
+    n += kind == kApply ? tm * tn : tm * (tm + 1) / 2;
+  }
+  return n;
+}
+
+void add_gemm_tiles(Plan* plan, GemmKind kind) {
+  const int v = plan->variant[kind];
+  std::vector<TileRef> logical;
+  for (size_t pi = 0; pi < plan->probs.size(); ++pi) {
+    int64_t m, c, k;
+    gemm_dims(plan->probs[pi], kind, &m, &c, &k);
+    const int64_t tm = ceil_div(m, kGemmTileRows[v]), tn = ceil_div(c, kGemmTileCols[v]);
+    for (int64_t i = 0; i < tm; ++i)
+      for (int64_t j = (kind == kApply ? 0 : i); j < tn; ++j)
+        logical.push_back(TileRef{int32_t(pi), int32_t((i << 16) | j)});
+  }
+  plan->tiles[kind] = xcd_order(logical);
+}
+
 }  // namespace
+
+std::vector<TileRef> xcd_order(const std::vector<TileRef>& logical) {
+  const int64_t n = int64_t(logical.size());
+  const int64_t q = n / kNumXCDs, r = n % kNumXCDs;
+  std::vector<TileRef> out(logical.size());
+  for (int64_t w = 0; w < n; ++w) {
+    const int64_t x = w % kNumXCDs, j = w / kNumXCDs;
+    out[w] = logical[x * q + std::min(x, r) + j];
+  }
+  return out;
+}
+
+int32_t choose_variant(const std::vector<Problem>& probs, GemmKind kind, int tile_policy) {
+  const bool sym = kind != kApply;
+  if (tile_policy > 0) {
+    const int v = tile_policy - 1;
+    if (sym && kGemmTileRows[v] != kGemmTileCols[v]) return kGemm128x128;
+    return v;
+  }
+  // Estimated time in units of one 128 x 128 tile on a CU: rounds of
+  // (CUs x workgroups per CU) tiles, each round costing its tile area over a
+  // per-shape efficiency (larger tiles reuse each loaded byte more).
+  struct Shape { int v; int per_cu; double area, eff; };
+  const Shape shapes[3] = {{kGemm128x128, 2, 1.0, 0.6}, {kGemm256x128, 1, 2.0, 0.85},
+                           {kGemm256x256, 1, 4.0, 1.0}};
+  int best = kGemm128x128;
+  double best_t = 0;
+  for (const Shape& sh : shapes) {
+    if (sym && kGemmTileRows[sh.v] != kGemmTileCols[sh.v]) continue;
+    const int64_t n = count_tiles(probs, kind, sh.v);
+    const int64_t slots = int64_t(kNumCUs) * sh.per_cu;
+    const double t = double((n + slots - 1) / slots) * sh.per_cu * sh.area / sh.eff;
+    if (best_t == 0 || t < best_t) {
+      best_t = t;
+      best = sh.v;
+    }
+  }
+  return best;
+}
 
 double ns_unit_flops(int64_t S, int64_t L, int K) {
   const double s = double(S), l = double(L);
@@ -66,11 +127,12 @@ double ns_unit_dense_flops(int64_t S, int64_t L, int K) {
 }
 
 std::string build_layout(const MatrixShape* mats, int32_t n_mats,
-                         int ns_elem_bytes, int ns_steps, Layout* out,
-                         bool* shape_error) {
+                         int ns_elem_bytes, int ns_steps, int tile_policy,
+                         Layout* out, bool* shape_error) {
   *shape_error = false;
   if (!mats || n_mats <= 0) return "mats must be a non-empty array";
   if (ns_steps < 0) return "ns_steps must be >= 0";
+  if (tile_policy < 0 || tile_policy > 3) return "tile_policy must be in [0, 3]";
   Layout L;
   L.mats.assign(mats, mats + n_mats);
   int64_t elems = 0;
@@ -83,7 +145,7 @@ std::string build_layout(const MatrixShape* mats, int32_t n_mats,
       return "matrix " + std::to_string(k) + ": sizes must be positive, at most 2^30, "
              "and the grid must divide rows and cols";
     }
-    if (ceil_div(std::max(m.rows, m.cols), kGemmTile) >= kMaxTiles) {
+    if (ceil_div(std::max(m.rows, m.cols), 64) >= kMaxTiles) {
       *shape_error = true;
       return "matrix " + std::to_string(k) + " is too large";
     }
@@ -139,7 +201,7 @@ std::string build_layout(const MatrixShape* mats, int32_t n_mats,
         p.seg_end = L.blocks[first_block + n_blocks - 1].seg_end;
         if (!place_problem(&p, &cursor, align_elems)) return false;
         plan.probs.push_back(p);
-        add_tiles(&plan, int32_t(plan.probs.size() - 1));
+        add_pack_tiles(&plan, int32_t(plan.probs.size() - 1));
         plan.ns_flops += ns_unit_flops(p.S, p.L, ns_steps);
         plan.ns_dense_flops += ns_unit_dense_flops(p.S, p.L, ns_steps);
         return true;
@@ -156,9 +218,13 @@ std::string build_layout(const MatrixShape* mats, int32_t n_mats,
       bi += nb;
     }
     plan.ws_elems = cursor;
-    if (plan.gram_tiles.size() > size_t(std::numeric_limits<int32_t>::max() / 2) ||
-        plan.apply_tiles.size() > size_t(std::numeric_limits<int32_t>::max() / 2) ||
-        plan.pack_tiles.size() > size_t(std::numeric_limits<int32_t>::max() / 2))
+    for (int kind = 0; kind < 3; ++kind) {
+      plan.variant[kind] = choose_variant(plan.probs, GemmKind(kind), tile_policy);
+      add_gemm_tiles(&plan, GemmKind(kind));
+      if (plan.tiles[kind].size() > size_t(std::numeric_limits<int32_t>::max() / 2))
+        return "too many tiles";
+    }
+    if (plan.pack_tiles.size() > size_t(std::numeric_limits<int32_t>::max() / 2))
       return "too many tiles";
   }
   *out = std::move(L);

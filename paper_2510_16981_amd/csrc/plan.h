@@ -12,8 +12,9 @@
 
 namespace muonbp {
 
-constexpr int kGemmTile = 128;          // square workgroup tile of the NS GEMMs
 constexpr int kPackTile = 64;           // square tile of the pack kernel
+constexpr int kNumCUs = 256;            // MI355X compute units
+constexpr int kNumXCDs = 8;             // dies; workgroups are dealt round-robin
 constexpr int64_t kSegTarget = 16384;   // elements per elementwise workgroup
 constexpr int64_t kWsAlignBytes = 256;  // alignment of every workspace buffer
 
@@ -45,12 +46,16 @@ struct Problem {
   int32_t first_block, n_blocks;
 };
 
+// The three grouped products of one NS iteration.
+enum GemmKind { kGram = 0, kPoly = 1, kApply = 2 };
+
 struct Plan {
   bool full = false;
   std::vector<Problem> probs;
   int64_t ws_elems = 0;
   std::vector<TileRef> pack_tiles;
-  std::vector<TileRef> gram_tiles, poly_tiles, apply_tiles;
+  int32_t variant[3] = {0, 0, 0};     // GemmVariant per GemmKind
+  std::vector<TileRef> tiles[3];      // workgroup order, per GemmKind
   double ns_flops = 0, ns_dense_flops = 0;
 };
 
@@ -64,11 +69,22 @@ struct Layout {
 };
 
 // Validates shapes and builds every table.  ns_elem_bytes sizes the
-// workspace alignment; ns_steps only feeds the flop counts.  Returns "" on
-// success, else a message (with *shape_error telling shape vs. argument).
+// workspace alignment; ns_steps only feeds the flop counts; tile_policy 0
+// picks each launch's tile shape from its tile counts, 1 + GemmVariant
+// forces one shape (square shapes only for the symmetric products).
+// Returns "" on success, else a message (with *shape_error telling shape
+// vs. argument).
 std::string build_layout(const MatrixShape* mats, int32_t n_mats,
-                         int ns_elem_bytes, int ns_steps, Layout* out,
-                         bool* shape_error);
+                         int ns_elem_bytes, int ns_steps, int tile_policy,
+                         Layout* out, bool* shape_error);
+
+// Tile shape the planner picks for one grouped product (exposed for tests).
+int32_t choose_variant(const std::vector<Problem>& probs, GemmKind kind, int tile_policy);
+
+// Workgroup order for a logical tile order: workgroup w runs on XCD w % 8, so
+// each XCD receives a contiguous run of logical tiles (shared operands stay
+// in that XCD's L2).
+std::vector<TileRef> xcd_order(const std::vector<TileRef>& logical);
 
 // Per-step flops of NS on one S x L unit for K iterations.
 double ns_unit_flops(int64_t S, int64_t L, int K);        // symmetric-aware

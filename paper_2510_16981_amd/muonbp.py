@@ -39,12 +39,13 @@ class Options(ctypes.Structure):
                 ("eps", ctypes.c_float), ("nesterov", ctypes.c_int32),
                 ("scale_mode", ctypes.c_int32), ("rms_beta", ctypes.c_float),
                 ("param_dtype", ctypes.c_int), ("state_dtype", ctypes.c_int),
-                ("ns_dtype", ctypes.c_int)]
+                ("ns_dtype", ctypes.c_int), ("tile_policy", ctypes.c_int32)]
 
 
 class PlanInfo(ctypes.Structure):
     _fields_ = [("n_problems", ctypes.c_int64), ("n_elements", ctypes.c_int64),
-                ("gemm_tiles", ctypes.c_int64 * 3), ("ns_flops", ctypes.c_double),
+                ("gemm_tiles", ctypes.c_int64 * 3), ("gemm_tile_rows", ctypes.c_int32 * 3),
+                ("gemm_tile_cols", ctypes.c_int32 * 3), ("ns_flops", ctypes.c_double),
                 ("ns_dense_flops", ctypes.c_double),
                 ("elementwise_bytes", ctypes.c_double),
                 ("workspace_bytes", ctypes.c_int64)]

@@ -112,15 +112,18 @@ def test_describe_plan_counts_and_flops(lib, name):
         dense = sum(O.ns_dense_flops(p, q, 5) for p, q in units)
         assert abs(info.ns_dense_flops - dense) <= 1e-9 * dense
         sym = 0.0
-        gram = apply = 0
+        gram = poly = apply = 0
+        (gr_, pr_, ar_), (gc_, pc_, ac_) = info.gemm_tile_rows, info.gemm_tile_cols
+        assert gr_ == gc_ and pr_ == pc_  # symmetric products use square tiles
         for p, q in units:
             S, L = min(p, q), max(p, q)
             sym += 5 * (S * (S + 1) * L + S * S * (S + 1) + 2 * S * S * L)
-            ts, tl = -(-S // 128), -(-L // 128)
-            gram += ts * (ts + 1) // 2
-            apply += ts * tl
+            tg, tp = -(-S // gr_), -(-S // pr_)
+            gram += tg * (tg + 1) // 2
+            poly += tp * (tp + 1) // 2
+            apply += -(-S // ar_) * -(-L // ac_)
         assert abs(info.ns_flops - sym) <= 1e-9 * sym
-        assert info.gemm_tiles[0] == gram and info.gemm_tiles[1] == gram
+        assert info.gemm_tiles[0] == gram and info.gemm_tiles[1] == poly
         assert info.gemm_tiles[2] == apply
         assert info.workspace_bytes > 0
 
@@ -134,6 +137,15 @@ def test_describe_plan_qkv_numbers(lib):
     assert abs(full.ns_dense_flops / 1e12 - 0.6013) < 5e-4
     assert abs(blk.ns_flops / 1e12 - 0.1632) < 5e-4
     assert abs(full.ns_flops / 1e12 - 0.4296) < 5e-4
+
+
+@pytest.mark.parametrize("policy,shape", [(1, (128, 128)), (2, (256, 128)), (3, (256, 256))])
+def test_tile_policy_forces_shape(lib, policy, shape):
+    mats = W.workload_matrices("qkv-2048x6144-bf16")
+    info = mb.describe_plan(mats, False, mb.options_default(tile_policy=policy))
+    assert (info.gemm_tile_rows[2], info.gemm_tile_cols[2]) == shape
+    sq = shape if shape[0] == shape[1] else (128, 128)
+    assert (info.gemm_tile_rows[0], info.gemm_tile_cols[0]) == sq
 
 
 def test_describe_plan_rejects_bad_grid(lib):

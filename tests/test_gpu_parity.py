@@ -79,6 +79,21 @@ def test_ragged_shapes_fp32(mats):
     _check(res, F32_TOL, free_u_tol=F32_TOL)
 
 
+BIG_RAGGED = [(520, 1000, 1, 2), (1000, 264, 2, 1), (300, 300, 1, 1)]
+
+
+@pytest.mark.parametrize("policy", [1, 2, 3], ids=["128x128", "256x128", "256x256"])
+@pytest.mark.parametrize("ns", ["bf16", "f32"])
+def test_every_tile_shape(policy, ns):
+    """Each NS GEMM tile shape, forced, on units spanning several tiles with
+    ragged edges in M, N and K (S = 264, 300, 500; L up to 1000)."""
+    announce(f"tile policy {policy} ns={ns}")
+    st = "f32" if ns == "f32" else "bf16"
+    res = run_case(Case(mats=BIG_RAGGED, period=2, steps=3, param=st, state=st, ns=ns,
+                        tile_policy=policy))
+    _check(res, F32_TOL if ns == "f32" else BF16_TOL)
+
+
 @pytest.mark.parametrize("param,state,ns", [("bf16", "f32", "bf16"), ("f32", "f32", "bf16"),
                                             ("f32", "bf16", "f32"), ("bf16", "bf16", "f32")])
 def test_dtype_combinations(param, state, ns):
