@@ -153,8 +153,8 @@ def main():
         prof = opt.profile_read()
         opt.profile_enable(False)
         torch.cuda.synchronize()
-        ns_ms = sum(prof[k][0] for k in ("gram", "poly", "apply"))
-        ns_launches = sum(prof[k][1] for k in ("gram", "poly", "apply"))
+        ns_ms = sum(prof[k][0] for k in mb.NS_KINDS)
+        ns_launches = sum(prof[k][1] for k in mb.NS_KINDS)
         flops = plan_flops(mats, kind == "full", K) * steps_kind
         info = mb.describe_plan(mats, kind == "full", opt.options)
         per[kind] = {

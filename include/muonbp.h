@@ -71,10 +71,14 @@ typedef struct {
   muonbp_dtype param_dtype; /* dtype of params and grads                       */
   muonbp_dtype state_dtype; /* dtype of the momentum buffer                    */
   muonbp_dtype ns_dtype;    /* dtype of NS operands (fp32 accumulate always)   */
-  int32_t tile_policy;      /* NS GEMM workgroup tile: 0 = chosen per launch
-                               from its tile counts; 1 = 128x128,
-                               2 = 256x128, 3 = 256x256 (the symmetric
-                               products fall back to 128x128 for 2)           */
+  int32_t tile_policy;      /* NS GEMM kernel: 0 = chosen per launch from its
+                               tile counts; 1/2/3 = 128x128 / 256x128 /
+                               256x256 tiles with a register-staged K loop;
+                               4/5/6 = the same tiles with an LDS-DMA K loop
+                               (bf16 NS only, K a multiple of 8, else the
+                               register loop); 7 = 128x128 tiles with the K
+                               loop split over two 4-wave groups.  Symmetric
+                               products use square tiles (128x128 for 2, 5). */
 } muonbp_options;
 
 /* Fill *opt with the defaults above.  NULL is ignored. */
@@ -137,6 +141,7 @@ typedef struct {
   int64_t gemm_tiles[3];   /* workgroup tiles per NS iteration: Gram, poly,
                               apply                                         */
   int32_t gemm_tile_rows[3], gemm_tile_cols[3]; /* their tile shapes         */
+  int64_t gemm_launches;   /* grouped GEMM launches per step (3 K)          */
   double ns_flops;         /* algorithmic NS flops per step: per S x L unit
                               and iteration S(S+1)L + S^2(S+1) + 2S^2 L
                               (symmetric products counted once)             */

@@ -48,9 +48,10 @@ struct PackDesc {
 };
 
 // One product of a grouped NS launch, all row-major with K contiguous:
-//   C[i][j] = alpha * sum_k X[i][k] Y[j][k] + beta * D[i][j]
-// and, when Ct is set, Ct[j][i] = alpha * sum_k X[i][k] Y[j][k] + beta * Dt[j][i]
-// where Dt holds D transposed (the same values, so Ct = C^T).
+//   C[i][j] = alpha * sum_k X[i][k] Y[j][k] + beta * D[i][j] + gamma [i == j]
+// and, when Ct is set, Ct[j][i] = the same value (Dt holds D transposed).
+// sym: the product is symmetric; its tile list holds upper tiles only and
+// the mirror write (Ct = C) is skipped on diagonal tiles.
 struct GemmDesc {
   const void* X;
   const void* Y;
@@ -60,12 +61,24 @@ struct GemmDesc {
   void* Ct;
   int32_t M, N, K;
   int32_t ldx, ldy, ldd, lddt, ldc, ldct;
+  float alpha, beta, gamma;
+  int32_t sym;
 };
 
-// Workgroup tile shapes of the NS GEMM (rows x columns of C per workgroup).
-enum GemmVariant : int32_t { kGemm128x128 = 0, kGemm256x128 = 1, kGemm256x256 = 2 };
-constexpr int kGemmTileRows[3] = {128, 256, 256};
-constexpr int kGemmTileCols[3] = {128, 128, 256};
+// Workgroup tile shapes of the NS GEMM (rows x columns of C per workgroup):
+// register-staged K loop (any dtype, any K) or LDS-DMA K loop (bf16, K a
+// multiple of 8).
+// kGemm128x128Split2 runs two K halves of each tile in one 8-wave
+// workgroup; the DMA kernels keep 3 K slices in flight.
+enum GemmVariant : int32_t {
+  kGemm128x128 = 0, kGemm256x128 = 1, kGemm256x256 = 2,
+  kGemmDma128x128 = 3, kGemmDma256x128 = 4, kGemmDma256x256 = 5,
+  kGemm128x128Split2 = 6,
+  kNumGemmVariants = 7
+};
+constexpr int kGemmTileRows[kNumGemmVariants] = {128, 256, 256, 128, 256, 256, 128};
+constexpr int kGemmTileCols[kNumGemmVariants] = {128, 128, 256, 128, 128, 256, 128};
+constexpr bool kGemmIsDma[kNumGemmVariants] = {false, false, false, true, true, true, false};
 
 // One workgroup tile of a grouped launch: problem index and packed
 // (tile row << 16 | tile column).

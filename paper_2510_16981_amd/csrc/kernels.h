@@ -27,13 +27,11 @@ hipError_t launch_pack(DType mom_t, DType grad_t, DType ns_t, int n_tiles,
                        const float* scales, float mu, int nesterov,
                        hipStream_t s);
 
-// Grouped C = alpha X Y^T + beta D (+ transposed copy) over a tile list
-// whose tile shape is `variant` (GemmVariant in device_types.h).
-// sym: problems are symmetric, the list holds upper tiles and the mirror
-// write (Ct = C) is skipped on diagonal tiles.
+// Grouped C = alpha X Y^T + beta D + gamma I (+ transposed copy) over a
+// tile list whose tile shape is `variant` (GemmVariant in device_types.h);
+// each tile names its problem descriptor, which carries the coefficients.
 hipError_t launch_ns_gemm(DType ns_t, int variant, int n_tiles, const GemmDesc* probs,
-                          const TileRef* tiles, float alpha, float beta,
-                          int sym, hipStream_t s);
+                          const TileRef* tiles, hipStream_t s);
 
 // X <- X (1 - eta lambda) - eta s_b U_b over every block segment.
 hipError_t launch_update(DType param_t, DType ns_t, bool vec, int n_segs,

@@ -10,6 +10,8 @@
 //  * k_update    -- X <- X (1 - eta lambda) - eta s U (Algorithm 1).
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include "kernels.h"
 
 namespace muonbp {
@@ -182,7 +184,8 @@ __global__ __launch_bounds__(kThreads) void k_pack(
 
 // ---------------------------------------------------------------- NS GEMM
 //
-// Grouped C = alpha X Y^T + beta D over a tile list, both operands row-major
+// Grouped C = alpha X Y^T + beta D + gamma I over a tile list (alpha, beta,
+// gamma and the symmetry flag per problem), both operands row-major
 // with K contiguous.  Workgroup tile BM x BN, 256 threads = 4 waves in a
 // 2 x 2 layout, (BM/2) x (BN/2) per wave as TM x TN MFMA 32x32 tiles.  The K
 // loop stages 128-byte K slices of X and Y rows through double-buffered LDS
@@ -223,6 +226,17 @@ __device__ __forceinline__ uint4 gld16(const void* p) {
   return make_uint4(v.x, v.y, v.z, v.w);
 }
 
+// Word 3 of a raw buffer descriptor on CDNA (gfx9 family): 32-bit data
+// format, no swizzle, bounds checked against the byte count in word 2.
+constexpr int kBufferWord3 = 0x00020000;
+
+// 16-byte buffer load at byte offset voff + soff; reads past the
+// descriptor's byte count (checked on voff) return zero.
+__device__ __forceinline__ uint4 bld16(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+  const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
 // Zero the elements of a 16-byte slice at positions >= nv (nv in [0, EPV]).
 template <typename T>
 __device__ __forceinline__ uint4 mask_tail(uint4 v, int nv) {
@@ -240,42 +254,133 @@ __device__ __forceinline__ uint4 mask_tail(uint4 v, int nv) {
   return v;
 }
 
-// Writes nrows x (8 * nchunk) of one wave's staged fp32 rows to out,
-// adding beta * add; `st` row pitch `pitch` floats.  Output row r, chunk c
-// of the staged block is element (r0 + r, c0 + 8c) of out; with `transposed`
-// the staged value is read at st[(8c + e) * pitch + r].
+// f[e] += beta * element e of the 8-element chunk held in v (one 16-byte
+// slice for bf16, two for fp32).
 template <typename T>
-__device__ __forceinline__ void store_rows(const float* st, int pitch, int nrows, int nchunk,
-                                           T* out, int ldo, const T* add, int lda, float beta,
-                                           int r0, int c0, int nr, int nc, bool transposed,
-                                           int lane) {
-  for (int q = lane; q < nrows * nchunk; q += 64) {
-    const int r = q / nchunk, c = (q - r * nchunk) * 8;
-    const int gr = r0 + r, gc = c0 + c;
-    if (gr >= nr || gc >= nc) continue;
-    float f[8];
+__device__ __forceinline__ void add8(float f[8], const uint4* v, float beta);
+template <>
+__device__ __forceinline__ void add8<bf16>(float f[8], const uint4* v, float beta) {
+  const uint32_t w[4] = {v[0].x, v[0].y, v[0].z, v[0].w};
 #pragma unroll
-    for (int e = 0; e < 8; ++e) f[e] = transposed ? st[(c + e) * pitch + r] : st[r * pitch + c + e];
-    const int64_t oo = int64_t(gr) * ldo + gc, oa = int64_t(gr) * lda + gc;
-    if (gc + 8 <= nc) {
-      if (add) {
-        float a8[8];
-        load8(add + oa, a8);
+  for (int i = 0; i < 4; ++i) {
+    f[2 * i] = fmaf(beta, __uint_as_float(w[i] << 16), f[2 * i]);
+    f[2 * i + 1] = fmaf(beta, __uint_as_float(w[i] & 0xffff0000u), f[2 * i + 1]);
+  }
+}
+template <>
+__device__ __forceinline__ void add8<float>(float f[8], const uint4* v, float beta) {
+  const uint32_t w[8] = {v[0].x, v[0].y, v[0].z, v[0].w, v[1].x, v[1].y, v[1].z, v[1].w};
 #pragma unroll
-        for (int e = 0; e < 8; ++e) f[e] = fmaf(beta, a8[e], f[e]);
-      }
-      store8(out + oo, f);
-    } else {
-      for (int e = 0; e < nc - gc; ++e) {
-        float v = f[e];
-        if (add) v = fmaf(beta, to_f<T>(add[oa + e]), v);
-        out[oo + e] = from_f<T>(v);
-      }
-    }
+  for (int i = 0; i < 8; ++i) f[i] = fmaf(beta, __uint_as_float(w[i]), f[i]);
+}
+
+// f[e] += gamma where row == col + e (the diagonal crosses this chunk).
+__device__ __forceinline__ void add_diag(float f[8], int row, int col, float gamma) {
+#pragma unroll
+  for (int e = 0; e < 8; ++e) f[e] += (row == col + e) ? gamma : 0.f;
+}
+
+// Store 8 values at out[row * ld + col ..]: one 16-byte (bf16) or two
+// 16-byte (fp32) stores when the chunk is inside [0, nr) x [0, nc), else the
+// in-range elements one by one.
+template <typename T>
+__device__ __forceinline__ void store_chunk(T* out, int ld, int row, int col, int nr, int nc,
+                                            const float f[8]) {
+  if (row >= nr || col >= nc) return;
+  T* p = out + int64_t(row) * ld + col;
+  if (col + 8 <= nc) {
+    store8(p, f);
+  } else {
+    for (int e = 0; e < nc - col; ++e) p[e] = from_f<T>(f[e]);
   }
 }
 
-template <typename T, int BM, int BN>
+// Epilogue shared by the NS GEMM kernels: writes the workgroup tile at
+// (m0, n0) from the accumulators of its 4 waves (2 x 2 layout, TM x TN MFMA
+// 32x32 tiles each).  st: this wave's free LDS block of 32 * (32 TN + 1)
+// floats.  gamma is added on the diagonal of C (row == column).  Waves with
+// active == false only take part in the workgroup barriers.
+template <typename T, int TM, int TN>
+__device__ __forceinline__ void gemm_epilogue(f32x16_t (&acc)[TM][TN], float* st,
+                                              const GemmDesc& d, int m0, int n0, bool diag,
+                                              float alpha, float beta, float gamma,
+                                              bool active = true) {
+  constexpr int ES = sizeof(T);
+  const int lane = threadIdx.x & 63, wave = (threadIdx.x >> 6) & 3;
+  const int wm = wave >> 1, wn = wave & 1;
+  // Epilogue, one MFMA row of the wave's sub-tile (32 x 32TN) per pass.
+  // The pass's beta * D (and beta * Dt) slices are requested first, as
+  // bounds-checked buffer loads (rows past the matrix read zero; columns
+  // past N only feed values that are not stored), so their latency overlaps
+  // the staging of alpha * acc in a wave-private LDS block (odd pitch).  Then
+  // each lane writes 8-element (16-byte) chunks of C rows and, for the
+  // transposed copy, of Ct rows.  32x32 accumulator layout: lane l holds
+  // column l % 32 and, for register v, row 8 (v / 4) + 4 (l / 32) + v % 4.
+  constexpr int P = 32 * TN + 1;
+  constexpr int NCH = 4 * TN;           // 8-element chunks per staged row
+  constexpr int CPL = 32 * NCH / 64;    // chunks per lane, C and Ct alike
+  const bool mirror = d.Ct != nullptr && !diag;
+  const bool has_d = d.D != nullptr;
+  const int wr0 = m0 + wm * 32 * TM, wc0 = n0 + wn * 32 * TN;
+  const __amdgpu_buffer_rsrc_t dr = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<void*>(has_d ? d.D : d.X), 0, has_d ? d.M * d.ldd * ES : 0, kBufferWord3);
+  const __amdgpu_buffer_rsrc_t dtr = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<void*>(has_d && d.Dt ? d.Dt : d.X), 0, has_d && d.Dt ? d.N * d.lddt * ES : 0,
+      kBufferWord3);
+  T* C = static_cast<T*>(d.C);
+  T* Ct = static_cast<T*>(d.Ct);
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+    const int r0 = wr0 + 32 * i;
+    constexpr int VPC = ES / 2;  // 16-byte slices per 8-element chunk
+    uint4 dv[CPL][VPC], dtv[CPL][VPC];
+    if (has_d && active) {
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) {
+        const int q = lane + 64 * c, r = q / NCH, ch = q - r * NCH;
+        const int o = ((r0 + r) * d.ldd + wc0 + 8 * ch) * ES;
+#pragma unroll
+        for (int h = 0; h < VPC; ++h) dv[c][h] = bld16(dr, o + 16 * h, 0);
+        if (mirror) {
+          const int rr = q >> 2, cc = q & 3;  // Ct row wc0 + rr, columns r0 + 8 cc ..
+          const int ot = ((wc0 + rr) * d.lddt + r0 + 8 * cc) * ES;
+#pragma unroll
+          for (int h = 0; h < VPC; ++h) dtv[c][h] = bld16(dtr, ot + 16 * h, 0);
+        }
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v)
+        st[(8 * (v >> 2) + 4 * (lane >> 5) + (v & 3)) * P + j * 32 + (lane & 31)] = alpha * acc[i][j][v];
+    __syncthreads();
+#pragma unroll
+    for (int c = 0; c < CPL && active; ++c) {
+      const int q = lane + 64 * c, r = q / NCH, ch = q - r * NCH;
+      float f[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) f[e] = st[r * P + 8 * ch + e];
+      if (has_d) add8<T>(f, dv[c], beta);
+      if (gamma != 0.f) add_diag(f, r0 + r, wc0 + 8 * ch, gamma);
+      store_chunk<T>(C, d.ldc, r0 + r, wc0 + 8 * ch, d.M, d.N, f);
+    }
+    if (mirror && active) {
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) {
+        const int q = lane + 64 * c, rr = q >> 2, cc = q & 3;
+        float f[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) f[e] = st[(8 * cc + e) * P + rr];
+        if (has_d) add8<T>(f, dtv[c], beta);
+        store_chunk<T>(Ct, d.ldct, wc0 + rr, r0 + 8 * cc, d.N, d.M, f);
+      }
+    }
+    __syncthreads();
+  }
+}
+
+template <typename T, int BM, int BN, int KS>
 struct GemmShape {
   static constexpr int EPV = 16 / sizeof(T);  // elements per 16-byte slice
   static constexpr int BK = 8 * EPV;          // elements per 128-byte K slice
@@ -286,15 +391,22 @@ struct GemmShape {
   static constexpr int LDS_X = BM * kLdsRow;
   static constexpr int LDS_STAGE = (BM + BN) * kLdsRow;
   static constexpr int ST_PITCH = 32 * TN + 1;  // epilogue staging pitch (floats)
-  static constexpr int LDS_EPI = 4 * 32 * ST_PITCH * 4;
-  static constexpr int LDS_BYTES = 2 * LDS_STAGE > LDS_EPI ? 2 * LDS_STAGE : LDS_EPI;
+  static constexpr int LDS_EPI = KS * 4 * 32 * ST_PITCH * 4;
+  static constexpr int LDS_RED = (KS - 1) * 4 * TM * TN * 16 * 64 * 4;  // split-K partials
+  static constexpr int LDS_LOOP = KS * 2 * LDS_STAGE;
+  static constexpr int LDS_BYTES = LDS_LOOP > LDS_EPI ? (LDS_LOOP > LDS_RED ? LDS_LOOP : LDS_RED)
+                                                      : (LDS_EPI > LDS_RED ? LDS_EPI : LDS_RED);
 };
 
-template <typename T, int BM, int BN>
-__global__ __launch_bounds__(kThreads) void k_ns_gemm(const GemmDesc* __restrict__ probs,
-                                                      const TileRef* __restrict__ tiles,
-                                                      float alpha, float beta, int sym) {
-  using G = GemmShape<T, BM, BN>;
+//
+// KS > 1 splits K inside the workgroup: KS groups of 4 waves each run the
+// K loop over every KS-th slice with their own LDS buffers, and the partial
+// sums are added in LDS (a fixed order) before the epilogue.  Used when a
+// launch has too few tiles to give every CU two workgroups.
+template <typename T, int BM, int BN, int KS>
+__global__ __launch_bounds__(kThreads * KS) void k_ns_gemm(const GemmDesc* __restrict__ probs,
+                                                           const TileRef* __restrict__ tiles) {
+  using G = GemmShape<T, BM, BN, KS>;
   constexpr int EPV = G::EPV, BK = G::BK, TM = G::TM, TN = G::TN, QX = G::QX, QY = G::QY;
   __shared__ __attribute__((aligned(16))) unsigned char lds[G::LDS_BYTES];
 
@@ -302,40 +414,49 @@ __global__ __launch_bounds__(kThreads) void k_ns_gemm(const GemmDesc* __restrict
   const GemmDesc d = probs[t.prob];
   const int ti = t.ij >> 16, tj = t.ij & 0xffff;
   const int m0 = ti * BM, n0 = tj * BN;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int grp = threadIdx.x >> 8;       // K group
+  const int tid = threadIdx.x & 255;      // thread inside the group
+  const int lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
+  unsigned char* glds = lds + grp * 2 * G::LDS_STAGE;
 
-  // Rows beyond M (N) are clamped to a valid row: they only feed output rows
-  // (columns) that are never stored.  Columns at or beyond K are masked to
-  // zero in the last K slice, which may straddle K (rows are padded to a
-  // multiple of 8 elements, so the 16-byte read stays inside the row).
+  // Operands are read with buffer loads: one 32-bit offset per 16-byte slice
+  // (constant over the K loop) plus the K position as a uniform scalar
+  // offset.  Rows at or beyond M (N) lie past the descriptor's byte count and
+  // read as zero; columns at or beyond K are masked to zero in the last K
+  // slice, which may straddle K (rows are padded to a multiple of 8 elements,
+  // so the read stays inside the row).
+  constexpr int ES = sizeof(T);
+  const int xbytes = d.M * d.ldx * ES, ybytes = d.N * d.ldy * ES;
+  const __amdgpu_buffer_rsrc_t xr =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(d.X), 0, xbytes, kBufferWord3);
+  const __amdgpu_buffer_rsrc_t yr =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(d.Y), 0, ybytes, kBufferWord3);
   const int kc = (tid & 7) * EPV;  // this thread's column inside a K slice
-  const T* xrow[QX];
-  const T* yrow[QY];
+  int xo[QX], yo[QY];
 #pragma unroll
-  for (int q = 0; q < QX; ++q)
-    xrow[q] = static_cast<const T*>(d.X) + int64_t(min(m0 + ((tid + kThreads * q) >> 3), d.M - 1)) * d.ldx;
+  for (int q = 0; q < QX; ++q) xo[q] = ((m0 + (tid >> 3) + 32 * q) * d.ldx + kc) * ES;
 #pragma unroll
-  for (int q = 0; q < QY; ++q)
-    yrow[q] = static_cast<const T*>(d.Y) + int64_t(min(n0 + ((tid + kThreads * q) >> 3), d.N - 1)) * d.ldy;
+  for (int q = 0; q < QY; ++q) yo[q] = ((n0 + (tid >> 3) + 32 * q) * d.ldy + kc) * ES;
   uint4 rx[QX], ry[QY];
   auto gload = [&](int k0) {
 #pragma unroll
-    for (int q = 0; q < QX; ++q) rx[q] = gld16(xrow[q] + k0 + kc);
+    for (int q = 0; q < QX; ++q) rx[q] = bld16(xr, xo[q], k0 * ES);
 #pragma unroll
-    for (int q = 0; q < QY; ++q) ry[q] = gld16(yrow[q] + k0 + kc);
+    for (int q = 0; q < QY; ++q) ry[q] = bld16(yr, yo[q], k0 * ES);
   };
+  // A slice entirely past K is read through an out-of-range offset: the
+  // bounds check covers the per-lane offset only (not the scalar K offset),
+  // so this is what keeps such lanes from touching memory past the row.
   auto gload_tail = [&](int k0) {
-    const int kk = k0 + kc;
-    const int nv = max(0, min(d.K - kk, EPV));
-    const int o = nv > 0 ? kk : 0;
+    const int nv = max(0, min(d.K - (k0 + kc), EPV));
 #pragma unroll
-    for (int q = 0; q < QX; ++q) rx[q] = mask_tail<T>(gld16(xrow[q] + o), nv);
+    for (int q = 0; q < QX; ++q) rx[q] = mask_tail<T>(bld16(xr, nv > 0 ? xo[q] : xbytes, k0 * ES), nv);
 #pragma unroll
-    for (int q = 0; q < QY; ++q) ry[q] = mask_tail<T>(gld16(yrow[q] + o), nv);
+    for (int q = 0; q < QY; ++q) ry[q] = mask_tail<T>(bld16(yr, nv > 0 ? yo[q] : ybytes, k0 * ES), nv);
   };
   auto lstore = [&](int buf) {
-    unsigned char* base = lds + buf * G::LDS_STAGE;
+    unsigned char* base = glds + buf * G::LDS_STAGE;
     const int off = (tid >> 3) * kLdsRow + (tid & 7) * 16;
 #pragma unroll
     for (int q = 0; q < QX; ++q)
@@ -353,62 +474,271 @@ __global__ __launch_bounds__(kThreads) void k_ns_gemm(const GemmDesc* __restrict
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
+  // Group grp handles K slices kt = KS it + grp, it < niter (the same count
+  // in every group, so all threads meet every barrier); slices past K load
+  // as zeros.
   const int nk = (d.K + BK - 1) / BK;
-  if (BK <= d.K) gload(0); else gload_tail(0);
+  const int niter = (nk + KS - 1) / KS;
+  auto fetch = [&](int kt) {
+    if ((kt + 1) * BK <= d.K) gload(kt * BK); else gload_tail(kt * BK);
+  };
+  fetch(grp);
   lstore(0);
   __syncthreads();
   const int xoff = (wm * 32 * TM + (lane & 31)) * kLdsRow;
   const int yoff = G::LDS_X + (wn * 32 * TN + (lane & 31)) * kLdsRow;
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) {
-      if ((kt + 2) * BK <= d.K) gload((kt + 1) * BK); else gload_tail((kt + 1) * BK);
-    }
-    const unsigned char* S = lds + buf * G::LDS_STAGE;
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
+  for (int it = 0; it < niter; ++it) {
+    const int buf = it & 1;
+    if (it + 1 < niter) fetch((it + 1) * KS + grp);
+    // Fragments of K step s + 1 are read from LDS before the MFMAs of step s
+    // (two register sets), so LDS latency overlaps the matrix pipeline.
+    const unsigned char* S = glds + buf * G::LDS_STAGE;
+    uint4 a[2][TM], b[2][TN];
+    auto frag = [&](int s, uint4* fa, uint4* fb) {
       const int koff = (2 * s + (lane >> 5)) * 16;
-      uint4 a[TM], b[TN];
 #pragma unroll
       for (int i = 0; i < TM; ++i)
-        a[i] = *reinterpret_cast<const uint4*>(S + xoff + i * 32 * kLdsRow + koff);
+        fa[i] = *reinterpret_cast<const uint4*>(S + xoff + i * 32 * kLdsRow + koff);
 #pragma unroll
       for (int j = 0; j < TN; ++j)
-        b[j] = *reinterpret_cast<const uint4*>(S + yoff + j * 32 * kLdsRow + koff);
+        fb[j] = *reinterpret_cast<const uint4*>(S + yoff + j * 32 * kLdsRow + koff);
+    };
+    frag(0, a[0], b[0]);
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      if (s < 3) frag(s + 1, a[(s + 1) & 1], b[(s + 1) & 1]);
+      // Keep the reads above where they are: the scheduler would otherwise
+      // sink each read next to its first use and expose its latency.
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = Mfma<T>::step(a[i], b[j], acc[i][j]);
+        for (int j = 0; j < TN; ++j) acc[i][j] = Mfma<T>::step(a[s & 1][i], b[s & 1][j], acc[i][j]);
+      __builtin_amdgcn_sched_barrier(0);
     }
-    if (kt + 1 < nk) lstore(buf ^ 1);
+    if (it + 1 < niter) lstore(buf ^ 1);
+    __syncthreads();
+  }
+  if (KS > 1) {
+    // Groups 1.. hand their partial sums to group 0 through LDS, register by
+    // register (same lane layout), and group 0 adds them in group order.
+    float* red = reinterpret_cast<float*>(lds);
+    constexpr int PER_WAVE = TM * TN * 16 * 64;
+    if (grp > 0) {
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int v = 0; v < 16; ++v)
+            red[((grp - 1) * 4 + wave) * PER_WAVE + ((i * TN + j) * 16 + v) * 64 + lane] = acc[i][j][v];
+    }
+    __syncthreads();
+    if (grp == 0) {
+      for (int g = 1; g < KS; ++g)
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v)
+              acc[i][j][v] += red[((g - 1) * 4 + wave) * PER_WAVE + ((i * TN + j) * 16 + v) * 64 + lane];
+    }
     __syncthreads();
   }
 
-  // Epilogue, one MFMA row of the wave's sub-tile at a time.  32x32
-  // accumulator layout: lane l holds column l % 32 and, for register v, row
-  // 8 (v / 4) + 4 (l / 32) + v % 4.  alpha * acc is staged in a wave-private
-  // LDS block (32 rows x 32 TN columns, odd pitch), then written as 16-byte
-  // chunks of C rows and, for the transposed copy, of Ct rows, adding
-  // beta * D (or beta * Dt) in fp32.
-  constexpr int P = G::ST_PITCH;
-  float* st = reinterpret_cast<float*>(lds) + wave * 32 * P;
-  const bool mirror = d.Ct != nullptr && !(sym && ti == tj);
-  const int wr0 = m0 + wm * 32 * TM, wc0 = n0 + wn * 32 * TN;
+  gemm_epilogue<T, TM, TN>(acc, reinterpret_cast<float*>(lds) + (threadIdx.x >> 6) * 32 * (32 * TN + 1),
+                           d, m0, n0, ti == tj && d.sym, d.alpha, d.beta, d.gamma, grp == 0);
+}
+
+// ---------------------------------------------------------------- NS GEMM, LDS-DMA pipeline
+//
+// bf16 variant of k_ns_gemm for units whose K is a multiple of 8.  Operand
+// slices go straight from global memory into LDS (buffer_load_dwordx4 ...
+// lds: lane l of a wave writes 16 bytes at the wave's LDS window + 16 l),
+// through a ring of kStages stages of 32-element (64-byte) K slices, kStages
+// - 1 slices ahead of the MFMAs; no registers hold prefetched data.  Inside
+// a stage a row occupies 64 bytes as four 16-byte chunks, chunk c stored at
+// position c ^ swz(row), swz(row) = ((row >> 1) & 3) ^ ((row >> 3) & 1), so
+// that any 8 (or 16) consecutive rows read at the same chunk by one MFMA
+// operand fetch hit distinct LDS banks.  Rows past M (N) and chunks past K
+// are read through an out-of-range offset and land as zeros.
+
+constexpr int kDmaRow = 64;  // bytes per staged row (32 bf16)
+
+// s_waitcnt immediate that waits until at most n vector-memory operations
+// of this wave are outstanding (exp and lgkm counters left at their maxima).
+constexpr int vmcnt_imm(int n) { return (n & 15) | (7 << 4) | (15 << 8) | ((n >> 4) << 14); }
+
+template <int BM, int BN, int NS>
+struct DmaShape {
+  static constexpr int TM = BM / 64, TN = BN / 64;
+  static constexpr int STAGE = (BM + BN) * kDmaRow;     // bytes per stage
+  static constexpr int LPW = (BM + BN) / 64;            // 1 KB loads per wave per stage
+  static constexpr int ST_PITCH = 32 * TN + 1;
+  static constexpr int LDS_EPI = 4 * 32 * ST_PITCH * 4;
+  static constexpr int LDS_BYTES = NS * STAGE > LDS_EPI ? NS * STAGE : LDS_EPI;
+};
+
+// Waits until at most `after` slices of LPW copies each are still in flight
+// for this wave (after in [0, MAXA]; s_waitcnt needs an immediate).
+template <int LPW, int MAXA>
+__device__ __forceinline__ void wait_slices(int after) {
+  if constexpr (MAXA > 0) {
+    if (after >= MAXA) {
+      __builtin_amdgcn_s_waitcnt(vmcnt_imm(MAXA * LPW));
+      return;
+    }
+    wait_slices<LPW, MAXA - 1>(after);
+  } else {
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+  }
+}
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+// One 16-byte buffer load per lane straight into LDS: lane l writes at
+// dst + 16 l; offsets past the descriptor's byte count write zeros.
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, lds_void_t* dst, int voff, int soff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, dst, 16, voff, soff, 0, 0);
+}
+
+__device__ __forceinline__ int swz(int row) { return ((row >> 1) & 3) ^ ((row >> 3) & 1); }
+
+
+// 16-byte LDS read issued without a compiler-inserted wait: the compiler
+// would otherwise make every LDS read wait for all copies into LDS still in
+// flight (it cannot tell the stages apart).  lds_wait() must complete the
+// reads before their registers are used; it takes the fragments as in/out
+// operands so that no use can be scheduled above it.
+__device__ __forceinline__ u32x4_t lds_read16(uint32_t addr) {
+  u32x4_t v;
+  asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(addr));
+  return v;
+}
+
+template <int N>
+__device__ __forceinline__ void lds_wait(u32x4_t (&f)[N]) {
+  static_assert(N == 4 || N == 6 || N == 8, "fragment count");
+  if constexpr (N == 4)
+    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(f[0]), "+v"(f[1]), "+v"(f[2]), "+v"(f[3]));
+  else if constexpr (N == 6)
+    asm volatile("s_waitcnt lgkmcnt(0)"
+                 : "+v"(f[0]), "+v"(f[1]), "+v"(f[2]), "+v"(f[3]), "+v"(f[4]), "+v"(f[5]));
+  else
+    asm volatile("s_waitcnt lgkmcnt(0)"
+                 : "+v"(f[0]), "+v"(f[1]), "+v"(f[2]), "+v"(f[3]), "+v"(f[4]), "+v"(f[5]),
+                   "+v"(f[6]), "+v"(f[7]));
+}
+
+// Workgroup barrier without the memory fence of __syncthreads(): the fence
+// would wait for every copy into LDS still in flight, including the ones the
+// pipeline keeps ahead on purpose.  Completion of the copies that matter is
+// waited for explicitly before it; the memory clobber keeps the compiler from
+// moving memory operations across it.
+__device__ __forceinline__ void barrier_no_fence() { asm volatile("s_barrier" ::: "memory"); }
+
+__device__ __forceinline__ uint32_t lds_addr(const unsigned char* p) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const lds_void_t*)p));
+}
+
+template <int BM, int BN, int NS>
+__global__ __launch_bounds__(kThreads) void k_ns_gemm_dma(const GemmDesc* __restrict__ probs,
+                                                          const TileRef* __restrict__ tiles) {
+  using G = DmaShape<BM, BN, NS>;
+  using T = bf16;
+  constexpr int TM = G::TM, TN = G::TN, LPW = G::LPW, ES = 2, NF = TM + TN;
+  __shared__ __attribute__((aligned(1024))) unsigned char lds[G::LDS_BYTES];
+
+  const TileRef t = tiles[blockIdx.x];
+  const GemmDesc d = probs[t.prob];
+  const int ti = t.ij >> 16, tj = t.ij & 0xffff;
+  const int m0 = ti * BM, n0 = tj * BN;
+  const int tid = threadIdx.x, lane = tid & 63;
+  // The wave index is uniform across the wave; saying so keeps the LDS
+  // window of each copy (held in M0) in a scalar register.
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
+
+  const int xbytes = d.M * d.ldx * ES, ybytes = d.N * d.ldy * ES;
+  const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(d.X), 0, xbytes, kBufferWord3);
+  const __amdgpu_buffer_rsrc_t yr = __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(d.Y), 0, ybytes, kBufferWord3);
+
+  // This lane's share of every stage: copy u = wave + 4 jj covers staged rows
+  // [16 u, 16 u + 16) (X rows first, then Y rows); the lane fills row
+  // 16 u + lane / 4 at physical chunk lane % 4.
+  int voff[LPW], chunk[LPW];
 #pragma unroll
-  for (int i = 0; i < TM; ++i) {
+  for (int jj = 0; jj < LPW; ++jj) {
+    const int u = wave + 4 * jj;
+    const int row = 16 * u + (lane >> 2);  // stage row (X rows, then Y rows)
+    const int c = (lane & 3) ^ swz(row);
+    chunk[jj] = c;
+    voff[jj] = row < BM ? ((m0 + row) * d.ldx + 8 * c) * ES : ((n0 + row - BM) * d.ldy + 8 * c) * ES;
+  }
+  const int nk = (d.K + 31) / 32;
+  auto issue = [&](int kt) {
+    unsigned char* base = lds + (kt % NS) * G::STAGE;
+    const int k0 = kt * 32;
+#pragma unroll
+    for (int jj = 0; jj < LPW; ++jj) {
+      const bool kin = k0 + 8 * chunk[jj] < d.K;
+      lds_void_t* dst = (lds_void_t*)(base + (wave + 4 * jj) * 1024);
+      if (wave + 4 * jj < BM / 16)  // uniform: X rows
+        dma16(xr, dst, kin ? voff[jj] : xbytes, k0 * ES);
+      else
+        dma16(yr, dst, kin ? voff[jj] : ybytes, k0 * ES);
+    }
+  };
+
+  f32x16_t acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
 #pragma unroll
     for (int j = 0; j < TN; ++j)
 #pragma unroll
-      for (int v = 0; v < 16; ++v)
-        st[(8 * (v >> 2) + 4 * (lane >> 5) + (v & 3)) * P + j * 32 + (lane & 31)] = alpha * acc[i][j][v];
-    __syncthreads();
-    store_rows<T>(st, P, 32, 4 * TN, static_cast<T*>(d.C), d.ldc, static_cast<const T*>(d.D), d.ldd,
-                  beta, wr0 + 32 * i, wc0, d.M, d.N, false, lane);
-    if (mirror)
-      store_rows<T>(st, P, 32 * TN, 4, static_cast<T*>(d.Ct), d.ldct, static_cast<const T*>(d.Dt),
-                    d.lddt, beta, wc0, wr0 + 32 * i, d.N, d.M, true, lane);
-    __syncthreads();
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+#pragma unroll
+  for (int s = 0; s < NS - 1; ++s)
+    if (s < nk) issue(s);
+
+  // LDS byte addresses of this lane's fragment rows in stage 0 (chunk
+  // position added per K step).
+  uint32_t fa[NF];
+  int fsw[NF];
+#pragma unroll
+  for (int f = 0; f < NF; ++f) {
+    const int r = f < TM ? wm * 32 * TM + 32 * f + (lane & 31) : BM + wn * 32 * TN + 32 * (f - TM) + (lane & 31);
+    fa[f] = lds_addr(lds) + r * kDmaRow;
+    fsw[f] = swz(r);
   }
+  for (int kt = 0; kt < nk; ++kt) {
+    // Wait until this wave's copies of slice kt have landed (slices issued
+    // later may stay in flight), make every wave's copies visible, refill
+    // the stage consumed one slice ago, then multiply.
+    wait_slices<LPW, NS - 2>(min(nk - 1, kt + NS - 2) - kt);
+    barrier_no_fence();
+    if (kt + NS - 1 < nk) issue(kt + NS - 1);
+    const uint32_t sbase = (kt % NS) * G::STAGE;
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      const int c = 2 * s + (lane >> 5);
+      u32x4_t fr[NF];
+#pragma unroll
+      for (int f = 0; f < NF; ++f) fr[f] = lds_read16(fa[f] + sbase + ((c ^ fsw[f]) << 4));
+      lds_wait(fr);
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = Mfma<T>::step(__builtin_bit_cast(uint4, fr[i]), __builtin_bit_cast(uint4, fr[TM + j]),
+                                    acc[i][j]);
+    }
+  }
+  __syncthreads();
+  gemm_epilogue<T, TM, TN>(acc, reinterpret_cast<float*>(lds) + wave * 32 * (32 * TN + 1), d, m0, n0,
+                           ti == tj && d.sym, d.alpha, d.beta, d.gamma);
 }
 
 // ---------------------------------------------------------------- update
@@ -504,23 +834,44 @@ hipError_t launch_pack(DType mom_t, DType grad_t, DType ns_t, int n_tiles, const
 }
 
 hipError_t launch_ns_gemm(DType ns_t, int variant, int n_tiles, const GemmDesc* probs,
-                          const TileRef* tiles, float alpha, float beta, int sym, hipStream_t s) {
+                          const TileRef* tiles, hipStream_t s) {
   if (n_tiles <= 0) return hipSuccess;
   return dispatch1(ns_t, [&](auto n) {
     using TN = decltype(n);
     switch (variant) {
       case kGemm128x128:
-        hipLaunchKernelGGL((k_ns_gemm<TN, 128, 128>), dim3(n_tiles), dim3(kThreads), 0, s, probs,
-                           tiles, alpha, beta, sym);
+        hipLaunchKernelGGL((k_ns_gemm<TN, 128, 128, 1>), dim3(n_tiles), dim3(kThreads), 0, s, probs,
+                           tiles);
         break;
       case kGemm256x128:
-        hipLaunchKernelGGL((k_ns_gemm<TN, 256, 128>), dim3(n_tiles), dim3(kThreads), 0, s, probs,
-                           tiles, alpha, beta, sym);
+        hipLaunchKernelGGL((k_ns_gemm<TN, 256, 128, 1>), dim3(n_tiles), dim3(kThreads), 0, s, probs,
+                           tiles);
         break;
       case kGemm256x256:
-        hipLaunchKernelGGL((k_ns_gemm<TN, 256, 256>), dim3(n_tiles), dim3(kThreads), 0, s, probs,
-                           tiles, alpha, beta, sym);
+        hipLaunchKernelGGL((k_ns_gemm<TN, 256, 256, 1>), dim3(n_tiles), dim3(kThreads), 0, s, probs,
+                           tiles);
         break;
+      case kGemm128x128Split2:
+        hipLaunchKernelGGL((k_ns_gemm<TN, 128, 128, 2>), dim3(n_tiles), dim3(2 * kThreads), 0, s,
+                           probs, tiles);
+        break;
+      case kGemmDma128x128:
+      case kGemmDma256x128:
+      case kGemmDma256x256:
+        if constexpr (std::is_same<TN, bf16>::value) {
+          if (variant == kGemmDma128x128)
+            hipLaunchKernelGGL((k_ns_gemm_dma<128, 128, 4>), dim3(n_tiles), dim3(kThreads), 0, s,
+                               probs, tiles);
+          else if (variant == kGemmDma256x128)
+            hipLaunchKernelGGL((k_ns_gemm_dma<256, 128, 4>), dim3(n_tiles), dim3(kThreads), 0, s,
+                               probs, tiles);
+          else
+            hipLaunchKernelGGL((k_ns_gemm_dma<256, 256, 4>), dim3(n_tiles), dim3(kThreads), 0, s,
+                               probs, tiles);
+          break;
+        } else {
+          return hipErrorInvalidValue;
+        }
       default:
         return hipErrorInvalidValue;
     }

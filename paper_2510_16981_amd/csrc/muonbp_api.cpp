@@ -30,10 +30,8 @@ struct PlanDev {
   ScaleDesc* scale = nullptr;
   PackDesc* pack = nullptr;
   TileRef* pack_tiles = nullptr;
-  GemmDesc* gram[2] = {nullptr, nullptr};
-  GemmDesc* poly = nullptr;
-  GemmDesc* apply[2] = {nullptr, nullptr};
-  TileRef* tiles[3] = {nullptr, nullptr, nullptr};  // per GemmKind
+  GemmDesc* descs = nullptr;             // kDescPerProblem per problem
+  std::vector<TileRef*> phase_tiles;     // one tile list per launch phase
   UpdDesc* upd = nullptr;
   std::vector<UpdDesc> upd_host;  // for muonbp_get_update
 };
@@ -105,7 +103,7 @@ std::string validate_opts(const muonbp_options& o) {
   if (o.nesterov != 0 && o.nesterov != 1) return "nesterov must be 0 or 1";
   if (o.scale_mode != 0 && o.scale_mode != 1) return "scale_mode must be 0 or 1";
   if (!std::isfinite(o.rms_beta)) return "rms_beta must be finite";
-  if (o.tile_policy < 0 || o.tile_policy > 3) return "tile_policy must be in [0, 3]";
+  if (o.tile_policy < 0 || o.tile_policy > kNumGemmVariants) return "tile_policy out of range";
   return "";
 }
 
@@ -140,7 +138,7 @@ hipError_t build_plan_tables(muonbp_ctx* c, int full) {
 
   std::vector<ScaleDesc> sd;
   std::vector<PackDesc> pk;
-  std::vector<GemmDesc> gram[2], poly, apply[2];
+  std::vector<GemmDesc> descs;
   for (const Problem& p : plan.probs) {
     sd.push_back(ScaleDesc{p.seg_begin, p.seg_end});
     const MatrixShape& m = c->lay.mats[p.mat];
@@ -166,18 +164,19 @@ hipError_t build_plan_tables(muonbp_ctx* c, int full) {
     }
     pk.push_back(d);
     const int32_t S = int32_t(p.S), Lr = int32_t(p.L), Sp = int32_t(p.Sp), Lp = int32_t(p.Lp);
-    for (int q = 0; q < 2; ++q) {
-      // A = Z_q Z_q^T
-      gram[q].push_back(GemmDesc{at(p.off_z[q]), at(p.off_z[q]), nullptr, nullptr, at(p.off_a),
-                                 at(p.off_a), S, S, Lr, Lp, Lp, 0, 0, Sp, Sp});
-      // Z_{1-q} = a Z_q + B Z_q, also stored transposed.
-      apply[q].push_back(GemmDesc{at(p.off_b), at(p.off_zt[q]), at(p.off_z[q]), at(p.off_zt[q]),
-                                  at(p.off_z[1 - q]), at(p.off_zt[1 - q]), S, Lr, S, Sp, Sp, Lp,
-                                  Sp, Lp, Sp});
-    }
-    // B = c A A^T + b A  (A symmetric)
-    poly.push_back(GemmDesc{at(p.off_a), at(p.off_a), at(p.off_a), at(p.off_a), at(p.off_b),
-                            at(p.off_b), S, S, S, Sp, Sp, Sp, Sp, Sp, Sp});
+    // Slots in DescSlot order.  Gram: A = Z_q Z_q^T (symmetric).
+    for (int q = 0; q < 2; ++q)
+      descs.push_back(GemmDesc{at(p.off_z[q]), at(p.off_z[q]), nullptr, nullptr, at(p.off_a),
+                               at(p.off_a), S, S, Lr, Lp, Lp, 0, 0, Sp, Sp, 1.f, 0.f, 0.f, 1});
+    // Polynomial: B = c A A^T + b A + a I (A symmetric; the a I term carries
+    // Algorithm 2's a X into the next product).
+    descs.push_back(GemmDesc{at(p.off_a), at(p.off_a), at(p.off_a), at(p.off_a), at(p.off_b),
+                             at(p.off_b), S, S, S, Sp, Sp, Sp, Sp, Sp, Sp, o.c, o.b, o.a, 1});
+    // Apply: Z_{1-q} = (a I + B) Z_q (= a Z_q + B Z_q), also stored transposed.
+    for (int q = 0; q < 2; ++q)
+      descs.push_back(GemmDesc{at(p.off_b), at(p.off_zt[q]), nullptr, nullptr, at(p.off_z[1 - q]),
+                               at(p.off_zt[1 - q]), S, Lr, S, Sp, Sp, 0, 0, Lp, Sp, 1.f, 0.f, 0.f,
+                               0});
   }
   // Update table: U of every block after K iterations (buffer K mod 2).
   const int fin = o.ns_steps & 1;
@@ -199,13 +198,10 @@ hipError_t build_plan_tables(muonbp_ctx* c, int full) {
   if ((e = upload(c, &pd.scale, sd)) != hipSuccess) return e;
   if ((e = upload(c, &pd.pack, pk)) != hipSuccess) return e;
   if ((e = upload(c, &pd.pack_tiles, plan.pack_tiles)) != hipSuccess) return e;
-  for (int q = 0; q < 2; ++q) {
-    if ((e = upload(c, &pd.gram[q], gram[q])) != hipSuccess) return e;
-    if ((e = upload(c, &pd.apply[q], apply[q])) != hipSuccess) return e;
-  }
-  if ((e = upload(c, &pd.poly, poly)) != hipSuccess) return e;
-  for (int k = 0; k < 3; ++k)
-    if ((e = upload(c, &pd.tiles[k], plan.tiles[k])) != hipSuccess) return e;
+  if ((e = upload(c, &pd.descs, descs)) != hipSuccess) return e;
+  pd.phase_tiles.assign(plan.phases.size(), nullptr);
+  for (size_t ph = 0; ph < plan.phases.size(); ++ph)
+    if ((e = upload(c, &pd.phase_tiles[ph], plan.phases[ph].tiles)) != hipSuccess) return e;
   if ((e = upload(c, &pd.upd, pd.upd_host)) != hipSuccess) return e;
   return hipSuccess;
 }
@@ -350,10 +346,11 @@ muonbp_status muonbp_describe_plan(const muonbp_matrix* mats, int32_t n_mats,
   out->n_problems = int64_t(p.probs.size());
   out->n_elements = lay.total_elems;
   for (int k = 0; k < 3; ++k) {
-    out->gemm_tiles[k] = int64_t(p.tiles[k].size());
+    out->gemm_tiles[k] = p.tiles_per_iter[k];
     out->gemm_tile_rows[k] = kGemmTileRows[p.variant[k]];
     out->gemm_tile_cols[k] = kGemmTileCols[p.variant[k]];
   }
+  out->gemm_launches = int64_t(p.phases.size());
   out->ns_flops = p.ns_flops;
   out->ns_dense_flops = p.ns_dense_flops;
   const double pb = double(dtype_size(o.param_dtype)), sb = double(dtype_size(o.state_dtype)),
@@ -507,23 +504,12 @@ muonbp_status muonbp_step(muonbp_ctx* c, void* const* params, const void* const*
                        c->scales, c->mu, o.nesterov, s);
   });
   if (e != hipSuccess) return hip_fail(c, e, "pack");
-  for (int k = 0; k < o.ns_steps; ++k) {
-    const int q = k & 1;
-    e = timed(c, 3, [&] {
-      return launch_ns_gemm(tn, plan.variant[kGram], int(plan.tiles[kGram].size()), pd.gram[q],
-                            pd.tiles[kGram], 1.f, 0.f, 1, s);
+  for (size_t ph = 0; ph < plan.phases.size(); ++ph) {
+    const GemmPhase& P = plan.phases[ph];
+    e = timed(c, 3 + P.kind, [&] {
+      return launch_ns_gemm(tn, P.variant, int(P.tiles.size()), pd.descs, pd.phase_tiles[ph], s);
     });
-    if (e != hipSuccess) return hip_fail(c, e, "gram");
-    e = timed(c, 4, [&] {
-      return launch_ns_gemm(tn, plan.variant[kPoly], int(plan.tiles[kPoly].size()), pd.poly,
-                            pd.tiles[kPoly], o.c, o.b, 1, s);
-    });
-    if (e != hipSuccess) return hip_fail(c, e, "poly");
-    e = timed(c, 5, [&] {
-      return launch_ns_gemm(tn, plan.variant[kApply], int(plan.tiles[kApply].size()), pd.apply[q],
-                            pd.tiles[kApply], 1.f, o.a, 0, s);
-    });
-    if (e != hipSuccess) return hip_fail(c, e, "apply");
+    if (e != hipSuccess) return hip_fail(c, e, "NS GEMM");
   }
   const float eta = full ? c->lr_full : c->lr_block;
   bool upd_vec = aligned;

@@ -59,18 +59,45 @@ int64_t count_tiles(const std::vector<Problem>& probs, GemmKind kind, int v) {
   return n;
 }
 
-void add_gemm_tiles(Plan* plan, GemmKind kind) {
-  const int v = plan->variant[kind];
-  std::vector<TileRef> logical;
-  for (size_t pi = 0; pi < plan->probs.size(); ++pi) {
-    int64_t m, c, k;
-    gemm_dims(plan->probs[pi], kind, &m, &c, &k);
-    const int64_t tm = ceil_div(m, kGemmTileRows[v]), tn = ceil_div(c, kGemmTileCols[v]);
-    for (int64_t i = 0; i < tm; ++i)
-      for (int64_t j = (kind == kApply ? 0 : i); j < tn; ++j)
-        logical.push_back(TileRef{int32_t(pi), int32_t((i << 16) | j)});
-  }
-  plan->tiles[kind] = xcd_order(logical);
+// Logical tile order of one product of one problem: bands of `group` tile
+// rows, each band walked column by column (rows inside a column first).  An
+// XCD's concurrent tiles then form a group x (tiles / group) block of C that
+// shares `group` X panels and as many Y panels as it has columns, instead of
+// one X panel and a Y panel per tile.
+void append_tiles(const Problem& p, GemmKind kind, int v, int32_t desc,
+                  std::vector<TileRef>* out) {
+  const int64_t group = (kGemmTileRows[v] == 128 && v != kGemm128x128Split2) ? 8 : 4;
+  int64_t m, c, k;
+  gemm_dims(p, kind, &m, &c, &k);
+  const int64_t tm = ceil_div(m, kGemmTileRows[v]), tn = ceil_div(c, kGemmTileCols[v]);
+  for (int64_t g0 = 0; g0 < tm; g0 += group)
+    for (int64_t j = (kind == kApply ? 0 : g0); j < tn; ++j)
+      for (int64_t i = g0; i < std::min(tm, g0 + group); ++i)
+        if (kind == kApply || i <= j) out->push_back(TileRef{desc, int32_t((i << 16) | j)});
+}
+
+int32_t slot_of(GemmKind kind, int iter) {
+  const int q = iter & 1;
+  return kind == kGram ? kSlotGram0 + q : kind == kPoly ? kSlotPoly : kSlotApply0 + q;
+}
+
+// Launch schedule of the K NS iterations: three launches per iteration
+// (every problem's Gram, then polynomial, then apply).
+void build_phases(Plan* plan, int ns_steps) {
+  plan->phases.clear();
+  const int32_t np = int32_t(plan->probs.size());
+  for (int iter = 0; iter < ns_steps; ++iter)
+    for (int kind = 0; kind < 3; ++kind) {
+      GemmPhase phase;
+      phase.variant = plan->variant[kind];
+      phase.kind = kind;
+      std::vector<TileRef> logical;
+      for (int32_t pi = 0; pi < np; ++pi)
+        append_tiles(plan->probs[pi], GemmKind(kind), phase.variant,
+                     pi * kDescPerProblem + slot_of(GemmKind(kind), iter), &logical);
+      phase.tiles = xcd_order(logical);
+      plan->phases.push_back(std::move(phase));
+    }
 }
 
 }  // namespace
@@ -86,32 +113,41 @@ std::vector<TileRef> xcd_order(const std::vector<TileRef>& logical) {
   return out;
 }
 
-int32_t choose_variant(const std::vector<Problem>& probs, GemmKind kind, int tile_policy) {
+bool dma_allowed(const std::vector<Problem>& probs, GemmKind kind, int ns_elem_bytes) {
+  if (ns_elem_bytes != 2) return false;
+  for (const Problem& p : probs) {
+    int64_t m, n, k;
+    gemm_dims(p, kind, &m, &n, &k);
+    if (k % 8 != 0) return false;
+  }
+  return true;
+}
+
+int32_t choose_variant(const std::vector<Problem>& probs, GemmKind kind, int tile_policy,
+                       int ns_elem_bytes) {
   const bool sym = kind != kApply;
+  const bool dma = dma_allowed(probs, kind, ns_elem_bytes);
+  auto usable = [&](int v) {
+    return (!sym || kGemmTileRows[v] == kGemmTileCols[v]) && (!kGemmIsDma[v] || dma);
+  };
   if (tile_policy > 0) {
-    const int v = tile_policy - 1;
-    if (sym && kGemmTileRows[v] != kGemmTileCols[v]) return kGemm128x128;
+    int v = tile_policy - 1;
+    if (kGemmIsDma[v] && !dma) v -= kGemmDma128x128;  // same shape, register K loop
+    if (sym && kGemmTileRows[v] != kGemmTileCols[v]) v = kGemmIsDma[v] ? kGemmDma128x128 : kGemm128x128;
     return v;
   }
-  // Estimated time in units of one 128 x 128 tile on a CU: rounds of
-  // (CUs x workgroups per CU) tiles, each round costing its tile area over a
-  // per-shape efficiency (larger tiles reuse each loaded byte more).
-  struct Shape { int v; int per_cu; double area, eff; };
-  const Shape shapes[3] = {{kGemm128x128, 2, 1.0, 0.6}, {kGemm256x128, 1, 2.0, 0.85},
-                           {kGemm256x256, 1, 4.0, 1.0}};
-  int best = kGemm128x128;
-  double best_t = 0;
-  for (const Shape& sh : shapes) {
-    if (sym && kGemmTileRows[sh.v] != kGemmTileCols[sh.v]) continue;
-    const int64_t n = count_tiles(probs, kind, sh.v);
-    const int64_t slots = int64_t(kNumCUs) * sh.per_cu;
-    const double t = double((n + slots - 1) / slots) * sh.per_cu * sh.area / sh.eff;
-    if (best_t == 0 || t < best_t) {
-      best_t = t;
-      best = sh.v;
-    }
-  }
-  return best;
+  // Rules from per-launch measurements on MI355X (NS workloads from one
+  // 2048 x 6144 matrix to 16-layer models): the symmetric products run best
+  // on 128 x 128 tiles; the apply product on 256 x 256 tiles once there are
+  // at least two tiles per CU, else on 128 x 128 tiles.  A launch with fewer
+  // than two 128 x 128 tiles per CU splits each tile's K loop over two
+  // 4-wave groups so that every CU still runs eight waves.
+  const int64_t n128 = count_tiles(probs, kind, kGemm128x128);
+  const int32_t small = n128 < 2 * kNumCUs ? kGemm128x128Split2 : kGemm128x128;
+  if (sym) return small;
+  if (count_tiles(probs, kind, kGemm256x256) >= 2 * kNumCUs)
+    return usable(kGemmDma256x256) ? kGemmDma256x256 : kGemm256x256;
+  return small;
 }
 
 double ns_unit_flops(int64_t S, int64_t L, int K) {
@@ -132,7 +168,7 @@ std::string build_layout(const MatrixShape* mats, int32_t n_mats,
   *shape_error = false;
   if (!mats || n_mats <= 0) return "mats must be a non-empty array";
   if (ns_steps < 0) return "ns_steps must be >= 0";
-  if (tile_policy < 0 || tile_policy > 3) return "tile_policy must be in [0, 3]";
+  if (tile_policy < 0 || tile_policy > kNumGemmVariants) return "tile_policy out of range";
   Layout L;
   L.mats.assign(mats, mats + n_mats);
   int64_t elems = 0;
@@ -219,11 +255,12 @@ std::string build_layout(const MatrixShape* mats, int32_t n_mats,
     }
     plan.ws_elems = cursor;
     for (int kind = 0; kind < 3; ++kind) {
-      plan.variant[kind] = choose_variant(plan.probs, GemmKind(kind), tile_policy);
-      add_gemm_tiles(&plan, GemmKind(kind));
-      if (plan.tiles[kind].size() > size_t(std::numeric_limits<int32_t>::max() / 2))
+      plan.variant[kind] = choose_variant(plan.probs, GemmKind(kind), tile_policy, ns_elem_bytes);
+      plan.tiles_per_iter[kind] = count_tiles(plan.probs, GemmKind(kind), plan.variant[kind]);
+      if (plan.tiles_per_iter[kind] > int64_t(std::numeric_limits<int32_t>::max() / 2))
         return "too many tiles";
     }
+    build_phases(&plan, ns_steps);
     if (plan.pack_tiles.size() > size_t(std::numeric_limits<int32_t>::max() / 2))
       return "too many tiles";
   }

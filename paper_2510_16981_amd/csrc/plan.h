@@ -49,13 +49,27 @@ struct Problem {
 // The three grouped products of one NS iteration.
 enum GemmKind { kGram = 0, kPoly = 1, kApply = 2 };
 
+// GEMM descriptors per problem: Gram reading Z[0] / Z[1], the polynomial,
+// apply reading Z[0] / Z[1].  TileRef::prob of a GEMM tile is
+// problem * kDescPerProblem + slot.
+enum DescSlot { kSlotGram0 = 0, kSlotGram1 = 1, kSlotPoly = 2, kSlotApply0 = 3, kSlotApply1 = 4 };
+constexpr int kDescPerProblem = 5;
+
+// One grouped GEMM launch of a step.
+struct GemmPhase {
+  int32_t variant = 0;         // GemmVariant of every tile
+  int32_t kind = 0;            // GemmKind
+  std::vector<TileRef> tiles;  // workgroup order
+};
+
 struct Plan {
   bool full = false;
   std::vector<Problem> probs;
   int64_t ws_elems = 0;
   std::vector<TileRef> pack_tiles;
   int32_t variant[3] = {0, 0, 0};     // GemmVariant per GemmKind
-  std::vector<TileRef> tiles[3];      // workgroup order, per GemmKind
+  int64_t tiles_per_iter[3] = {0, 0, 0};
+  std::vector<GemmPhase> phases;      // in launch order, 3 per NS iteration
   double ns_flops = 0, ns_dense_flops = 0;
 };
 
@@ -69,17 +83,19 @@ struct Layout {
 };
 
 // Validates shapes and builds every table.  ns_elem_bytes sizes the
-// workspace alignment; ns_steps only feeds the flop counts; tile_policy 0
-// picks each launch's tile shape from its tile counts, 1 + GemmVariant
-// forces one shape (square shapes only for the symmetric products).
+// workspace alignment and allows the bf16-only LDS-DMA kernels; ns_steps
+// only feeds the flop counts; tile_policy 0 picks each launch's tile shape
+// from its tile counts, 1 + GemmVariant forces one (square shapes only for
+// the symmetric products; the register K loop where DMA is not allowed).
 // Returns "" on success, else a message (with *shape_error telling shape
 // vs. argument).
 std::string build_layout(const MatrixShape* mats, int32_t n_mats,
                          int ns_elem_bytes, int ns_steps, int tile_policy,
                          Layout* out, bool* shape_error);
 
-// Tile shape the planner picks for one grouped product (exposed for tests).
-int32_t choose_variant(const std::vector<Problem>& probs, GemmKind kind, int tile_policy);
+// Tile shape the planner picks for one grouped product.
+int32_t choose_variant(const std::vector<Problem>& probs, GemmKind kind, int tile_policy,
+                       int ns_elem_bytes);
 
 // Workgroup order for a logical tile order: workgroup w runs on XCD w % 8, so
 // each XCD receives a contiguous run of logical tiles (shared operands stay

@@ -16,6 +16,7 @@ LIB_PATH = os.path.join(HERE, "libmuonbp.so")
 
 F32, BF16 = 0, 1
 KERNEL_KINDS = ("momentum", "scale", "pack", "gram", "poly", "apply", "update")
+NS_KINDS = ("gram", "poly", "apply")
 
 STATUS = {0: "MUONBP_OK", 1: "MUONBP_E_INVALID", 2: "MUONBP_E_SHAPE",
           3: "MUONBP_E_DTYPE", 4: "MUONBP_E_NOMEM", 5: "MUONBP_E_HIP",
@@ -45,7 +46,8 @@ class Options(ctypes.Structure):
 class PlanInfo(ctypes.Structure):
     _fields_ = [("n_problems", ctypes.c_int64), ("n_elements", ctypes.c_int64),
                 ("gemm_tiles", ctypes.c_int64 * 3), ("gemm_tile_rows", ctypes.c_int32 * 3),
-                ("gemm_tile_cols", ctypes.c_int32 * 3), ("ns_flops", ctypes.c_double),
+                ("gemm_tile_cols", ctypes.c_int32 * 3), ("gemm_launches", ctypes.c_int64),
+                ("ns_flops", ctypes.c_double),
                 ("ns_dense_flops", ctypes.c_double),
                 ("elementwise_bytes", ctypes.c_double),
                 ("workspace_bytes", ctypes.c_int64)]

@@ -139,7 +139,9 @@ def test_describe_plan_qkv_numbers(lib):
     assert abs(full.ns_flops / 1e12 - 0.4296) < 5e-4
 
 
-@pytest.mark.parametrize("policy,shape", [(1, (128, 128)), (2, (256, 128)), (3, (256, 256))])
+@pytest.mark.parametrize("policy,shape", [(1, (128, 128)), (2, (256, 128)), (3, (256, 256)),
+                                          (4, (128, 128)), (5, (256, 128)), (6, (256, 256)),
+                                          (7, (128, 128))])
 def test_tile_policy_forces_shape(lib, policy, shape):
     mats = W.workload_matrices("qkv-2048x6144-bf16")
     info = mb.describe_plan(mats, False, mb.options_default(tile_policy=policy))
@@ -151,3 +153,12 @@ def test_tile_policy_forces_shape(lib, policy, shape):
 def test_describe_plan_rejects_bad_grid(lib):
     with pytest.raises(mb.MuonBPError):
         mb.describe_plan([(10, 10, 3, 1)], False)
+
+
+def test_three_launches_per_iteration(lib):
+    for name in ("qkv-2048x6144-bf16", "llama-32L-d4096-bf16"):
+        for full in (False, True):
+            info = mb.describe_plan(W.workload_matrices(name), full)
+            assert info.gemm_launches == 3 * 5
+    info = mb.describe_plan([(64, 64, 1, 1)], False, mb.options_default(ns_steps=0))
+    assert info.gemm_launches == 0

@@ -82,11 +82,15 @@ def test_ragged_shapes_fp32(mats):
 BIG_RAGGED = [(520, 1000, 1, 2), (1000, 264, 2, 1), (300, 300, 1, 1)]
 
 
-@pytest.mark.parametrize("policy", [1, 2, 3], ids=["128x128", "256x128", "256x256"])
+@pytest.mark.parametrize("policy", [1, 2, 3, 4, 5, 6, 7],
+                         ids=["128x128", "256x128", "256x256", "dma128x128", "dma256x128",
+                              "dma256x256", "128x128split2"])
 @pytest.mark.parametrize("ns", ["bf16", "f32"])
 def test_every_tile_shape(policy, ns):
-    """Each NS GEMM tile shape, forced, on units spanning several tiles with
-    ragged edges in M, N and K (S = 264, 300, 500; L up to 1000)."""
+    """Each NS GEMM kernel, forced, on units spanning several tiles with
+    ragged edges in M, N and K (S = 264, 300, 500; L up to 1000).  The DMA
+    kernels run where K is a multiple of 8 and fall back otherwise (fp32, or
+    the 300 x 300 unit)."""
     announce(f"tile policy {policy} ns={ns}")
     st = "f32" if ns == "f32" else "bf16"
     res = run_case(Case(mats=BIG_RAGGED, period=2, steps=3, param=st, state=st, ns=ns,
@@ -148,26 +152,31 @@ def test_deterministic():
         assert np.array_equal(x, y)
 
 
-def test_blocks_match_independent_shards():
+@pytest.mark.parametrize("policy", [1, 0], ids=["fixed-tiles", "auto-tiles"])
+def test_blocks_match_independent_shards(policy):
     """Each block of a sharded matrix is what a device holding only that
-    shard computes: one context over a 2 x 3 grid equals six single-block
-    contexts, bit for bit (BlockMuon, P = infinity)."""
+    shard computes: one context over a 2 x 3 grid against six single-block
+    contexts (BlockMuon, P = infinity).  With a fixed tile shape the kernels
+    and their summation order are the same, so the results are equal bit
+    for bit; with automatic shapes the batch may pick another kernel (the
+    staggered schedule, split K), so they agree to bf16 rounding."""
     import torch
     from paper_2510_16981_amd import muonbp as mb
     from paper_2510_16981_amd import workload as W
-    announce("sharding equivalence")
+    announce(f"sharding equivalence, tile policy {policy}")
     m, n, gr, gc = 256, 384, 2, 3
     bm, bn = m // gr, n // gc
+    opts = mb.options_default(tile_policy=policy)
     G = [W.quantize(W.lowrank_grad(m, n, 16, 0, 0, t), "bf16").cuda() for t in range(3)]
     X0 = W.quantize(W.init_param(m, n, 0, 0), "bf16").cuda()
-    whole = mb.MuonBP([(m, n, gr, gc)], 0, 0.01, 0.02, 0.9, 0.1)
+    whole = mb.MuonBP([(m, n, gr, gc)], 0, 0.01, 0.02, 0.9, 0.1, options=opts)
     X = X0.clone()
     for t in range(3):
         whole.step([X], [G[t]], t)
     parts = []
     for i in range(gr):
         for j in range(gc):
-            ctx = mb.MuonBP([(bm, bn, 1, 1)], 0, 0.01, 0.02, 0.9, 0.1)
+            ctx = mb.MuonBP([(bm, bn, 1, 1)], 0, 0.01, 0.02, 0.9, 0.1, options=opts)
             Xb = X0[i * bm:(i + 1) * bm, j * bn:(j + 1) * bn].contiguous()
             for t in range(3):
                 Gb = G[t][i * bm:(i + 1) * bm, j * bn:(j + 1) * bn].contiguous()
@@ -177,7 +186,13 @@ def test_blocks_match_independent_shards():
             ctx.close()
     torch.cuda.synchronize()
     for i, j, Xb in parts:
-        assert torch.equal(X[i * bm:(i + 1) * bm, j * bn:(j + 1) * bn], Xb)
+        ref = X[i * bm:(i + 1) * bm, j * bn:(j + 1) * bn]
+        if policy:
+            assert torch.equal(ref, Xb)
+        else:
+            d = (ref.double() - Xb.double()).norm() / (ref.double() - X0[i * bm:(i + 1) * bm,
+                                                                      j * bn:(j + 1) * bn].double()).norm()
+            assert d <= 2e-2, float(d)
     whole.close()
 
 
