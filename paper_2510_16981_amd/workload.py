@@ -48,6 +48,9 @@ WORKLOADS = {
         rank=128, period=5, steps=10),
 }
 
+# Periods swept for the 8B-shaped model (P = 0 stands for infinity).
+PERIOD_SWEEP = [1, 2, 5, 10, 0]
+
 
 def workload_matrices(name: str):
     """List of (rows, cols, grid_rows, grid_cols) for a named workload."""
@@ -81,6 +84,34 @@ def lowrank_grad(m: int, n: int, rank: int, seed: int, k: int, t: int,
 def init_param(m: int, n: int, seed: int, k: int, std: float = 0.02) -> np.ndarray:
     """X_0 for matrix k (float64), N(0, std^2)."""
     return std * _rng(seed, _KIND_PARAM, k).standard_normal((m, n))
+
+
+def device_grad(m: int, n: int, rank: int, seed: int, k: int, noise_std: float = 1e-3,
+                device: str = "cuda"):
+    """Timing-only stand-in for lowrank_grad at model scale, drawn on the GPU
+    (torch): a rank-`rank` product with singular values close to 1/i (the
+    factors are Gaussian with columns scaled to unit expected norm, not
+    orthonormalised) plus N(0, noise_std^2) noise, returned as bf16.  Its
+    values differ from lowrank_grad's; use it only where nothing is checked
+    against the oracle."""
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed(int(seed) * 1000003 + int(k))
+    r = min(rank, m, n)
+    U = torch.randn(m, r, generator=g, device=device) / m ** 0.5
+    V = torch.randn(n, r, generator=g, device=device) / n ** 0.5
+    s = 1.0 / torch.arange(1, r + 1, device=device, dtype=torch.float32)
+    G = (U * s) @ V.T
+    G += noise_std * torch.randn(m, n, generator=g, device=device)
+    return G.to(torch.bfloat16)
+
+
+def device_param(m: int, n: int, seed: int, k: int, std: float = 0.02, device: str = "cuda"):
+    """Timing-only X_0 ~ N(0, std^2) drawn on the GPU, bf16."""
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed(int(seed) * 1000003 + int(k) + 7919)
+    return (std * torch.randn(m, n, generator=g, device=device)).to(torch.bfloat16)
 
 
 def quantize(x: np.ndarray, dtype: str):
