@@ -156,17 +156,26 @@ muonbp_status muonbp_describe_plan(const muonbp_matrix* mats, int32_t n_mats,
                                    const muonbp_options* opt, int32_t full,
                                    muonbp_plan_info* out);
 
-/* Per-kernel timing.  While enabled, every launch of the context is
- * bracketed by HIP events on its stream; muonbp_profile_read synchronises,
- * accumulates the elapsed times per kernel kind and resets the records.
- * Kinds: 0 momentum, 1 scale, 2 pack, 3 gram, 4 poly, 5 apply, 6 update. */
-#define MUONBP_N_KERNEL_KINDS 7
+/* Kernel timing with HIP events on the context's stream.
+ * muonbp_profile_enable(ctx, mode): 0 off; 1 every launch bracketed by its
+ * own pair of events (per-kernel detail; the markers between launches cost
+ * time of their own); 2 one pair per step around the whole sequence of NS
+ * GEMM launches, which then run back to back (kind 7; its launch count is
+ * the number of GEMM launches covered).  muonbp_profile_read synchronises,
+ * returns the elapsed times summed per kind over the records made since the
+ * previous read, and forgets those records.
+ * Kinds: 0 momentum, 1 scale, 2 pack, 3 gram, 4 poly, 5 apply, 6 update,
+ * 7 NS GEMM span.  The *_full_steps fields are the part enqueued by full
+ * steps (block steps: the difference).  E_INVALID for a mode outside 0..2. */
+#define MUONBP_N_KERNEL_KINDS 8
 typedef struct {
-  double ms[MUONBP_N_KERNEL_KINDS];       /* summed kernel time             */
+  double ms[MUONBP_N_KERNEL_KINDS];       /* summed elapsed time, all steps */
   int64_t launches[MUONBP_N_KERNEL_KINDS];
+  double ms_full_steps[MUONBP_N_KERNEL_KINDS];
+  int64_t launches_full_steps[MUONBP_N_KERNEL_KINDS];
 } muonbp_profile;
 
-muonbp_status muonbp_profile_enable(muonbp_ctx* ctx, int32_t enable);
+muonbp_status muonbp_profile_enable(muonbp_ctx* ctx, int32_t mode);
 muonbp_status muonbp_profile_read(muonbp_ctx* ctx, muonbp_profile* out);
 
 /* Static text for a status code. */

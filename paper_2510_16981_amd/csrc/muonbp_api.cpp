@@ -38,6 +38,8 @@ struct PlanDev {
 
 struct ProfRec {
   int kind;
+  int full;      // launched by a full step
+  int launches;  // launches between the two events
   hipEvent_t start, stop;
 };
 
@@ -73,11 +75,10 @@ struct muonbp_ctx {
   bool poisoned = false;
   std::string err;
 
-  bool prof = false;
+  int prof = 0;  // 0 off, 1 every launch, 2 one span over the NS GEMM launches
   std::vector<ProfRec> prof_recs;
   std::vector<hipEvent_t> ev_pool;
-  double prof_ms[MUONBP_N_KERNEL_KINDS] = {};
-  int64_t prof_n[MUONBP_N_KERNEL_KINDS] = {};
+  int prof_full = 0;  // kind of the step being enqueued
 };
 
 namespace {
@@ -215,7 +216,7 @@ void free_ctx(muonbp_ctx* c) {
   }
   for (auto& r : c->prof_recs) {
     (void)hipEventDestroy(r.start);
-    (void)hipEventDestroy(r.stop);
+    if (r.stop) (void)hipEventDestroy(r.stop);
   }
   for (hipEvent_t e : c->ev_pool) (void)hipEventDestroy(e);
   delete c;
@@ -244,7 +245,7 @@ hipEvent_t take_event(muonbp_ctx* c) {
 
 template <typename F>
 hipError_t timed(muonbp_ctx* c, int kind, F&& launch) {
-  if (!c->prof) return launch();
+  if (c->prof != 1) return launch();
   hipEvent_t a = take_event(c), b = take_event(c);
   if (!a || !b) return hipErrorOutOfMemory;
   hipError_t e = hipEventRecord(a, c->stream);
@@ -253,7 +254,23 @@ hipError_t timed(muonbp_ctx* c, int kind, F&& launch) {
   if (e != hipSuccess) return e;
   e = hipEventRecord(b, c->stream);
   if (e != hipSuccess) return e;
-  c->prof_recs.push_back(ProfRec{kind, a, b});
+  c->prof_recs.push_back(ProfRec{kind, c->prof_full, 1, a, b});
+  return hipSuccess;
+}
+
+// Span mode: one event before the first and one after the last NS GEMM
+// launch of a step (kind 7); the launches in between run back to back.
+hipError_t span_mark(muonbp_ctx* c, bool begin, int launches) {
+  if (c->prof != 2 || launches == 0) return hipSuccess;
+  hipEvent_t ev = take_event(c);
+  if (!ev) return hipErrorOutOfMemory;
+  hipError_t e = hipEventRecord(ev, c->stream);
+  if (e != hipSuccess) return e;
+  if (begin) {
+    c->prof_recs.push_back(ProfRec{7, c->prof_full, launches, ev, nullptr});
+  } else {
+    c->prof_recs.back().stop = ev;
+  }
   return hipSuccess;
 }
 
@@ -489,6 +506,7 @@ muonbp_status muonbp_step(muonbp_ctx* c, void* const* params, const void* const*
   const DType tp = dt(o.param_dtype), tm = dt(o.state_dtype), tn = dt(o.ns_dtype);
   const int nsegs = int(c->lay.segs.size());
   const hipStream_t s = c->stream;
+  c->prof_full = full;
 
   e = timed(c, 0, [&] {
     return launch_momentum(tp, tm, aligned, nsegs, c->segs, c->blocks, mats, c->mom, c->mu,
@@ -504,13 +522,16 @@ muonbp_status muonbp_step(muonbp_ctx* c, void* const* params, const void* const*
                        c->scales, c->mu, o.nesterov, s);
   });
   if (e != hipSuccess) return hip_fail(c, e, "pack");
-  for (size_t ph = 0; ph < plan.phases.size(); ++ph) {
+  const int nphases = int(plan.phases.size());
+  if ((e = span_mark(c, true, nphases)) != hipSuccess) return hip_fail(c, e, "profiling event");
+  for (int ph = 0; ph < nphases; ++ph) {
     const GemmPhase& P = plan.phases[ph];
     e = timed(c, 3 + P.kind, [&] {
       return launch_ns_gemm(tn, P.variant, int(P.tiles.size()), pd.descs, pd.phase_tiles[ph], s);
     });
     if (e != hipSuccess) return hip_fail(c, e, "NS GEMM");
   }
+  if ((e = span_mark(c, false, nphases)) != hipSuccess) return hip_fail(c, e, "profiling event");
   const float eta = full ? c->lr_full : c->lr_block;
   bool upd_vec = aligned;
   e = timed(c, 6, [&] {
@@ -597,31 +618,35 @@ muonbp_status muonbp_synchronize(muonbp_ctx* c) {
 
 muonbp_status muonbp_profile_enable(muonbp_ctx* c, int32_t enable) {
   if (!c) return MUONBP_E_INVALID;
-  c->prof = enable != 0;
+  if (enable < 0 || enable > 2) return fail(c, MUONBP_E_INVALID, "profile mode must be 0, 1 or 2");
+  c->prof = enable;
   return MUONBP_OK;
 }
 
 muonbp_status muonbp_profile_read(muonbp_ctx* c, muonbp_profile* out) {
   if (!c || !out) return MUONBP_E_INVALID;
   if (c->poisoned) return fail(c, MUONBP_E_STATE, "context poisoned: " + c->err);
+  *out = muonbp_profile{};
   for (ProfRec& r : c->prof_recs) {
+    if (!r.stop) {  // span left open by a failed step
+      c->ev_pool.push_back(r.start);
+      continue;
+    }
     hipError_t e = hipEventSynchronize(r.stop);
     if (e != hipSuccess) return hip_fail(c, e, "hipEventSynchronize");
     float ms = 0.f;
     e = hipEventElapsedTime(&ms, r.start, r.stop);
     if (e != hipSuccess) return hip_fail(c, e, "hipEventElapsedTime");
-    c->prof_ms[r.kind] += ms;
-    c->prof_n[r.kind] += 1;
+    out->ms[r.kind] += ms;
+    out->launches[r.kind] += r.launches;
+    if (r.full) {
+      out->ms_full_steps[r.kind] += ms;
+      out->launches_full_steps[r.kind] += r.launches;
+    }
     c->ev_pool.push_back(r.start);
     c->ev_pool.push_back(r.stop);
   }
   c->prof_recs.clear();
-  for (int k = 0; k < MUONBP_N_KERNEL_KINDS; ++k) {
-    out->ms[k] = c->prof_ms[k];
-    out->launches[k] = c->prof_n[k];
-    c->prof_ms[k] = 0;
-    c->prof_n[k] = 0;
-  }
   return MUONBP_OK;
 }
 

@@ -15,7 +15,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libmuonbp.so")
 
 F32, BF16 = 0, 1
-KERNEL_KINDS = ("momentum", "scale", "pack", "gram", "poly", "apply", "update")
+KERNEL_KINDS = ("momentum", "scale", "pack", "gram", "poly", "apply", "update", "ns_span")
 NS_KINDS = ("gram", "poly", "apply")
 
 STATUS = {0: "MUONBP_OK", 1: "MUONBP_E_INVALID", 2: "MUONBP_E_SHAPE",
@@ -54,7 +54,9 @@ class PlanInfo(ctypes.Structure):
 
 
 class Profile(ctypes.Structure):
-    _fields_ = [("ms", ctypes.c_double * 7), ("launches", ctypes.c_int64 * 7)]
+    _fields_ = [("ms", ctypes.c_double * 8), ("launches", ctypes.c_int64 * 8),
+                ("ms_full_steps", ctypes.c_double * 8),
+                ("launches_full_steps", ctypes.c_int64 * 8)]
 
 
 _lib = None
@@ -223,13 +225,23 @@ class MuonBP:
     def synchronize(self) -> None:
         self._check(self.lib.muonbp_synchronize(self.ctx), "synchronize")
 
-    def profile_enable(self, on: bool = True) -> None:
-        self._check(self.lib.muonbp_profile_enable(self.ctx, int(bool(on))), "profile_enable")
+    def profile_enable(self, on=True) -> None:
+        """True / 1: events around every launch; 2: one span per step over
+        the NS GEMM launches (kind "ns_span"); False / 0: off."""
+        self._check(self.lib.muonbp_profile_enable(self.ctx, int(on)), "profile_enable")
 
-    def profile_read(self) -> dict:
+    def profile_read(self, split: bool = False) -> dict:
+        """{kind: (ms, launches)} summed over the launches recorded since the
+        last read; with split=True, {"block": {...}, "full": {...}} by the
+        kind of step that enqueued them."""
         p = Profile()
         self._check(self.lib.muonbp_profile_read(self.ctx, ctypes.byref(p)), "profile_read")
-        return {k: (p.ms[i], p.launches[i]) for i, k in enumerate(KERNEL_KINDS)}
+        if not split:
+            return {k: (p.ms[i], p.launches[i]) for i, k in enumerate(KERNEL_KINDS)}
+        return {"full": {k: (p.ms_full_steps[i], p.launches_full_steps[i])
+                         for i, k in enumerate(KERNEL_KINDS)},
+                "block": {k: (p.ms[i] - p.ms_full_steps[i], p.launches[i] - p.launches_full_steps[i])
+                          for i, k in enumerate(KERNEL_KINDS)}}
 
     def close(self) -> None:
         if getattr(self, "ctx", None):
