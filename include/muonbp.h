@@ -77,8 +77,15 @@ typedef struct {
                                4/5/6 = the same tiles with an LDS-DMA K loop
                                (bf16 NS only, K a multiple of 8, else the
                                register loop); 7 = 128x128 tiles with the K
-                               loop split over two 4-wave groups.  Symmetric
-                               products use square tiles (128x128 for 2, 5). */
+                               loop split over two 4-wave groups; 8/9/10 =
+                               128x128 / 256x128 / 256x256 tiles with the
+                               LDS-DMA loop interleaved with the MFMAs (same
+                               conditions as 4-6).  Symmetric products use
+                               square tiles (128x128 for 2, 5, 9). */
+  int32_t k_split;          /* interleaved DMA kernels only: 1..8 = each
+                               tile's K loop shared by that many workgroups
+                               (fp32 partial sums added by the last one to
+                               finish); 0 = no split. */
 } muonbp_options;
 
 /* Fill *opt with the defaults above.  NULL is ignored. */
@@ -148,6 +155,7 @@ typedef struct {
   double ns_dense_flops;   /* Sec. 2.2 cost 2K(2 L S^2 + S^3), S <= L        */
   double elementwise_bytes;/* algorithmic HBM bytes of the non-NS kernels    */
   int64_t workspace_bytes; /* NS workspace this plan needs                  */
+  int32_t gemm_split[3];   /* workgroups sharing one tile's K loop (1 = none) */
 } muonbp_plan_info;
 
 /* Plan description for a set of matrices without creating a context

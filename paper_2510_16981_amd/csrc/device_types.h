@@ -74,17 +74,21 @@ enum GemmVariant : int32_t {
   kGemm128x128 = 0, kGemm256x128 = 1, kGemm256x256 = 2,
   kGemmDma128x128 = 3, kGemmDma256x128 = 4, kGemmDma256x256 = 5,
   kGemm128x128Split2 = 6,
-  kNumGemmVariants = 7
+  kGemmDmaP128x128 = 7, kGemmDmaP256x128 = 8, kGemmDmaP256x256 = 9,
+  kNumGemmVariants = 10
 };
-constexpr int kGemmTileRows[kNumGemmVariants] = {128, 256, 256, 128, 256, 256, 128};
-constexpr int kGemmTileCols[kNumGemmVariants] = {128, 128, 256, 128, 128, 256, 128};
-constexpr bool kGemmIsDma[kNumGemmVariants] = {false, false, false, true, true, true, false};
+constexpr int kGemmTileRows[kNumGemmVariants] = {128, 256, 256, 128, 256, 256, 128, 128, 256, 256};
+constexpr int kGemmTileCols[kNumGemmVariants] = {128, 128, 256, 128, 128, 256, 128, 128, 128, 256};
+constexpr bool kGemmIsDma[kNumGemmVariants] = {false, false, false, true, true, true, false,
+                                               true,  true,  true};
 
 // One workgroup tile of a grouped launch: problem index and packed
 // (tile row << 16 | tile column).
 struct TileRef {
   int32_t prob;
   int32_t ij;
+  int32_t slot;  // K-split launches: index of the tile's partial sums and counter
+  int32_t part;  // K-split launches: which share of the K slices
 };
 
 // Update source of one block for one plan: U window and RMS scale.

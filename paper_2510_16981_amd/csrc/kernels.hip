@@ -741,6 +741,197 @@ __global__ __launch_bounds__(kThreads) void k_ns_gemm_dma(const GemmDesc* __rest
                            ti == tj && d.sym, d.alpha, d.beta, d.gamma);
 }
 
+// ---------------------------------------------------------------- NS GEMM, interleaved DMA pipeline
+//
+// Same operand staging as k_ns_gemm_dma (4-stage ring of 32-element K
+// slices, straight from global memory into LDS), but scheduled so that the
+// matrix pipeline never drains at a slice boundary:
+//
+//   * both K steps of a slice are read from LDS one step ahead, each read
+//     issued between two MFMAs of the previous step;
+//   * the barrier that publishes the next slice sits in the middle of the
+//     current slice's second step (the MFMAs already issued keep running);
+//   * right after it, the copy that refills the slot just consumed and the
+//     reads of the next slice's first step are spread over the remaining
+//     MFMAs.
+//
+// Slices past K are copied too (as zeros, through an out-of-range offset),
+// so the loop has no branches and every wait is a constant count.
+
+//
+// K split (nsplit > 1): the workgroups of one tile each run about 1/nsplit
+// of its K slices (share t.part), store their fp32 sums at
+// ksum[(t.slot * nsplit + part) * BM * BN] (MFMA register order), and count
+// themselves in kcount[t.slot].  The last to arrive adds the nsplit sums in
+// share order (the result does not depend on the arrival order), resets
+// the counter for the next launch and runs the epilogue; the others exit.
+// No workgroup waits for another.
+template <int BM, int BN>
+__global__ __launch_bounds__(kThreads) void k_ns_gemm_dmap(const GemmDesc* __restrict__ probs,
+                                                           const TileRef* __restrict__ tiles,
+                                                           int nsplit, float* __restrict__ ksum,
+                                                           int* __restrict__ kcount) {
+  constexpr int NS = 4;
+  using G = DmaShape<BM, BN, NS>;
+  using T = bf16;
+  constexpr int TM = G::TM, TN = G::TN, LPW = G::LPW, ES = 2, NF = TM + TN;
+  constexpr int NM = TM * TN;  // MFMAs per K step
+  constexpr int H = NM / 2;    // MFMAs of the second step issued before the barrier
+  __shared__ __attribute__((aligned(1024))) unsigned char lds[G::LDS_BYTES];
+
+  const TileRef t = tiles[blockIdx.x];
+  const GemmDesc d = probs[t.prob];
+  const int ti = t.ij >> 16, tj = t.ij & 0xffff;
+  const int m0 = ti * BM, n0 = tj * BN;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
+
+  const int xbytes = d.M * d.ldx * ES, ybytes = d.N * d.ldy * ES;
+  const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(d.X), 0, xbytes, kBufferWord3);
+  const __amdgpu_buffer_rsrc_t yr = __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(d.Y), 0, ybytes, kBufferWord3);
+
+  int voff[LPW], chunk[LPW];
+#pragma unroll
+  for (int jj = 0; jj < LPW; ++jj) {
+    const int u = wave + 4 * jj;
+    const int row = 16 * u + (lane >> 2);
+    const int c = (lane & 3) ^ swz(row);
+    chunk[jj] = c;
+    voff[jj] = row < BM ? ((m0 + row) * d.ldx + 8 * c) * ES : ((n0 + row - BM) * d.ldy + 8 * c) * ES;
+  }
+  const int nk_all = (d.K + 31) / 32;
+  const int kb = nsplit > 1 ? t.part * nk_all / nsplit : 0;
+  const int ke = nsplit > 1 ? (t.part + 1) * nk_all / nsplit : nk_all;
+  // Copy jj of slice kt into its ring slot (slices outside [kb, ke) as zeros).
+  auto copy = [&](int kt, int jj) {
+    unsigned char* base = lds + (kt % NS) * G::STAGE;
+    const int k0 = kt * 32;
+    const bool kin = kt < ke && k0 + 8 * chunk[jj] < d.K;
+    lds_void_t* dst = (lds_void_t*)(base + (wave + 4 * jj) * 1024);
+    if (wave + 4 * jj < BM / 16)  // uniform: X rows
+      dma16(xr, dst, kin ? voff[jj] : xbytes, k0 * ES);
+    else
+      dma16(yr, dst, kin ? voff[jj] : ybytes, k0 * ES);
+  };
+
+  f32x16_t acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+  uint32_t fa[NF];
+  int fsw[NF];
+#pragma unroll
+  for (int f = 0; f < NF; ++f) {
+    const int r = f < TM ? wm * 32 * TM + 32 * f + (lane & 31) : BM + wn * 32 * TN + 32 * (f - TM) + (lane & 31);
+    fa[f] = lds_addr(lds) + r * kDmaRow;
+    fsw[f] = swz(r);
+  }
+  auto read1 = [&](int kt, int s, int f) {
+    const uint32_t sbase = (kt % NS) * G::STAGE;
+    const int c = 2 * s + (lane >> 5);
+    return lds_read16(fa[f] + sbase + ((c ^ fsw[f]) << 4));
+  };
+  auto mfma = [&](const u32x4_t (&fr)[NF], int q) {
+    const int i = q / TN, j = q % TN;
+    acc[i][j] = Mfma<T>::step(__builtin_bit_cast(uint4, fr[i]), __builtin_bit_cast(uint4, fr[TM + j]),
+                              acc[i][j]);
+  };
+
+  // Prologue: fill the ring, publish slice kb, read its first K step.
+#pragma unroll
+  for (int s = 0; s < NS; ++s)
+#pragma unroll
+    for (int jj = 0; jj < LPW; ++jj) copy(kb + s, jj);
+  __builtin_amdgcn_s_waitcnt(vmcnt_imm((NS - 1) * LPW));
+  barrier_no_fence();
+  u32x4_t f0[NF], f1[NF];
+#pragma unroll
+  for (int f = 0; f < NF; ++f) f0[f] = read1(kb, 0, f);
+  lds_wait(f0);
+
+  for (int kt = kb; kt < ke; ++kt) {
+    // Step 0 of slice kt, with the reads of its step 1.
+#pragma unroll
+    for (int q = 0; q < NM; ++q) {
+      mfma(f0, q);
+      if (q < NF) f1[q] = read1(kt, 1, q);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    lds_wait(f1);
+    // Step 1, first part.
+#pragma unroll
+    for (int q = 0; q < H; ++q) {
+      mfma(f1, q);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    // Slice kt + 1 has landed for this wave (two later slices may still be
+    // in flight); after the barrier it has landed for every wave, and no
+    // wave reads slice kt any more, so its slot takes slice kt + NS.
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * LPW));
+    barrier_no_fence();
+    // Step 1, rest, with the reads of slice kt + 1 and the refill copies.
+    constexpr int OPS = LPW + NF;
+#pragma unroll
+    for (int q = H; q < NM; ++q) {
+      mfma(f1, q);
+      constexpr int R = NM - H;
+      const int lo = (q - H) * OPS / R, hi = (q - H + 1) * OPS / R;
+#pragma unroll
+      for (int o = lo; o < hi; ++o) {
+        if (o < NF) f0[o] = read1(kt + 1, 0, o);
+        else copy(kt + NS, o - NF);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    lds_wait(f0);
+  }
+  // Zero-filled copies past the share may still be in flight: let them land
+  // before the epilogue reuses the ring.
+  __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+  if (nsplit > 1) {
+    // The sums are stored and loaded as device-coherent relaxed atomics
+    // (they bypass the per-XCD caches), and every store has completed before
+    // the share is counted.  A device-scope fence would do the same for
+    // plain accesses but writes back and invalidates the whole L2, which
+    // costs the other workgroups their cached operands.
+    constexpr int PER_WAVE = NM * 16 * 64;
+    float* mine = ksum + (size_t(t.slot) * nsplit + t.part) * (BM * BN) + wave * PER_WAVE;
+#pragma unroll
+    for (int q = 0; q < NM; ++q)
+#pragma unroll
+      for (int v = 0; v < 16; ++v)
+        __hip_atomic_store(mine + (q * 16 + v) * 64 + lane, acc[q / TN][q % TN][v], __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+    __shared__ int last;
+    __syncthreads();
+    if (tid == 0)
+      last = __hip_atomic_fetch_add(kcount + t.slot, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+             nsplit - 1;
+    __syncthreads();
+    if (!last) return;
+    const float* all = ksum + size_t(t.slot) * nsplit * (BM * BN) + wave * PER_WAVE;
+    for (int p = 0; p < nsplit; ++p)
+#pragma unroll
+      for (int q = 0; q < NM; ++q)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const float x = __hip_atomic_load(all + size_t(p) * (BM * BN) + (q * 16 + v) * 64 + lane,
+                                            __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          acc[q / TN][q % TN][v] = p == 0 ? x : acc[q / TN][q % TN][v] + x;
+        }
+    if (tid == 0) __hip_atomic_store(kcount + t.slot, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  __syncthreads();
+  gemm_epilogue<T, TM, TN>(acc, reinterpret_cast<float*>(lds) + wave * 32 * (32 * TN + 1), d, m0, n0,
+                           ti == tj && d.sym, d.alpha, d.beta, d.gamma);
+}
+
 // ---------------------------------------------------------------- update
 
 template <typename TP, typename TU, bool VEC>
@@ -834,7 +1025,9 @@ hipError_t launch_pack(DType mom_t, DType grad_t, DType ns_t, int n_tiles, const
 }
 
 hipError_t launch_ns_gemm(DType ns_t, int variant, int n_tiles, const GemmDesc* probs,
-                          const TileRef* tiles, hipStream_t s) {
+                          const TileRef* tiles, int nsplit, float* ksum, int* kcount,
+                          hipStream_t s) {
+  if (nsplit > 1 && (!ksum || !kcount || variant < kGemmDmaP128x128)) return hipErrorInvalidValue;
   if (n_tiles <= 0) return hipSuccess;
   return dispatch1(ns_t, [&](auto n) {
     using TN = decltype(n);
@@ -855,6 +1048,23 @@ hipError_t launch_ns_gemm(DType ns_t, int variant, int n_tiles, const GemmDesc* 
         hipLaunchKernelGGL((k_ns_gemm<TN, 128, 128, 2>), dim3(n_tiles), dim3(2 * kThreads), 0, s,
                            probs, tiles);
         break;
+      case kGemmDmaP128x128:
+      case kGemmDmaP256x128:
+      case kGemmDmaP256x256:
+        if constexpr (std::is_same<TN, bf16>::value) {
+          if (variant == kGemmDmaP128x128)
+            hipLaunchKernelGGL((k_ns_gemm_dmap<128, 128>), dim3(n_tiles), dim3(kThreads), 0, s, probs,
+                               tiles, nsplit, ksum, kcount);
+          else if (variant == kGemmDmaP256x128)
+            hipLaunchKernelGGL((k_ns_gemm_dmap<256, 128>), dim3(n_tiles), dim3(kThreads), 0, s, probs,
+                               tiles, nsplit, ksum, kcount);
+          else
+            hipLaunchKernelGGL((k_ns_gemm_dmap<256, 256>), dim3(n_tiles), dim3(kThreads), 0, s, probs,
+                               tiles, nsplit, ksum, kcount);
+          break;
+        } else {
+          return hipErrorInvalidValue;
+        }
       case kGemmDma128x128:
       case kGemmDma256x128:
       case kGemmDma256x256:

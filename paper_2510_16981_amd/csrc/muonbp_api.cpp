@@ -57,6 +57,8 @@ struct muonbp_ctx {
   void* ws = nullptr;
   float* partials = nullptr;
   float* scales = nullptr;
+  float* ksum = nullptr;   // fp32 partial sums of K-split NS GEMM launches
+  int* kcount = nullptr;   // one arrival counter per tile of such a launch (kept zeroed)
   SegDesc* segs = nullptr;
   BlockDesc* blocks = nullptr;
   PlanDev pd[2];
@@ -105,6 +107,7 @@ std::string validate_opts(const muonbp_options& o) {
   if (o.scale_mode != 0 && o.scale_mode != 1) return "scale_mode must be 0 or 1";
   if (!std::isfinite(o.rms_beta)) return "rms_beta must be finite";
   if (o.tile_policy < 0 || o.tile_policy > kNumGemmVariants) return "tile_policy out of range";
+  if (o.k_split < 0 || o.k_split > kMaxKSplit) return "k_split out of range";
   return "";
 }
 
@@ -316,6 +319,7 @@ void muonbp_options_default(muonbp_options* o) {
   o->state_dtype = MUONBP_BF16;
   o->ns_dtype = MUONBP_BF16;
   o->tile_policy = 0;
+  o->k_split = 0;
 }
 
 const char* muonbp_status_string(muonbp_status s) {
@@ -352,7 +356,7 @@ muonbp_status muonbp_describe_plan(const muonbp_matrix* mats, int32_t n_mats,
   bool shape_err = false;
   try {
     if (!build_layout(shapes.data(), n_mats, int(dtype_size(o.ns_dtype)), o.ns_steps,
-                      o.tile_policy, &lay, &shape_err)
+                      o.tile_policy, o.k_split, &lay, &shape_err)
              .empty())
       return shape_err ? MUONBP_E_SHAPE : MUONBP_E_INVALID;
   } catch (const std::bad_alloc&) {
@@ -366,6 +370,7 @@ muonbp_status muonbp_describe_plan(const muonbp_matrix* mats, int32_t n_mats,
     out->gemm_tiles[k] = p.tiles_per_iter[k];
     out->gemm_tile_rows[k] = kGemmTileRows[p.variant[k]];
     out->gemm_tile_cols[k] = kGemmTileCols[p.variant[k]];
+    out->gemm_split[k] = p.nsplit[k];
   }
   out->gemm_launches = int64_t(p.phases.size());
   out->ns_flops = p.ns_flops;
@@ -401,7 +406,7 @@ muonbp_status muonbp_create(const muonbp_matrix* mats, int32_t n_mats, int64_t p
   try {
     bool shape_err = false;
     std::string msg = build_layout(shapes.data(), n_mats, int(dtype_size(o.ns_dtype)), o.ns_steps,
-                                   o.tile_policy, &c->lay, &shape_err);
+                                   o.tile_policy, o.k_split, &c->lay, &shape_err);
     if (!msg.empty()) {
       free_ctx(c);
       return shape_err ? MUONBP_E_SHAPE : MUONBP_E_INVALID;
@@ -448,6 +453,16 @@ muonbp_status muonbp_create(const muonbp_matrix* mats, int32_t n_mats, int64_t p
   c->partials = static_cast<float*>(p);
   if ((e = dev_alloc(c, &p, n_probs * sizeof(float))) != hipSuccess) return bail(e, "scales");
   c->scales = static_cast<float*>(p);
+  const int64_t split_floats = std::max(c->lay.plan[0].split_floats, c->lay.plan[1].split_floats);
+  const int64_t split_slots = std::max(c->lay.plan[0].split_slots, c->lay.plan[1].split_slots);
+  if (split_slots > 0) {
+    if ((e = dev_alloc(c, &p, size_t(split_floats) * sizeof(float))) != hipSuccess) return bail(e, "split sums");
+    c->ksum = static_cast<float*>(p);
+    if ((e = dev_alloc(c, &p, size_t(split_slots) * sizeof(int))) != hipSuccess) return bail(e, "split counters");
+    c->kcount = static_cast<int*>(p);
+    if ((e = hipMemset(c->kcount, 0, size_t(split_slots) * sizeof(int))) != hipSuccess)
+      return bail(e, "split counters");
+  }
   if ((e = upload(c, &c->segs, c->lay.segs)) != hipSuccess) return bail(e, "segments");
   std::vector<BlockDesc> bd;
   for (const BlockPlan& b : c->lay.blocks) {
@@ -527,7 +542,8 @@ muonbp_status muonbp_step(muonbp_ctx* c, void* const* params, const void* const*
   for (int ph = 0; ph < nphases; ++ph) {
     const GemmPhase& P = plan.phases[ph];
     e = timed(c, 3 + P.kind, [&] {
-      return launch_ns_gemm(tn, P.variant, int(P.tiles.size()), pd.descs, pd.phase_tiles[ph], s);
+      return launch_ns_gemm(tn, P.variant, int(P.tiles.size()), pd.descs, pd.phase_tiles[ph],
+                            P.nsplit, c->ksum, c->kcount, s);
     });
     if (e != hipSuccess) return hip_fail(c, e, "NS GEMM");
   }

@@ -85,16 +85,32 @@ int32_t slot_of(GemmKind kind, int iter) {
 // (every problem's Gram, then polynomial, then apply).
 void build_phases(Plan* plan, int ns_steps) {
   plan->phases.clear();
+  plan->split_floats = plan->split_slots = 0;
   const int32_t np = int32_t(plan->probs.size());
   for (int iter = 0; iter < ns_steps; ++iter)
     for (int kind = 0; kind < 3; ++kind) {
       GemmPhase phase;
       phase.variant = plan->variant[kind];
       phase.kind = kind;
+      phase.nsplit = plan->nsplit[kind];
       std::vector<TileRef> logical;
       for (int32_t pi = 0; pi < np; ++pi)
         append_tiles(plan->probs[pi], GemmKind(kind), phase.variant,
                      pi * kDescPerProblem + slot_of(GemmKind(kind), iter), &logical);
+      if (phase.nsplit > 1) {
+        // The shares of one tile are adjacent, so that the XCD order below
+        // keeps them on one XCD (one L2) as a rule.
+        std::vector<TileRef> parts;
+        parts.reserve(logical.size() * size_t(phase.nsplit));
+        for (size_t ti = 0; ti < logical.size(); ++ti)
+          for (int32_t q = 0; q < phase.nsplit; ++q)
+            parts.push_back(TileRef{logical[ti].prob, logical[ti].ij, int32_t(ti), q});
+        plan->split_slots = std::max<int64_t>(plan->split_slots, int64_t(logical.size()));
+        plan->split_floats = std::max<int64_t>(
+            plan->split_floats, int64_t(logical.size()) * phase.nsplit *
+                                    kGemmTileRows[phase.variant] * kGemmTileCols[phase.variant]);
+        logical.swap(parts);
+      }
       phase.tiles = xcd_order(logical);
       plan->phases.push_back(std::move(phase));
     }
@@ -127,27 +143,44 @@ int32_t choose_variant(const std::vector<Problem>& probs, GemmKind kind, int til
                        int ns_elem_bytes) {
   const bool sym = kind != kApply;
   const bool dma = dma_allowed(probs, kind, ns_elem_bytes);
-  auto usable = [&](int v) {
-    return (!sym || kGemmTileRows[v] == kGemmTileCols[v]) && (!kGemmIsDma[v] || dma);
-  };
   if (tile_policy > 0) {
     int v = tile_policy - 1;
-    if (kGemmIsDma[v] && !dma) v -= kGemmDma128x128;  // same shape, register K loop
-    if (sym && kGemmTileRows[v] != kGemmTileCols[v]) v = kGemmIsDma[v] ? kGemmDma128x128 : kGemm128x128;
+    // Without the DMA path: the same tile shape with the register K loop.
+    if (kGemmIsDma[v] && !dma) v -= v >= kGemmDmaP128x128 ? kGemmDmaP128x128 : kGemmDma128x128;
+    if (sym && kGemmTileRows[v] != kGemmTileCols[v])
+      v = !kGemmIsDma[v] ? kGemm128x128 : v >= kGemmDmaP128x128 ? kGemmDmaP128x128 : kGemmDma128x128;
     return v;
   }
   // Rules from per-launch measurements on MI355X (NS workloads from one
-  // 2048 x 6144 matrix to 16-layer models): the symmetric products run best
-  // on 128 x 128 tiles; the apply product on 256 x 256 tiles once there are
-  // at least two tiles per CU, else on 128 x 128 tiles.  A launch with fewer
-  // than two 128 x 128 tiles per CU splits each tile's K loop over two
-  // 4-wave groups so that every CU still runs eight waves.
+  // 2048 x 6144 matrix to the 8B-shaped model).  With the interleaved DMA
+  // loop (bf16, K a multiple of 8): 256 x 256 tiles once a launch has at
+  // least two of them per CU, else 256 x 128 tiles when those reach two per
+  // CU (apply only), else 128 x 128 tiles.  Register K loop otherwise:
+  // symmetric products on 128 x 128 tiles (split over two K groups below two
+  // tiles per CU), the apply product on 256 x 256 tiles from two per CU.
+  if (dma) {
+    if (count_tiles(probs, kind, kGemmDmaP256x256) >= 2 * kNumCUs) return kGemmDmaP256x256;
+    if (!sym && count_tiles(probs, kind, kGemmDmaP256x128) >= 2 * kNumCUs) return kGemmDmaP256x128;
+    return kGemmDmaP128x128;
+  }
   const int64_t n128 = count_tiles(probs, kind, kGemm128x128);
   const int32_t small = n128 < 2 * kNumCUs ? kGemm128x128Split2 : kGemm128x128;
   if (sym) return small;
-  if (count_tiles(probs, kind, kGemm256x256) >= 2 * kNumCUs)
-    return usable(kGemmDma256x256) ? kGemmDma256x256 : kGemm256x256;
+  if (count_tiles(probs, kind, kGemm256x256) >= 2 * kNumCUs) return kGemm256x256;
   return small;
+}
+
+// K split of the interleaved DMA kernels: each tile shared by q workgroups,
+// each on about 1/q of the K slices, the last to finish adding the partial
+// sums.  Only on request (k_split > 0): the partial sums have to cross the
+// per-XCD caches, and on MI355X that traffic (a full fp32 tile per share)
+// cost more than the extra CUs gained on every launch measured (the 2048 x
+// 6144 shards' Gram: 35 us split 3 ways against 27 us unsplit).
+int32_t choose_split(const std::vector<Problem>& probs, GemmKind kind, int32_t v, int k_split) {
+  (void)probs;
+  (void)kind;
+  if (v != kGemmDmaP128x128 && v != kGemmDmaP256x128 && v != kGemmDmaP256x256) return 1;
+  return k_split > 0 ? k_split : 1;
 }
 
 double ns_unit_flops(int64_t S, int64_t L, int K) {
@@ -163,12 +196,13 @@ double ns_unit_dense_flops(int64_t S, int64_t L, int K) {
 }
 
 std::string build_layout(const MatrixShape* mats, int32_t n_mats,
-                         int ns_elem_bytes, int ns_steps, int tile_policy,
+                         int ns_elem_bytes, int ns_steps, int tile_policy, int k_split,
                          Layout* out, bool* shape_error) {
   *shape_error = false;
   if (!mats || n_mats <= 0) return "mats must be a non-empty array";
   if (ns_steps < 0) return "ns_steps must be >= 0";
   if (tile_policy < 0 || tile_policy > kNumGemmVariants) return "tile_policy out of range";
+  if (k_split < 0 || k_split > kMaxKSplit) return "k_split out of range";
   Layout L;
   L.mats.assign(mats, mats + n_mats);
   int64_t elems = 0;
@@ -256,8 +290,9 @@ std::string build_layout(const MatrixShape* mats, int32_t n_mats,
     plan.ws_elems = cursor;
     for (int kind = 0; kind < 3; ++kind) {
       plan.variant[kind] = choose_variant(plan.probs, GemmKind(kind), tile_policy, ns_elem_bytes);
+      plan.nsplit[kind] = choose_split(plan.probs, GemmKind(kind), plan.variant[kind], k_split);
       plan.tiles_per_iter[kind] = count_tiles(plan.probs, GemmKind(kind), plan.variant[kind]);
-      if (plan.tiles_per_iter[kind] > int64_t(std::numeric_limits<int32_t>::max() / 2))
+      if (plan.tiles_per_iter[kind] * plan.nsplit[kind] > int64_t(std::numeric_limits<int32_t>::max() / 2))
         return "too many tiles";
     }
     build_phases(&plan, ns_steps);

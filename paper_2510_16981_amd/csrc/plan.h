@@ -17,6 +17,7 @@ constexpr int kNumCUs = 256;            // MI355X compute units
 constexpr int kNumXCDs = 8;             // dies; workgroups are dealt round-robin
 constexpr int64_t kSegTarget = 16384;   // elements per elementwise workgroup
 constexpr int64_t kWsAlignBytes = 256;  // alignment of every workspace buffer
+constexpr int kMaxKSplit = 8;           // workgroups that may share one tile's K loop
 
 struct MatrixShape {
   int64_t rows, cols;
@@ -59,6 +60,7 @@ constexpr int kDescPerProblem = 5;
 struct GemmPhase {
   int32_t variant = 0;         // GemmVariant of every tile
   int32_t kind = 0;            // GemmKind
+  int32_t nsplit = 1;          // workgroups per tile, each on a share of K
   std::vector<TileRef> tiles;  // workgroup order
 };
 
@@ -68,7 +70,10 @@ struct Plan {
   int64_t ws_elems = 0;
   std::vector<TileRef> pack_tiles;
   int32_t variant[3] = {0, 0, 0};     // GemmVariant per GemmKind
+  int32_t nsplit[3] = {1, 1, 1};      // K split per GemmKind
   int64_t tiles_per_iter[3] = {0, 0, 0};
+  int64_t split_floats = 0;           // fp32 partial sums of the largest split launch
+  int64_t split_slots = 0;            // tiles of the largest split launch (one counter each)
   std::vector<GemmPhase> phases;      // in launch order, 3 per NS iteration
   double ns_flops = 0, ns_dense_flops = 0;
 };
@@ -90,12 +95,15 @@ struct Layout {
 // Returns "" on success, else a message (with *shape_error telling shape
 // vs. argument).
 std::string build_layout(const MatrixShape* mats, int32_t n_mats,
-                         int ns_elem_bytes, int ns_steps, int tile_policy,
+                         int ns_elem_bytes, int ns_steps, int tile_policy, int k_split,
                          Layout* out, bool* shape_error);
 
 // Tile shape the planner picks for one grouped product.
 int32_t choose_variant(const std::vector<Problem>& probs, GemmKind kind, int tile_policy,
                        int ns_elem_bytes);
+
+int32_t choose_split(const std::vector<Problem>& probs, GemmKind kind, int32_t variant,
+                     int k_split);
 
 // Workgroup order for a logical tile order: workgroup w runs on XCD w % 8, so
 // each XCD receives a contiguous run of logical tiles (shared operands stay

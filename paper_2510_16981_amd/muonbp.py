@@ -40,7 +40,8 @@ class Options(ctypes.Structure):
                 ("eps", ctypes.c_float), ("nesterov", ctypes.c_int32),
                 ("scale_mode", ctypes.c_int32), ("rms_beta", ctypes.c_float),
                 ("param_dtype", ctypes.c_int), ("state_dtype", ctypes.c_int),
-                ("ns_dtype", ctypes.c_int), ("tile_policy", ctypes.c_int32)]
+                ("ns_dtype", ctypes.c_int), ("tile_policy", ctypes.c_int32),
+                ("k_split", ctypes.c_int32)]
 
 
 class PlanInfo(ctypes.Structure):
@@ -50,7 +51,8 @@ class PlanInfo(ctypes.Structure):
                 ("ns_flops", ctypes.c_double),
                 ("ns_dense_flops", ctypes.c_double),
                 ("elementwise_bytes", ctypes.c_double),
-                ("workspace_bytes", ctypes.c_int64)]
+                ("workspace_bytes", ctypes.c_int64),
+                ("gemm_split", ctypes.c_int32 * 3)]
 
 
 class Profile(ctypes.Structure):

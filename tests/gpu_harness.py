@@ -48,6 +48,7 @@ class Case:
     seed: int = 0
     zero_mats: Sequence[int] = ()
     tile_policy: int = 0
+    k_split: int = 0
     check_steps: Optional[Sequence[int]] = None  # None = every step
 
 
@@ -92,7 +93,8 @@ def run_case(case: Case, keep_updates: bool = False) -> Result:
     opts = mb.options_default(ns_steps=case.ns_steps, nesterov=case.nesterov,
                               scale_mode=case.scale_mode, rms_beta=case.rms_beta,
                               param_dtype=DT[case.param], state_dtype=DT[case.state],
-                              ns_dtype=DT[case.ns], tile_policy=case.tile_policy)
+                              ns_dtype=DT[case.ns], tile_policy=case.tile_policy,
+                              k_split=case.k_split)
     opt = mb.MuonBP(case.mats, case.period, case.lr_block, case.lr_full, case.momentum,
                     case.weight_decay, options=opts)
     orc = O.MuonBPOracle([O.MatrixSpec(*m) for m in case.mats],

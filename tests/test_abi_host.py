@@ -52,6 +52,7 @@ def test_options_default(lib):
     assert abs(o.eps - 1e-7) < 1e-12
     assert (o.nesterov, o.scale_mode, o.rms_beta) == (0, 0, 1.0)
     assert (o.param_dtype, o.state_dtype, o.ns_dtype) == (mb.BF16, mb.BF16, mb.BF16)
+    assert (o.tile_policy, o.k_split) == (0, 0)
 
 
 def test_status_strings(lib):
@@ -82,6 +83,8 @@ def test_create_rejects_bad_arguments_before_gpu(lib):
     assert _create(lib, [(8, 8, 1, 1)], opt=mb.options_default(param_dtype=7))[0] == 3
     assert _create(lib, [(8, 8, 1, 1)], opt=mb.options_default(ns_steps=-1))[0] == 1
     assert _create(lib, [(8, 8, 1, 1)], opt=mb.options_default(scale_mode=3))[0] == 1
+    assert _create(lib, [(8, 8, 1, 1)], opt=mb.options_default(k_split=9))[0] == 1
+    assert _create(lib, [(8, 8, 1, 1)], opt=mb.options_default(tile_policy=11))[0] == 1
 
 
 def test_null_context_calls(lib):
@@ -141,7 +144,8 @@ def test_describe_plan_qkv_numbers(lib):
 
 @pytest.mark.parametrize("policy,shape", [(1, (128, 128)), (2, (256, 128)), (3, (256, 256)),
                                           (4, (128, 128)), (5, (256, 128)), (6, (256, 256)),
-                                          (7, (128, 128))])
+                                          (7, (128, 128)), (8, (128, 128)), (9, (256, 128)),
+                                          (10, (256, 256))])
 def test_tile_policy_forces_shape(lib, policy, shape):
     mats = W.workload_matrices("qkv-2048x6144-bf16")
     info = mb.describe_plan(mats, False, mb.options_default(tile_policy=policy))
@@ -162,3 +166,20 @@ def test_three_launches_per_iteration(lib):
             assert info.gemm_launches == 3 * 5
     info = mb.describe_plan([(64, 64, 1, 1)], False, mb.options_default(ns_steps=0))
     assert info.gemm_launches == 0
+
+
+def test_k_split_applies_to_dma_pipeline_only(lib):
+    """A forced K split reaches the interleaved DMA kernels (bf16, K a
+    multiple of 8); other kernels never split."""
+    mats = W.workload_matrices("qkv-2048x6144-bf16")
+    info = mb.describe_plan(mats, False, mb.options_default(tile_policy=8, k_split=4))
+    assert list(info.gemm_split) == [4, 4, 4]
+    info = mb.describe_plan(mats, False, mb.options_default(tile_policy=1, k_split=4))
+    assert list(info.gemm_split) == [1, 1, 1]
+    info = mb.describe_plan(mats, False, mb.options_default(ns_dtype=mb.F32, k_split=4))
+    assert list(info.gemm_split) == [1, 1, 1]
+    # Not requested: no split.
+    for name in W.WORKLOADS:
+        for full in (False, True):
+            info = mb.describe_plan(W.workload_matrices(name), full)
+            assert list(info.gemm_split) == [1, 1, 1]

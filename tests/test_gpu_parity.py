@@ -82,9 +82,10 @@ def test_ragged_shapes_fp32(mats):
 BIG_RAGGED = [(520, 1000, 1, 2), (1000, 264, 2, 1), (300, 300, 1, 1)]
 
 
-@pytest.mark.parametrize("policy", [1, 2, 3, 4, 5, 6, 7],
+@pytest.mark.parametrize("policy", [1, 2, 3, 4, 5, 6, 7, 8, 9, 10],
                          ids=["128x128", "256x128", "256x256", "dma128x128", "dma256x128",
-                              "dma256x256", "128x128split2"])
+                              "dma256x256", "128x128split2", "dmap128x128", "dmap256x128",
+                              "dmap256x256"])
 @pytest.mark.parametrize("ns", ["bf16", "f32"])
 def test_every_tile_shape(policy, ns):
     """Each NS GEMM kernel, forced, on units spanning several tiles with
@@ -96,6 +97,31 @@ def test_every_tile_shape(policy, ns):
     res = run_case(Case(mats=BIG_RAGGED, period=2, steps=3, param=st, state=st, ns=ns,
                         tile_policy=policy))
     _check(res, F32_TOL if ns == "f32" else BF16_TOL)
+
+
+# Units whose K is a multiple of 8 (so the DMA kernels run) with ragged M,
+# N and K tails, transposed units and one long K (136 x 2048).
+ALIGNED = [(264, 1040, 1, 2), (1040, 264, 2, 1), (296, 296, 1, 1), (136, 2048, 1, 1)]
+
+
+@pytest.mark.parametrize("ksplit", [0, 2, 3, 8])
+@pytest.mark.parametrize("policy", [8, 9, 10], ids=["dmap128x128", "dmap256x128", "dmap256x256"])
+def test_dma_pipeline_and_k_split(policy, ksplit):
+    """The interleaved DMA kernels, with each tile's K loop shared by 2..8
+    workgroups (0 = not split).  With 8, the 136-row units' A.A and apply
+    products (5 K slices) leave some shares with no slice at all."""
+    announce(f"dma pipeline policy {policy} k_split {ksplit}")
+    res = run_case(Case(mats=ALIGNED, period=2, steps=3, tile_policy=policy, k_split=ksplit))
+    _check(res, BF16_TOL)
+
+
+def test_k_split_deterministic():
+    """Shares are added in a fixed order, whichever workgroup finishes last."""
+    announce("k split determinism")
+    c = Case(mats=ALIGNED, period=2, steps=3, tile_policy=8, k_split=3)
+    a, b = run_case(c), run_case(c)
+    for x, y in zip(a.final_params, b.final_params):
+        assert np.array_equal(x, y)
 
 
 @pytest.mark.parametrize("param,state,ns", [("bf16", "f32", "bf16"), ("f32", "f32", "bf16"),
