@@ -77,11 +77,13 @@ typedef struct {
                                4/5/6 = the same tiles with an LDS-DMA K loop
                                (bf16 NS only, K a multiple of 8, else the
                                register loop); 7 = 128x128 tiles with the K
-                               loop split over two 4-wave groups; 8/9/10 =
-                               128x128 / 256x128 / 256x256 tiles with the
+                               loop split over two 4-wave groups; 8/9/10/
+                               11/12/13 = 128x128 / 256x128 / 256x256 /
+                               192x256 / 256x192 / 192x192 tiles with the
                                LDS-DMA loop interleaved with the MFMAs (same
                                conditions as 4-6).  Symmetric products use
-                               square tiles (128x128 for 2, 5, 9). */
+                               square tiles (128x128 for 2, 5, 9; 192x192
+                               for 11, 12). */
   int32_t k_split;          /* interleaved DMA kernels only: 1..8 = each
                                tile's K loop shared by that many workgroups
                                (fp32 partial sums added by the last one to

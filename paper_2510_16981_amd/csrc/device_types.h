@@ -49,18 +49,18 @@ struct PackDesc {
 
 // One product of a grouped NS launch, all row-major with K contiguous:
 //   C[i][j] = alpha * sum_k X[i][k] Y[j][k] + beta * D[i][j] + gamma [i == j]
-// and, when Ct is set, Ct[j][i] = the same value (Dt holds D transposed).
+// and, when Ct is set, Ct[j][i] = the same value.  With both Ct and D set,
+// D must be symmetric (the transposed tile reuses D's tile).
 // sym: the product is symmetric; its tile list holds upper tiles only and
 // the mirror write (Ct = C) is skipped on diagonal tiles.
 struct GemmDesc {
   const void* X;
   const void* Y;
   const void* D;
-  const void* Dt;
   void* C;
   void* Ct;
   int32_t M, N, K;
-  int32_t ldx, ldy, ldd, lddt, ldc, ldct;
+  int32_t ldx, ldy, ldd, ldc, ldct;
   float alpha, beta, gamma;
   int32_t sym;
 };
@@ -75,12 +75,17 @@ enum GemmVariant : int32_t {
   kGemmDma128x128 = 3, kGemmDma256x128 = 4, kGemmDma256x256 = 5,
   kGemm128x128Split2 = 6,
   kGemmDmaP128x128 = 7, kGemmDmaP256x128 = 8, kGemmDmaP256x256 = 9,
-  kNumGemmVariants = 10
+  kGemmDmaP192x256 = 10, kGemmDmaP256x192 = 11, kGemmDmaP192x192 = 12,
+  kNumGemmVariants = 13
 };
-constexpr int kGemmTileRows[kNumGemmVariants] = {128, 256, 256, 128, 256, 256, 128, 128, 256, 256};
-constexpr int kGemmTileCols[kNumGemmVariants] = {128, 128, 256, 128, 128, 256, 128, 128, 128, 256};
+constexpr int kGemmTileRows[kNumGemmVariants] = {128, 256, 256, 128, 256, 256, 128,
+                                                 128, 256, 256, 192, 256, 192};
+constexpr int kGemmTileCols[kNumGemmVariants] = {128, 128, 256, 128, 128, 256, 128,
+                                                 128, 128, 256, 256, 192, 192};
 constexpr bool kGemmIsDma[kNumGemmVariants] = {false, false, false, true, true, true, false,
-                                               true,  true,  true};
+                                               true,  true,  true,  true, true, true};
+// Interleaved DMA kernels (k_ns_gemm_dmap).
+constexpr bool gemm_is_dmap(int v) { return v >= kGemmDmaP128x128; }
 
 // One workgroup tile of a grouped launch: problem index and packed
 // (tile row << 16 | tile column).

@@ -21,7 +21,7 @@ hipError_t launch_scale(int n_probs, const ScaleDesc* sd, const float* partials,
                         float* scales, float eps, hipStream_t s);
 
 // Z0 = s_p Y_p written straight and transposed into the NS workspace.
-hipError_t launch_pack(DType mom_t, DType grad_t, DType ns_t, int n_tiles,
+hipError_t launch_pack(DType mom_t, DType grad_t, DType ns_t, bool vec, int n_tiles,
                        const TileRef* tiles, const PackDesc* pd,
                        const MatPtrs* mats, const void* mom,
                        const float* scales, float mu, int nesterov,

@@ -146,7 +146,13 @@ __global__ __launch_bounds__(64) void k_scale(const ScaleDesc* __restrict__ sd,
 
 // ---------------------------------------------------------------- pack
 
-template <typename TM, typename TG, typename TN>
+// Z = s Y (straight) and Z^T = s Y^T (transposed) for one 64 x 64 tile of a
+// problem, Y = M (or G + mu M with Nesterov).  The transposed copy goes
+// through LDS.  VEC: columns, windows and leading dimensions are multiples
+// of 8 elements and the pointers 16-byte aligned, so every access is one
+// 16-byte chunk of 8 elements (the last chunk of a Z^T row may be cut by the
+// problem's row count).
+template <typename TM, typename TG, typename TN, bool VEC>
 __global__ __launch_bounds__(kThreads) void k_pack(
     const TileRef* __restrict__ tiles, const PackDesc* __restrict__ pd,
     const MatPtrs* __restrict__ mats, const TM* __restrict__ mom,
@@ -160,6 +166,52 @@ __global__ __launch_bounds__(kThreads) void k_pack(
   const TG* g = static_cast<const TG*>(mats[d.mat].grad) + d.in_mat_off;
   TN* ds = static_cast<TN*>(d.dst_s);
   TN* dt = static_cast<TN*>(d.dst_t);
+  if (VEC) {
+    // Straight copy: 64 rows x 8 chunks, two chunks per thread.
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int q = threadIdx.x + kThreads * i, rr = q >> 3, ch = q & 7;
+      const int r = r0 + rr, c = c0 + 8 * ch;
+      float y[8];
+      if (r < d.rows && c < d.cols) {
+        const int64_t o = int64_t(r) * d.ld + c;
+        load8(m + o, y);
+        if (nesterov) {
+          float gv[8];
+          load8(g + o, gv);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) y[e] = fmaf(mu, y[e], gv[e]);
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) y[e] *= s;
+        store8(ds + int64_t(r) * d.ld_s + c, y);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) y[e] = 0.f;
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) tile[rr][8 * ch + e] = y[e];
+    }
+    __syncthreads();
+    // Transposed copy: Z^T rows c0 .. c0 + 63, chunks of 8 rows of Y.
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int q = threadIdx.x + kThreads * i, cc = q >> 3, j = q & 7;
+      const int c = c0 + cc, r = r0 + 8 * j;
+      if (c < d.cols && r < d.rows) {
+        float y[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) y[e] = tile[8 * j + e][cc];
+        TN* p = dt + int64_t(c) * d.ld_t + r;
+        if (r + 8 <= d.rows) {
+          store8(p, y);
+        } else {
+          for (int e = 0; e < d.rows - r; ++e) p[e] = from_f<TN>(y[e]);
+        }
+      }
+    }
+    return;
+  }
   const int lc = threadIdx.x & 63, lr = threadIdx.x >> 6;
 #pragma unroll 4
   for (int i = 0; i < 16; ++i) {
@@ -308,52 +360,48 @@ __device__ __forceinline__ void gemm_epilogue(f32x16_t (&acc)[TM][TN], float* st
   constexpr int ES = sizeof(T);
   const int lane = threadIdx.x & 63, wave = (threadIdx.x >> 6) & 3;
   const int wm = wave >> 1, wn = wave & 1;
-  // Epilogue, one MFMA row of the wave's sub-tile (32 x 32TN) per pass.
-  // The pass's beta * D (and beta * Dt) slices are requested first, as
+  // One pass per MFMA row of the wave's sub-tile (32 x 32TN): alpha * acc
+  // is staged in a wave-private LDS block (odd pitch), then each lane
+  // writes 8-element (16-byte) chunks of C rows and, for the transposed
+  // copy, of Ct rows read down the staged columns.  beta * D arrives as
   // bounds-checked buffer loads (rows past the matrix read zero; columns
-  // past N only feed values that are not stored), so their latency overlaps
-  // the staging of alpha * acc in a wave-private LDS block (odd pitch).  Then
-  // each lane writes 8-element (16-byte) chunks of C rows and, for the
-  // transposed copy, of Ct rows.  32x32 accumulator layout: lane l holds
-  // column l % 32 and, for register v, row 8 (v / 4) + 4 (l / 32) + v % 4.
+  // past N only feed values that are not stored), issued one pass ahead so
+  // their latency overlaps the previous pass.  D is added to the staged
+  // rows in place, and the Ct chunks are read after that, so the transposed
+  // tile needs no loads of its own (D is symmetric whenever Ct is written).
+  // 32x32 accumulator layout: lane l holds column l % 32 and, for register
+  // v, row 8 (v / 4) + 4 (l / 32) + v % 4.
   constexpr int P = 32 * TN + 1;
   constexpr int NCH = 4 * TN;           // 8-element chunks per staged row
   constexpr int CPL = 32 * NCH / 64;    // chunks per lane, C and Ct alike
+  constexpr int VPC = ES / 2;           // 16-byte slices per 8-element chunk
   const bool mirror = d.Ct != nullptr && !diag;
   const bool has_d = d.D != nullptr;
   const int wr0 = m0 + wm * 32 * TM, wc0 = n0 + wn * 32 * TN;
   const __amdgpu_buffer_rsrc_t dr = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<void*>(has_d ? d.D : d.X), 0, has_d ? d.M * d.ldd * ES : 0, kBufferWord3);
-  const __amdgpu_buffer_rsrc_t dtr = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<void*>(has_d && d.Dt ? d.Dt : d.X), 0, has_d && d.Dt ? d.N * d.lddt * ES : 0,
-      kBufferWord3);
   T* C = static_cast<T*>(d.C);
   T* Ct = static_cast<T*>(d.Ct);
+  uint4 dv[2][CPL][VPC];
+  auto load_d = [&](int i, uint4 (&buf)[CPL][VPC]) {
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) {
+      const int q = lane + 64 * c, r = q / NCH, ch = q - r * NCH;
+      const int o = ((wr0 + 32 * i + r) * d.ldd + wc0 + 8 * ch) * ES;
+#pragma unroll
+      for (int h = 0; h < VPC; ++h) buf[c][h] = bld16(dr, o + 16 * h, 0);
+    }
+  };
+  if (has_d && active) load_d(0, dv[0]);
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
     const int r0 = wr0 + 32 * i;
-    constexpr int VPC = ES / 2;  // 16-byte slices per 8-element chunk
-    uint4 dv[CPL][VPC], dtv[CPL][VPC];
-    if (has_d && active) {
-#pragma unroll
-      for (int c = 0; c < CPL; ++c) {
-        const int q = lane + 64 * c, r = q / NCH, ch = q - r * NCH;
-        const int o = ((r0 + r) * d.ldd + wc0 + 8 * ch) * ES;
-#pragma unroll
-        for (int h = 0; h < VPC; ++h) dv[c][h] = bld16(dr, o + 16 * h, 0);
-        if (mirror) {
-          const int rr = q >> 2, cc = q & 3;  // Ct row wc0 + rr, columns r0 + 8 cc ..
-          const int ot = ((wc0 + rr) * d.lddt + r0 + 8 * cc) * ES;
-#pragma unroll
-          for (int h = 0; h < VPC; ++h) dtv[c][h] = bld16(dtr, ot + 16 * h, 0);
-        }
-      }
-    }
 #pragma unroll
     for (int j = 0; j < TN; ++j)
 #pragma unroll
       for (int v = 0; v < 16; ++v)
         st[(8 * (v >> 2) + 4 * (lane >> 5) + (v & 3)) * P + j * 32 + (lane & 31)] = alpha * acc[i][j][v];
+    if (i + 1 < TM && has_d && active) load_d(i + 1, dv[(i + 1) & 1]);
     __syncthreads();
 #pragma unroll
     for (int c = 0; c < CPL && active; ++c) {
@@ -361,10 +409,15 @@ __device__ __forceinline__ void gemm_epilogue(f32x16_t (&acc)[TM][TN], float* st
       float f[8];
 #pragma unroll
       for (int e = 0; e < 8; ++e) f[e] = st[r * P + 8 * ch + e];
-      if (has_d) add8<T>(f, dv[c], beta);
+      if (has_d) add8<T>(f, dv[i & 1][c], beta);
       if (gamma != 0.f) add_diag(f, r0 + r, wc0 + 8 * ch, gamma);
       store_chunk<T>(C, d.ldc, r0 + r, wc0 + 8 * ch, d.M, d.N, f);
+      if (mirror && has_d) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) st[r * P + 8 * ch + e] = f[e];
+      }
     }
+    if (mirror && has_d) __syncthreads();
     if (mirror && active) {
 #pragma unroll
       for (int c = 0; c < CPL; ++c) {
@@ -372,7 +425,6 @@ __device__ __forceinline__ void gemm_epilogue(f32x16_t (&acc)[TM][TN], float* st
         float f[8];
 #pragma unroll
         for (int e = 0; e < 8; ++e) f[e] = st[(8 * cc + e) * P + rr];
-        if (has_d) add8<T>(f, dtv[c], beta);
         store_chunk<T>(Ct, d.ldct, wc0 + rr, r0 + 8 * cc, d.N, d.M, f);
       }
     }
@@ -619,12 +671,18 @@ __device__ __forceinline__ u32x4_t lds_read16(uint32_t addr) {
 
 template <int N>
 __device__ __forceinline__ void lds_wait(u32x4_t (&f)[N]) {
-  static_assert(N == 4 || N == 6 || N == 8, "fragment count");
+  static_assert(N >= 4 && N <= 8, "fragment count");
   if constexpr (N == 4)
     asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(f[0]), "+v"(f[1]), "+v"(f[2]), "+v"(f[3]));
+  else if constexpr (N == 5)
+    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(f[0]), "+v"(f[1]), "+v"(f[2]), "+v"(f[3]), "+v"(f[4]));
   else if constexpr (N == 6)
     asm volatile("s_waitcnt lgkmcnt(0)"
                  : "+v"(f[0]), "+v"(f[1]), "+v"(f[2]), "+v"(f[3]), "+v"(f[4]), "+v"(f[5]));
+  else if constexpr (N == 7)
+    asm volatile("s_waitcnt lgkmcnt(0)"
+                 : "+v"(f[0]), "+v"(f[1]), "+v"(f[2]), "+v"(f[3]), "+v"(f[4]), "+v"(f[5]),
+                   "+v"(f[6]));
   else
     asm volatile("s_waitcnt lgkmcnt(0)"
                  : "+v"(f[0]), "+v"(f[1]), "+v"(f[2]), "+v"(f[3]), "+v"(f[4]), "+v"(f[5]),
@@ -749,8 +807,8 @@ __global__ __launch_bounds__(kThreads) void k_ns_gemm_dma(const GemmDesc* __rest
 //
 //   * both K steps of a slice are read from LDS one step ahead, each read
 //     issued between two MFMAs of the previous step;
-//   * the barrier that publishes the next slice sits in the middle of the
-//     current slice's second step (the MFMAs already issued keep running);
+//   * the barrier that publishes the next slice sits right after the first
+//     MFMA of the current slice's second step (that MFMA keeps running);
 //   * right after it, the copy that refills the slot just consumed and the
 //     reads of the next slice's first step are spread over the remaining
 //     MFMAs.
@@ -776,7 +834,11 @@ __global__ __launch_bounds__(kThreads) void k_ns_gemm_dmap(const GemmDesc* __res
   using T = bf16;
   constexpr int TM = G::TM, TN = G::TN, LPW = G::LPW, ES = 2, NF = TM + TN;
   constexpr int NM = TM * TN;  // MFMAs per K step
-  constexpr int H = NM / 2;    // MFMAs of the second step issued before the barrier
+  // MFMAs of the second step issued before the barrier: one keeps the
+  // matrix pipeline busy while the barrier resolves, and leaves the rest of
+  // the step to hide the next slice's reads (measured: 2-4% faster than
+  // half the step on every tile shape).
+  constexpr int H = 1;
   __shared__ __attribute__((aligned(1024))) unsigned char lds[G::LDS_BYTES];
 
   const TileRef t = tiles[blockIdx.x];
@@ -1006,9 +1068,10 @@ hipError_t launch_scale(int n_probs, const ScaleDesc* sd, const float* partials,
   return hipGetLastError();
 }
 
-hipError_t launch_pack(DType mom_t, DType grad_t, DType ns_t, int n_tiles, const TileRef* tiles,
-                       const PackDesc* pd, const MatPtrs* mats, const void* mom,
-                       const float* scales, float mu, int nesterov, hipStream_t s) {
+hipError_t launch_pack(DType mom_t, DType grad_t, DType ns_t, bool vec, int n_tiles,
+                       const TileRef* tiles, const PackDesc* pd, const MatPtrs* mats,
+                       const void* mom, const float* scales, float mu, int nesterov,
+                       hipStream_t s) {
   if (n_tiles <= 0) return hipSuccess;
   return dispatch1(mom_t, [&](auto m) {
     return dispatch1(grad_t, [&](auto g) {
@@ -1016,8 +1079,12 @@ hipError_t launch_pack(DType mom_t, DType grad_t, DType ns_t, int n_tiles, const
         using TM = decltype(m);
         using TG = decltype(g);
         using TN = decltype(n);
-        hipLaunchKernelGGL((k_pack<TM, TG, TN>), dim3(n_tiles), dim3(kThreads), 0, s, tiles, pd,
-                           mats, static_cast<const TM*>(mom), scales, mu, nesterov);
+        if (vec)
+          hipLaunchKernelGGL((k_pack<TM, TG, TN, true>), dim3(n_tiles), dim3(kThreads), 0, s, tiles,
+                             pd, mats, static_cast<const TM*>(mom), scales, mu, nesterov);
+        else
+          hipLaunchKernelGGL((k_pack<TM, TG, TN, false>), dim3(n_tiles), dim3(kThreads), 0, s, tiles,
+                             pd, mats, static_cast<const TM*>(mom), scales, mu, nesterov);
         return hipGetLastError();
       });
     });
@@ -1027,7 +1094,7 @@ hipError_t launch_pack(DType mom_t, DType grad_t, DType ns_t, int n_tiles, const
 hipError_t launch_ns_gemm(DType ns_t, int variant, int n_tiles, const GemmDesc* probs,
                           const TileRef* tiles, int nsplit, float* ksum, int* kcount,
                           hipStream_t s) {
-  if (nsplit > 1 && (!ksum || !kcount || variant < kGemmDmaP128x128)) return hipErrorInvalidValue;
+  if (nsplit > 1 && (!ksum || !kcount || !gemm_is_dmap(variant))) return hipErrorInvalidValue;
   if (n_tiles <= 0) return hipSuccess;
   return dispatch1(ns_t, [&](auto n) {
     using TN = decltype(n);
@@ -1051,16 +1118,22 @@ hipError_t launch_ns_gemm(DType ns_t, int variant, int n_tiles, const GemmDesc* 
       case kGemmDmaP128x128:
       case kGemmDmaP256x128:
       case kGemmDmaP256x256:
+      case kGemmDmaP192x256:
+      case kGemmDmaP256x192:
+      case kGemmDmaP192x192:
         if constexpr (std::is_same<TN, bf16>::value) {
-          if (variant == kGemmDmaP128x128)
-            hipLaunchKernelGGL((k_ns_gemm_dmap<128, 128>), dim3(n_tiles), dim3(kThreads), 0, s, probs,
-                               tiles, nsplit, ksum, kcount);
-          else if (variant == kGemmDmaP256x128)
-            hipLaunchKernelGGL((k_ns_gemm_dmap<256, 128>), dim3(n_tiles), dim3(kThreads), 0, s, probs,
-                               tiles, nsplit, ksum, kcount);
-          else
-            hipLaunchKernelGGL((k_ns_gemm_dmap<256, 256>), dim3(n_tiles), dim3(kThreads), 0, s, probs,
-                               tiles, nsplit, ksum, kcount);
+#define MUONBP_DMAP(BM_, BN_)                                                                  \
+  hipLaunchKernelGGL((k_ns_gemm_dmap<BM_, BN_>), dim3(n_tiles), dim3(kThreads), 0, s, probs, \
+                     tiles, nsplit, ksum, kcount)
+          switch (variant) {
+            case kGemmDmaP128x128: MUONBP_DMAP(128, 128); break;
+            case kGemmDmaP256x128: MUONBP_DMAP(256, 128); break;
+            case kGemmDmaP256x256: MUONBP_DMAP(256, 256); break;
+            case kGemmDmaP192x256: MUONBP_DMAP(192, 256); break;
+            case kGemmDmaP256x192: MUONBP_DMAP(256, 192); break;
+            default: MUONBP_DMAP(192, 192); break;
+          }
+#undef MUONBP_DMAP
           break;
         } else {
           return hipErrorInvalidValue;

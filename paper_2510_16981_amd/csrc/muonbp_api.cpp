@@ -170,17 +170,16 @@ hipError_t build_plan_tables(muonbp_ctx* c, int full) {
     const int32_t S = int32_t(p.S), Lr = int32_t(p.L), Sp = int32_t(p.Sp), Lp = int32_t(p.Lp);
     // Slots in DescSlot order.  Gram: A = Z_q Z_q^T (symmetric).
     for (int q = 0; q < 2; ++q)
-      descs.push_back(GemmDesc{at(p.off_z[q]), at(p.off_z[q]), nullptr, nullptr, at(p.off_a),
-                               at(p.off_a), S, S, Lr, Lp, Lp, 0, 0, Sp, Sp, 1.f, 0.f, 0.f, 1});
+      descs.push_back(GemmDesc{at(p.off_z[q]), at(p.off_z[q]), nullptr, at(p.off_a), at(p.off_a),
+                               S, S, Lr, Lp, Lp, 0, Sp, Sp, 1.f, 0.f, 0.f, 1});
     // Polynomial: B = c A A^T + b A + a I (A symmetric; the a I term carries
     // Algorithm 2's a X into the next product).
-    descs.push_back(GemmDesc{at(p.off_a), at(p.off_a), at(p.off_a), at(p.off_a), at(p.off_b),
-                             at(p.off_b), S, S, S, Sp, Sp, Sp, Sp, Sp, Sp, o.c, o.b, o.a, 1});
+    descs.push_back(GemmDesc{at(p.off_a), at(p.off_a), at(p.off_a), at(p.off_b), at(p.off_b), S, S,
+                             S, Sp, Sp, Sp, Sp, Sp, o.c, o.b, o.a, 1});
     // Apply: Z_{1-q} = (a I + B) Z_q (= a Z_q + B Z_q), also stored transposed.
     for (int q = 0; q < 2; ++q)
-      descs.push_back(GemmDesc{at(p.off_b), at(p.off_zt[q]), nullptr, nullptr, at(p.off_z[1 - q]),
-                               at(p.off_zt[1 - q]), S, Lr, S, Sp, Sp, 0, 0, Lp, Sp, 1.f, 0.f, 0.f,
-                               0});
+      descs.push_back(GemmDesc{at(p.off_b), at(p.off_zt[q]), nullptr, at(p.off_z[1 - q]),
+                               at(p.off_zt[1 - q]), S, Lr, S, Sp, Sp, 0, Lp, Sp, 1.f, 0.f, 0.f, 0});
   }
   // Update table: U of every block after K iterations (buffer K mod 2).
   const int fin = o.ns_steps & 1;
@@ -533,7 +532,7 @@ muonbp_status muonbp_step(muonbp_ctx* c, void* const* params, const void* const*
   });
   if (e != hipSuccess) return hip_fail(c, e, "scale");
   e = timed(c, 2, [&] {
-    return launch_pack(tm, tp, tn, int(plan.pack_tiles.size()), pd.pack_tiles, pd.pack, mats, c->mom,
+    return launch_pack(tm, tp, tn, aligned, int(plan.pack_tiles.size()), pd.pack_tiles, pd.pack, mats, c->mom,
                        c->scales, c->mu, o.nesterov, s);
   });
   if (e != hipSuccess) return hip_fail(c, e, "pack");

@@ -139,29 +139,79 @@ bool dma_allowed(const std::vector<Problem>& probs, GemmKind kind, int ns_elem_b
   return true;
 }
 
+// Time model of one launch of the interleaved DMA kernel, in microseconds,
+// fitted to per-launch measurements on MI355X (engine clock about 1.7 GHz
+// under sustained MFMA load): rounds of resident workgroups x (fixed cost +
+// K slices x time per 32-deep slice).  The fixed cost (launch, ring fill,
+// epilogue) is 6.5 us.  A slice costs the tile's MFMA cycles over an
+// efficiency that grows with the MFMAs per wave and K step: 4 (128 x 128):
+// 0.49, 8: 0.55, 16 (256 x 256): 0.61.  128 x 128 tiles fit two per CU,
+// and then take 0.65 us per slice each; larger tiles fit one.
+double dmap_launch_us(const std::vector<Problem>& probs, GemmKind kind, int v) {
+  int64_t tiles = 0;
+  double slices = 0;
+  for (const Problem& p : probs) {
+    int64_t m, c, k;
+    gemm_dims(p, kind, &m, &c, &k);
+    const int64_t tm = ceil_div(m, kGemmTileRows[v]), tn = ceil_div(c, kGemmTileCols[v]);
+    const int64_t nt = kind == kApply ? tm * tn : tm * (tm + 1) / 2;
+    tiles += nt;
+    slices += double(nt) * double(ceil_div(k, 32));
+  }
+  if (tiles == 0) return 0;
+  slices /= double(tiles);
+  const int nm = (kGemmTileRows[v] / 64) * (kGemmTileCols[v] / 64);
+  const double eff = nm <= 4 ? 0.49 : nm <= 8 ? 0.49 + 0.015 * (nm - 4)
+                                              : std::min(0.61, 0.55 + 0.0075 * (nm - 8));
+  const double slice_us = nm * 2 * 32 / eff / 1700.0;
+  constexpr double kFixedUs = 6.5;
+  const double one = kFixedUs + slices * slice_us;  // a round with one tile per CU
+  if (v != kGemmDmaP128x128) return double(ceil_div(tiles, kNumCUs)) * one;
+  const double two = kFixedUs + slices * 0.65;      // a round with two tiles per CU
+  const int64_t full = tiles / (2 * kNumCUs), rest = tiles % (2 * kNumCUs);
+  return double(full) * two + (rest == 0 ? 0.0 : rest <= kNumCUs ? one : two);
+}
+
 int32_t choose_variant(const std::vector<Problem>& probs, GemmKind kind, int tile_policy,
                        int ns_elem_bytes) {
   const bool sym = kind != kApply;
   const bool dma = dma_allowed(probs, kind, ns_elem_bytes);
   if (tile_policy > 0) {
     int v = tile_policy - 1;
-    // Without the DMA path: the same tile shape with the register K loop.
-    if (kGemmIsDma[v] && !dma) v -= v >= kGemmDmaP128x128 ? kGemmDmaP128x128 : kGemmDma128x128;
-    if (sym && kGemmTileRows[v] != kGemmTileCols[v])
-      v = !kGemmIsDma[v] ? kGemm128x128 : v >= kGemmDmaP128x128 ? kGemmDmaP128x128 : kGemmDma128x128;
+    // Symmetric products take square tiles; without the DMA path, the
+    // register K loop on the same (or, for 192-wide tiles, the nearest) shape.
+    if (sym && kGemmTileRows[v] != kGemmTileCols[v]) {
+      static const int32_t square[kNumGemmVariants] = {0, 0, 2, 3, 3, 5, 6, 7, 7, 9, 12, 12, 12};
+      v = square[v];
+    }
+    if (kGemmIsDma[v] && !dma) {
+      static const int32_t twin[kNumGemmVariants] = {0, 1, 2, 0, 1, 2, 6, 0, 1, 2, 2, 2, 0};
+      v = twin[v];
+    }
     return v;
   }
-  // Rules from per-launch measurements on MI355X (NS workloads from one
-  // 2048 x 6144 matrix to the 8B-shaped model).  With the interleaved DMA
-  // loop (bf16, K a multiple of 8): 256 x 256 tiles once a launch has at
-  // least two of them per CU, else 256 x 128 tiles when those reach two per
-  // CU (apply only), else 128 x 128 tiles.  Register K loop otherwise:
+  // With the interleaved DMA loop (bf16, K a multiple of 8): the tile shape
+  // the time model above puts first (square shapes for the symmetric
+  // products).  Register K loop otherwise (rules from per-launch
+  // measurements on MI355X):
   // symmetric products on 128 x 128 tiles (split over two K groups below two
   // tiles per CU), the apply product on 256 x 256 tiles from two per CU.
   if (dma) {
-    if (count_tiles(probs, kind, kGemmDmaP256x256) >= 2 * kNumCUs) return kGemmDmaP256x256;
-    if (!sym && count_tiles(probs, kind, kGemmDmaP256x128) >= 2 * kNumCUs) return kGemmDmaP256x128;
-    return kGemmDmaP128x128;
+    static const int32_t sym_cands[] = {kGemmDmaP128x128, kGemmDmaP192x192, kGemmDmaP256x256};
+    static const int32_t gen_cands[] = {kGemmDmaP128x128, kGemmDmaP256x128, kGemmDmaP192x256,
+                                        kGemmDmaP256x192, kGemmDmaP256x256};
+    int32_t best = kGemmDmaP128x128;
+    double best_us = dmap_launch_us(probs, kind, best);
+    const int32_t* c = sym ? sym_cands : gen_cands;
+    const int nc = sym ? 3 : 5;
+    for (int i = 1; i < nc; ++i) {
+      const double us = dmap_launch_us(probs, kind, c[i]);
+      if (us < best_us) {
+        best = c[i];
+        best_us = us;
+      }
+    }
+    return best;
   }
   const int64_t n128 = count_tiles(probs, kind, kGemm128x128);
   const int32_t small = n128 < 2 * kNumCUs ? kGemm128x128Split2 : kGemm128x128;
@@ -179,7 +229,7 @@ int32_t choose_variant(const std::vector<Problem>& probs, GemmKind kind, int til
 int32_t choose_split(const std::vector<Problem>& probs, GemmKind kind, int32_t v, int k_split) {
   (void)probs;
   (void)kind;
-  if (v != kGemmDmaP128x128 && v != kGemmDmaP256x128 && v != kGemmDmaP256x256) return 1;
+  if (!gemm_is_dmap(v)) return 1;
   return k_split > 0 ? k_split : 1;
 }
 

@@ -84,7 +84,7 @@ def test_create_rejects_bad_arguments_before_gpu(lib):
     assert _create(lib, [(8, 8, 1, 1)], opt=mb.options_default(ns_steps=-1))[0] == 1
     assert _create(lib, [(8, 8, 1, 1)], opt=mb.options_default(scale_mode=3))[0] == 1
     assert _create(lib, [(8, 8, 1, 1)], opt=mb.options_default(k_split=9))[0] == 1
-    assert _create(lib, [(8, 8, 1, 1)], opt=mb.options_default(tile_policy=11))[0] == 1
+    assert _create(lib, [(8, 8, 1, 1)], opt=mb.options_default(tile_policy=14))[0] == 1
 
 
 def test_null_context_calls(lib):
@@ -142,16 +142,35 @@ def test_describe_plan_qkv_numbers(lib):
     assert abs(full.ns_flops / 1e12 - 0.4296) < 5e-4
 
 
-@pytest.mark.parametrize("policy,shape", [(1, (128, 128)), (2, (256, 128)), (3, (256, 256)),
-                                          (4, (128, 128)), (5, (256, 128)), (6, (256, 256)),
-                                          (7, (128, 128)), (8, (128, 128)), (9, (256, 128)),
-                                          (10, (256, 256))])
-def test_tile_policy_forces_shape(lib, policy, shape):
+@pytest.mark.parametrize("policy,shape,square", [
+    (1, (128, 128), 128), (2, (256, 128), 128), (3, (256, 256), 256), (4, (128, 128), 128),
+    (5, (256, 128), 128), (6, (256, 256), 256), (7, (128, 128), 128), (8, (128, 128), 128),
+    (9, (256, 128), 128), (10, (256, 256), 256), (11, (192, 256), 192), (12, (256, 192), 192),
+    (13, (192, 192), 192)])
+def test_tile_policy_forces_shape(lib, policy, shape, square):
+    """A forced tile shape reaches the apply product; the symmetric products
+    take the nearest square shape."""
     mats = W.workload_matrices("qkv-2048x6144-bf16")
     info = mb.describe_plan(mats, False, mb.options_default(tile_policy=policy))
     assert (info.gemm_tile_rows[2], info.gemm_tile_cols[2]) == shape
-    sq = shape if shape[0] == shape[1] else (128, 128)
-    assert (info.gemm_tile_rows[0], info.gemm_tile_cols[0]) == sq
+    assert (info.gemm_tile_rows[0], info.gemm_tile_cols[0]) == (square, square)
+    assert (info.gemm_tile_rows[1], info.gemm_tile_cols[1]) == (square, square)
+
+
+def test_tile_model_choices(lib):
+    """The planner's time model picks tiles that fill the 256 CUs: the
+    2048 x 768 shards' apply takes 192 x 256 tiles (256 of them), the whole
+    2048 x 6144 matrix's apply 256 x 192 tiles (256), and the large models
+    256 x 256 tiles."""
+    mats = W.workload_matrices("qkv-2048x6144-bf16")
+    blk, full = mb.describe_plan(mats, False), mb.describe_plan(mats, True)
+    assert (blk.gemm_tile_rows[2], blk.gemm_tile_cols[2], blk.gemm_tiles[2]) == (192, 256, 256)
+    assert (full.gemm_tile_rows[2], full.gemm_tile_cols[2], full.gemm_tiles[2]) == (256, 192, 256)
+    big = mb.describe_plan(W.workload_matrices("llama-32L-d4096-bf16"), False)
+    assert list(big.gemm_tile_rows) == [256, 256, 256] and list(big.gemm_tile_cols) == [256, 256, 256]
+    # fp32 NS operands: register K loop shapes only.
+    f32 = mb.describe_plan(mats, False, mb.options_default(ns_dtype=mb.F32))
+    assert f32.gemm_tile_rows[2] in (128, 256) and f32.gemm_tile_cols[2] in (128, 256)
 
 
 def test_describe_plan_rejects_bad_grid(lib):
