@@ -440,8 +440,13 @@ def main():
     kinds = list(per)
     ew = {}
     for kname, bpe in (("momentum", 6), ("update", 6)):
+        n_launch = sum(per[k]["detail_launches"][kname] for k in kinds)
+        if n_launch == 0:
+            ew[kname] = {"fused": True,
+                         "note": "applied inside the last NS product (no kernel of its own)"}
+            continue
         ms = (sum(per[k]["detail_kernel_ms_per_step"][kname] * per[k]["ms_per_step_reps"]
-                  for k in kinds) / sum(per[k]["detail_launches"][kname] for k in kinds))
+                  for k in kinds) / n_launch)
         gbs = n_el * bpe / (ms * 1e-3) / 1e9
         ew[kname] = {"bytes_per_elem": bpe, "gbs": gbs, "frac_hbm_peak": gbs / HBM_PEAK_GBS,
                      "footprint_bytes": n_el * bpe, "timing": "detail pass",

@@ -58,6 +58,7 @@ class Result:
     u_free_err: List[float] = field(default_factory=list)  # U vs free-running oracle
     m_err: List[float] = field(default_factory=list)
     x_err: List[float] = field(default_factory=list)
+    dx_err: List[float] = field(default_factory=list)  # X_t - X_0 against the oracle's
     fulls: List[bool] = field(default_factory=list)
     final_params: List[np.ndarray] = field(default_factory=list)
     final_mom: List[np.ndarray] = field(default_factory=list)
@@ -65,7 +66,8 @@ class Result:
 
     def worst(self) -> Dict[str, float]:
         f = lambda v: max(v) if v else 0.0
-        return dict(u=f(self.u_err), u_free=f(self.u_free_err), m=f(self.m_err), x=f(self.x_err))
+        return dict(u=f(self.u_err), u_free=f(self.u_free_err), m=f(self.m_err), x=f(self.x_err),
+                    dx=f(self.dx_err))
 
 
 def make_inputs(case: Case):
@@ -106,6 +108,7 @@ def run_case(case: Case, keep_updates: bool = False) -> Result:
     params_h, grads_h = make_inputs(case)
     params = [p.cuda() for p in params_h]
     x_ref = [p.double().numpy() for p in params_h]
+    x_init = [x.copy() for x in x_ref]
     res = Result()
     for t in range(case.steps):
         g_dev = [g.cuda() for g in grads_h[t]]
@@ -120,6 +123,11 @@ def run_case(case: Case, keep_updates: bool = False) -> Result:
         torch.cuda.synchronize()
         for k, (r, c, gr, gc) in enumerate(case.mats):
             m_gpu = opt.get_momentum(k).double().cpu().numpy()
+            torch.cuda.synchronize()
+            res.m_err.append(rel(m_gpu, rec.M[k]))
+            x_gpu = params[k].double().cpu().numpy()
+            res.x_err.append(rel(x_gpu, x_ref[k]))
+            res.dx_err.append(rel(x_gpu - x_init[k], x_ref[k] - x_init[k]))
             u_gpu = opt.get_update(k).double().cpu().numpy()
             torch.cuda.synchronize()
             # Teacher forcing: the oracle orthogonalizes the GPU's own state.
@@ -133,8 +141,6 @@ def run_case(case: Case, keep_updates: bool = False) -> Result:
                 p, q = (r, c) if full else (r // gr, c // gc)
                 u_free = u_free / O.rms_scale(p, q, case.rms_beta)
             res.u_free_err.append(rel(u_gpu, u_free))
-            res.m_err.append(rel(m_gpu, rec.M[k]))
-            res.x_err.append(rel(params[k].double().cpu().numpy(), x_ref[k]))
             if keep_updates:
                 res.updates.setdefault(t, []).append(u_gpu)
     torch.cuda.synchronize()
