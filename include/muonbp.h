@@ -57,6 +57,8 @@ typedef struct {
 /* Options.  Defaults (muonbp_options_default) follow Algorithm 2:
  * K = 5, (a, b, c) = (2, -1.5, 0.5), eps = 1e-7, no Nesterov, no RMS scaling,
  * bf16 params, momentum and NS operands, automatic tile shapes. */
+#define MUONBP_MAX_COEFFS 16
+
 typedef struct {
   int32_t ns_steps;         /* K >= 0, Newton-Schulz iterations (Alg. 2)       */
   float a, b, c;            /* quintic coefficients (Alg. 2)                   */
@@ -88,6 +90,11 @@ typedef struct {
                                tile's K loop shared by that many workgroups
                                (fp32 partial sums added by the last one to
                                finish); 0 = no split. */
+  int32_t coeff_count;      /* 0 = every NS iteration uses (a, b, c) above;
+                               1..MUONBP_MAX_COEFFS = iteration k uses
+                               coeff_table[min(k, coeff_count - 1)] (tuned or
+                               per-iteration quintics, Sec. 2.2). */
+  float coeff_table[3 * MUONBP_MAX_COEFFS];  /* (a_k, b_k, c_k) triples */
 } muonbp_options;
 
 /* Fill *opt with the defaults above.  NULL is ignored. */
@@ -125,6 +132,11 @@ muonbp_status muonbp_step(muonbp_ctx* ctx, void* const* params,
 
 /* Change eta_block and eta_full for later steps (learning-rate schedules). */
 muonbp_status muonbp_set_lr(muonbp_ctx* ctx, float lr_block, float lr_full);
+
+/* Change the period P for later steps (a period schedule, or an adaptive
+ * period: the next step is full iff P > 0 and step mod P = 0, Alg. 1).
+ * P = 0 means infinity.  E_INVALID for P < 0 (the context stays usable). */
+muonbp_status muonbp_set_period(muonbp_ctx* ctx, int64_t period);
 
 /* Change the stream used by later calls. */
 muonbp_status muonbp_set_stream(muonbp_ctx* ctx, void* hip_stream);

@@ -55,16 +55,32 @@ NS_A, NS_B, NS_C = 2.0, -1.5, 0.5
 NS_EPS = 1e-7
 
 
+def ns_coefficients(coeffs, K: int) -> List[Tuple[float, float, float]]:
+    """(a, b, c) of each of the K iterations.  ``coeffs`` is one triple (the
+    same quintic every iteration, as printed in Algorithm 2) or a table of
+    triples, one per iteration, whose last entry repeats past its end (the
+    tuned or per-iteration coefficients that Sec. 2.2 mentions)."""
+    arr = np.asarray(coeffs, dtype=np.float64)
+    if arr.ndim == 1:
+        if arr.shape != (3,):
+            raise ValueError("coeffs must be (a, b, c) or a table of them")
+        return [tuple(arr)] * K
+    if arr.ndim != 2 or arr.shape[1] != 3 or arr.shape[0] == 0:
+        raise ValueError("coeffs must be (a, b, c) or a table of them")
+    return [tuple(arr[min(k, arr.shape[0] - 1)]) for k in range(K)]
+
+
 def orthogonalize_via_ns(G, K: int = 5, eps: float = NS_EPS,
-                         coeffs: Tuple[float, float, float] = (NS_A, NS_B, NS_C),
+                         coeffs=(NS_A, NS_B, NS_C),
                          transpose_tall: bool = True) -> np.ndarray:
     """Algorithm 2 (Orthogonalize-via-NS), in fp64.
 
     X <- G / (||G||_F + eps); K times: A <- X X^T, B <- b A + c A^2,
-    X <- a X + B X.  With ``transpose_tall`` the iteration runs on G^T when G
-    has more rows than columns and the result is transposed back.
+    X <- a X + B X, with iteration k's (a, b, c) from ``ns_coefficients``.
+    With ``transpose_tall`` the iteration runs on G^T when G has more rows
+    than columns and the result is transposed back.
     """
-    a, b, c = (float(v) for v in coeffs)
+    table = ns_coefficients(coeffs, K)
     G = np.asarray(G, dtype=np.float64)
     if G.ndim != 2:
         raise ValueError("G must be a matrix")
@@ -72,7 +88,7 @@ def orthogonalize_via_ns(G, K: int = 5, eps: float = NS_EPS,
     if transposed:
         G = G.T
     X = G / (np.linalg.norm(G, "fro") + eps)
-    for _ in range(K):
+    for a, b, c in table:
         A = X @ X.T
         B = b * A + c * (A @ A)
         X = a * X + B @ X
@@ -154,7 +170,7 @@ class OracleConfig:
     weight_decay: float = 0.0
     ns_steps: int = 5
     eps: float = NS_EPS
-    coeffs: Tuple[float, float, float] = (NS_A, NS_B, NS_C)
+    coeffs: tuple = (NS_A, NS_B, NS_C)  # one (a, b, c), or a per-iteration table
     nesterov: bool = False
     scale_mode: int = 0        # 0: s = 1 (Algorithm 1);  1: RMS matching
     rms_beta: float = 1.0

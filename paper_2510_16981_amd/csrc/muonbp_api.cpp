@@ -30,7 +30,7 @@ struct PlanDev {
   ScaleDesc* scale = nullptr;
   PackDesc* pack = nullptr;
   TileRef* pack_tiles = nullptr;
-  GemmDesc* descs = nullptr;             // kDescPerProblem per problem
+  GemmDesc* descs = nullptr;             // Layout::desc_per_problem per problem
   std::vector<TileRef*> phase_tiles;     // one tile list per launch phase
   UpdDesc* upd = nullptr;
   std::vector<UpdDesc> upd_host;  // for muonbp_get_update
@@ -98,6 +98,23 @@ muonbp_status hip_fail(muonbp_ctx* c, hipError_t e, const char* what) {
   return MUONBP_E_HIP;
 }
 
+// Polynomial descriptors per problem: one for the constant quintic, else
+// one per table entry that some iteration uses.
+int poly_slots(const muonbp_options& o) {
+  if (o.coeff_count <= 0) return 1;
+  return std::max(1, std::min(o.coeff_count, o.ns_steps));
+}
+
+// Iteration k's (a, b, c) (Alg. 2; a table's last entry repeats).
+void ns_coeffs(const muonbp_options& o, int k, float* a, float* b, float* c) {
+  if (o.coeff_count <= 0) {
+    *a = o.a, *b = o.b, *c = o.c;
+    return;
+  }
+  const int e = std::min(k, o.coeff_count - 1);
+  *a = o.coeff_table[3 * e], *b = o.coeff_table[3 * e + 1], *c = o.coeff_table[3 * e + 2];
+}
+
 std::string validate_opts(const muonbp_options& o) {
   if (o.ns_steps < 0 || o.ns_steps > 1000) return "ns_steps must be in [0, 1000]";
   if (!(o.eps >= 0.f) || !std::isfinite(o.eps)) return "eps must be finite and >= 0";
@@ -108,6 +125,9 @@ std::string validate_opts(const muonbp_options& o) {
   if (!std::isfinite(o.rms_beta)) return "rms_beta must be finite";
   if (o.tile_policy < 0 || o.tile_policy > kNumGemmVariants) return "tile_policy out of range";
   if (o.k_split < 0 || o.k_split > kMaxKSplit) return "k_split out of range";
+  if (o.coeff_count < 0 || o.coeff_count > MUONBP_MAX_COEFFS) return "coeff_count out of range";
+  for (int i = 0; i < 3 * o.coeff_count; ++i)
+    if (!std::isfinite(o.coeff_table[i])) return "coefficients must be finite";
   return "";
 }
 
@@ -172,14 +192,18 @@ hipError_t build_plan_tables(muonbp_ctx* c, int full) {
     for (int q = 0; q < 2; ++q)
       descs.push_back(GemmDesc{at(p.off_z[q]), at(p.off_z[q]), nullptr, at(p.off_a), at(p.off_a),
                                S, S, Lr, Lp, Lp, 0, Sp, Sp, 1.f, 0.f, 0.f, 1});
-    // Polynomial: B = c A A^T + b A + a I (A symmetric; the a I term carries
-    // Algorithm 2's a X into the next product).
-    descs.push_back(GemmDesc{at(p.off_a), at(p.off_a), at(p.off_a), at(p.off_b), at(p.off_b), S, S,
-                             S, Sp, Sp, Sp, Sp, Sp, o.c, o.b, o.a, 1});
     // Apply: Z_{1-q} = (a I + B) Z_q (= a Z_q + B Z_q), also stored transposed.
     for (int q = 0; q < 2; ++q)
       descs.push_back(GemmDesc{at(p.off_b), at(p.off_zt[q]), nullptr, at(p.off_z[1 - q]),
                                at(p.off_zt[1 - q]), S, Lr, S, Sp, Sp, 0, Lp, Sp, 1.f, 0.f, 0.f, 0});
+    // Polynomial of iteration k: B = c_k A A^T + b_k A + a_k I (A symmetric;
+    // the a I term carries Algorithm 2's a X into the apply).
+    for (int k = 0; k < c->lay.poly_slots; ++k) {
+      float a, b, cc;
+      ns_coeffs(o, k, &a, &b, &cc);
+      descs.push_back(GemmDesc{at(p.off_a), at(p.off_a), at(p.off_a), at(p.off_b), at(p.off_b), S,
+                               S, S, Sp, Sp, Sp, Sp, Sp, cc, b, a, 1});
+    }
   }
   // Update table: U of every block after K iterations (buffer K mod 2).
   const int fin = o.ns_steps & 1;
@@ -355,7 +379,7 @@ muonbp_status muonbp_describe_plan(const muonbp_matrix* mats, int32_t n_mats,
   bool shape_err = false;
   try {
     if (!build_layout(shapes.data(), n_mats, int(dtype_size(o.ns_dtype)), o.ns_steps,
-                      o.tile_policy, o.k_split, &lay, &shape_err)
+                      poly_slots(o), o.tile_policy, o.k_split, &lay, &shape_err)
              .empty())
       return shape_err ? MUONBP_E_SHAPE : MUONBP_E_INVALID;
   } catch (const std::bad_alloc&) {
@@ -405,7 +429,7 @@ muonbp_status muonbp_create(const muonbp_matrix* mats, int32_t n_mats, int64_t p
   try {
     bool shape_err = false;
     std::string msg = build_layout(shapes.data(), n_mats, int(dtype_size(o.ns_dtype)), o.ns_steps,
-                                   o.tile_policy, o.k_split, &c->lay, &shape_err);
+                                   poly_slots(o), o.tile_policy, o.k_split, &c->lay, &shape_err);
     if (!msg.empty()) {
       free_ctx(c);
       return shape_err ? MUONBP_E_SHAPE : MUONBP_E_INVALID;
@@ -563,6 +587,13 @@ muonbp_status muonbp_set_lr(muonbp_ctx* c, float lr_block, float lr_full) {
     return fail(c, MUONBP_E_INVALID, "learning rates must be finite");
   c->lr_block = lr_block;
   c->lr_full = lr_full;
+  return MUONBP_OK;
+}
+
+muonbp_status muonbp_set_period(muonbp_ctx* c, int64_t period) {
+  if (!c) return MUONBP_E_INVALID;
+  if (period < 0) return fail(c, MUONBP_E_INVALID, "period must be >= 0 (0 = infinity)");
+  c->period = period;
   return MUONBP_OK;
 }
 

@@ -76,14 +76,16 @@ void append_tiles(const Problem& p, GemmKind kind, int v, int32_t desc,
         if (kind == kApply || i <= j) out->push_back(TileRef{desc, int32_t((i << 16) | j)});
 }
 
-int32_t slot_of(GemmKind kind, int iter) {
+int32_t slot_of(GemmKind kind, int iter, int poly_slots) {
   const int q = iter & 1;
-  return kind == kGram ? kSlotGram0 + q : kind == kPoly ? kSlotPoly : kSlotApply0 + q;
+  return kind == kGram ? kSlotGram0 + q
+         : kind == kPoly ? kSlotPoly0 + std::min(iter, poly_slots - 1)
+                         : kSlotApply0 + q;
 }
 
 // Launch schedule of the K NS iterations: three launches per iteration
 // (every problem's Gram, then polynomial, then apply).
-void build_phases(Plan* plan, int ns_steps) {
+void build_phases(Plan* plan, int ns_steps, int poly_slots, int desc_per_problem) {
   plan->phases.clear();
   plan->split_floats = plan->split_slots = 0;
   const int32_t np = int32_t(plan->probs.size());
@@ -96,7 +98,8 @@ void build_phases(Plan* plan, int ns_steps) {
       std::vector<TileRef> logical;
       for (int32_t pi = 0; pi < np; ++pi)
         append_tiles(plan->probs[pi], GemmKind(kind), phase.variant,
-                     pi * kDescPerProblem + slot_of(GemmKind(kind), iter), &logical);
+                     pi * desc_per_problem + slot_of(GemmKind(kind), iter, poly_slots),
+                     &logical);
       if (phase.nsplit > 1) {
         // The shares of one tile are adjacent, so that the XCD order below
         // keeps them on one XCD (one L2) as a rule.
@@ -246,11 +249,12 @@ double ns_unit_dense_flops(int64_t S, int64_t L, int K) {
 }
 
 std::string build_layout(const MatrixShape* mats, int32_t n_mats,
-                         int ns_elem_bytes, int ns_steps, int tile_policy, int k_split,
-                         Layout* out, bool* shape_error) {
+                         int ns_elem_bytes, int ns_steps, int poly_slots, int tile_policy,
+                         int k_split, Layout* out, bool* shape_error) {
   *shape_error = false;
   if (!mats || n_mats <= 0) return "mats must be a non-empty array";
   if (ns_steps < 0) return "ns_steps must be >= 0";
+  if (poly_slots < 1 || poly_slots > 64) return "poly_slots out of range";
   if (tile_policy < 0 || tile_policy > kNumGemmVariants) return "tile_policy out of range";
   if (k_split < 0 || k_split > kMaxKSplit) return "k_split out of range";
   Layout L;
@@ -273,6 +277,8 @@ std::string build_layout(const MatrixShape* mats, int32_t n_mats,
     elems += m.rows * m.cols;
   }
   L.total_elems = elems;
+  L.poly_slots = poly_slots;
+  L.desc_per_problem = kSlotPoly0 + poly_slots;
 
   // Blocks in matrix order, row-major inside each grid; segments per block.
   for (int32_t k = 0; k < n_mats; ++k) {
@@ -345,7 +351,7 @@ std::string build_layout(const MatrixShape* mats, int32_t n_mats,
       if (plan.tiles_per_iter[kind] * plan.nsplit[kind] > int64_t(std::numeric_limits<int32_t>::max() / 2))
         return "too many tiles";
     }
-    build_phases(&plan, ns_steps);
+    build_phases(&plan, ns_steps, poly_slots, kSlotPoly0 + poly_slots);
     if (plan.pack_tiles.size() > size_t(std::numeric_limits<int32_t>::max() / 2))
       return "too many tiles";
   }

@@ -50,11 +50,11 @@ struct Problem {
 // The three grouped products of one NS iteration.
 enum GemmKind { kGram = 0, kPoly = 1, kApply = 2 };
 
-// GEMM descriptors per problem: Gram reading Z[0] / Z[1], the polynomial,
-// apply reading Z[0] / Z[1].  TileRef::prob of a GEMM tile is
-// problem * kDescPerProblem + slot.
-enum DescSlot { kSlotGram0 = 0, kSlotGram1 = 1, kSlotPoly = 2, kSlotApply0 = 3, kSlotApply1 = 4 };
-constexpr int kDescPerProblem = 5;
+// GEMM descriptors per problem: Gram reading Z[0] / Z[1], apply reading
+// Z[0] / Z[1], then one polynomial per distinct iteration coefficient set
+// (kSlotPoly0 + k for iteration k, the last one repeated).  TileRef::prob
+// of a GEMM tile is problem * Layout::desc_per_problem + slot.
+enum DescSlot { kSlotGram0 = 0, kSlotGram1 = 1, kSlotApply0 = 2, kSlotApply1 = 3, kSlotPoly0 = 4 };
 
 // One grouped GEMM launch of a step.
 struct GemmPhase {
@@ -84,6 +84,8 @@ struct Layout {
   std::vector<BlockPlan> blocks;
   std::vector<SegDesc> segs;
   int64_t total_elems = 0;
+  int32_t poly_slots = 1;        // distinct polynomial descriptors per problem
+  int32_t desc_per_problem = 5;  // kSlotPoly0 + poly_slots
   Plan plan[2];  // [0] block plan, [1] full plan
 };
 
@@ -95,7 +97,8 @@ struct Layout {
 // Returns "" on success, else a message (with *shape_error telling shape
 // vs. argument).
 std::string build_layout(const MatrixShape* mats, int32_t n_mats,
-                         int ns_elem_bytes, int ns_steps, int tile_policy, int k_split,
+                         int ns_elem_bytes, int ns_steps, int poly_slots, int tile_policy,
+                         int k_split,
                          Layout* out, bool* shape_error);
 
 // Tile shape the planner picks for one grouped product.

@@ -41,7 +41,8 @@ class Options(ctypes.Structure):
                 ("scale_mode", ctypes.c_int32), ("rms_beta", ctypes.c_float),
                 ("param_dtype", ctypes.c_int), ("state_dtype", ctypes.c_int),
                 ("ns_dtype", ctypes.c_int), ("tile_policy", ctypes.c_int32),
-                ("k_split", ctypes.c_int32)]
+                ("k_split", ctypes.c_int32), ("coeff_count", ctypes.c_int32),
+                ("coeff_table", ctypes.c_float * (3 * 16))]
 
 
 class PlanInfo(ctypes.Structure):
@@ -80,6 +81,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                          ctypes.POINTER(Options), P, ctypes.POINTER(P)]),
         "muonbp_step": (ctypes.c_int, [P, ctypes.POINTER(P), ctypes.POINTER(P), I64]),
         "muonbp_set_lr": (ctypes.c_int, [P, F, F]),
+        "muonbp_set_period": (ctypes.c_int, [P, I64]),
         "muonbp_set_stream": (ctypes.c_int, [P, P]),
         "muonbp_get_momentum": (ctypes.c_int, [P, I32, P]),
         "muonbp_set_momentum": (ctypes.c_int, [P, I32, P]),
@@ -102,13 +104,26 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     return lib
 
 
+MAX_COEFFS = 16
+
+
 def options_default(**overrides) -> Options:
+    """Library defaults with fields overridden by keyword; ``coeffs`` (a list
+    of (a, b, c) triples, one per NS iteration, the last repeated) fills
+    coeff_count and coeff_table."""
     o = Options()
     load_library().muonbp_options_default(ctypes.byref(o))
+    table = overrides.pop("coeffs", None)
     for k, v in overrides.items():
         if not hasattr(o, k):
             raise AttributeError(k)
         setattr(o, k, v)
+    if table is not None:
+        if not 1 <= len(table) <= MAX_COEFFS:
+            raise ValueError(f"1..{MAX_COEFFS} coefficient triples")
+        o.coeff_count = len(table)
+        for i, (a, b, c) in enumerate(table):
+            o.coeff_table[3 * i:3 * i + 3] = (float(a), float(b), float(c))
     return o
 
 
@@ -193,6 +208,10 @@ class MuonBP:
 
     def set_lr(self, lr_block: float, lr_full: float) -> None:
         self._check(self.lib.muonbp_set_lr(self.ctx, float(lr_block), float(lr_full)), "set_lr")
+
+    def set_period(self, period: int) -> None:
+        self._check(self.lib.muonbp_set_period(self.ctx, int(period)), "set_period")
+        self.period = int(period)
 
     def set_stream(self, stream) -> None:
         self._check(self.lib.muonbp_set_stream(self.ctx, ctypes.c_void_p(stream.cuda_stream)),

@@ -49,6 +49,8 @@ class Case:
     zero_mats: Sequence[int] = ()
     tile_policy: int = 0
     k_split: int = 0
+    coeffs: Optional[Sequence[tuple]] = None  # per-iteration (a, b, c) table
+    period_schedule: Optional[Dict[int, int]] = None  # step -> new period (set before it)
     check_steps: Optional[Sequence[int]] = None  # None = every step
 
 
@@ -92,11 +94,12 @@ def run_case(case: Case, keep_updates: bool = False) -> Result:
     import torch
     from paper_2510_16981_amd import muonbp as mb
 
+    extra = {} if case.coeffs is None else {"coeffs": list(case.coeffs)}
     opts = mb.options_default(ns_steps=case.ns_steps, nesterov=case.nesterov,
                               scale_mode=case.scale_mode, rms_beta=case.rms_beta,
                               param_dtype=DT[case.param], state_dtype=DT[case.state],
                               ns_dtype=DT[case.ns], tile_policy=case.tile_policy,
-                              k_split=case.k_split)
+                              k_split=case.k_split, **extra)
     opt = mb.MuonBP(case.mats, case.period, case.lr_block, case.lr_full, case.momentum,
                     case.weight_decay, options=opts)
     orc = O.MuonBPOracle([O.MatrixSpec(*m) for m in case.mats],
@@ -104,13 +107,18 @@ def run_case(case: Case, keep_updates: bool = False) -> Result:
                                         lr_full=case.lr_full, momentum=case.momentum,
                                         weight_decay=case.weight_decay, ns_steps=case.ns_steps,
                                         nesterov=bool(case.nesterov), scale_mode=case.scale_mode,
-                                        rms_beta=case.rms_beta))
+                                        rms_beta=case.rms_beta,
+                                        coeffs=(O.NS_A, O.NS_B, O.NS_C) if case.coeffs is None
+                                        else tuple(case.coeffs)))
     params_h, grads_h = make_inputs(case)
     params = [p.cuda() for p in params_h]
     x_ref = [p.double().numpy() for p in params_h]
     x_init = [x.copy() for x in x_ref]
     res = Result()
     for t in range(case.steps):
+        if case.period_schedule and t in case.period_schedule:
+            opt.set_period(case.period_schedule[t])
+            orc.cfg.period = case.period_schedule[t]
         g_dev = [g.cuda() for g in grads_h[t]]
         opt.step(params, g_dev, t)
         full = opt.is_full(t)
@@ -133,6 +141,8 @@ def run_case(case: Case, keep_updates: bool = False) -> Result:
             # Teacher forcing: the oracle orthogonalizes the GPU's own state.
             y = g64[k] + case.momentum * m_gpu if case.nesterov else m_gpu
             ns = dict(K=case.ns_steps)
+            if case.coeffs is not None:
+                ns["coeffs"] = list(case.coeffs)
             u_tf = O.orthogonalize_via_ns(y, **ns) if full else \
                 O.orthogonalize_blockwise(y, (gr, gc), **ns)
             res.u_err.append(rel(u_gpu, u_tf))

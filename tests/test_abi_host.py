@@ -52,7 +52,9 @@ def test_options_default(lib):
     assert abs(o.eps - 1e-7) < 1e-12
     assert (o.nesterov, o.scale_mode, o.rms_beta) == (0, 0, 1.0)
     assert (o.param_dtype, o.state_dtype, o.ns_dtype) == (mb.BF16, mb.BF16, mb.BF16)
-    assert (o.tile_policy, o.k_split) == (0, 0)
+    assert (o.tile_policy, o.k_split, o.coeff_count) == (0, 0, 0)
+    t = mb.options_default(coeffs=[(3.0, -3.2, 1.2), (2.0, -1.5, 0.5)])
+    assert t.coeff_count == 2 and list(t.coeff_table[:6]) == pytest.approx([3.0, -3.2, 1.2, 2.0, -1.5, 0.5])
 
 
 def test_status_strings(lib):
@@ -84,12 +86,17 @@ def test_create_rejects_bad_arguments_before_gpu(lib):
     assert _create(lib, [(8, 8, 1, 1)], opt=mb.options_default(ns_steps=-1))[0] == 1
     assert _create(lib, [(8, 8, 1, 1)], opt=mb.options_default(scale_mode=3))[0] == 1
     assert _create(lib, [(8, 8, 1, 1)], opt=mb.options_default(k_split=9))[0] == 1
+    assert _create(lib, [(8, 8, 1, 1)], opt=mb.options_default(coeff_count=17))[0] == 1
+    bad = mb.options_default(coeffs=[(2.0, -1.5, 0.5)])
+    bad.coeff_table[1] = float("nan")
+    assert _create(lib, [(8, 8, 1, 1)], opt=bad)[0] == 1
     assert _create(lib, [(8, 8, 1, 1)], opt=mb.options_default(tile_policy=14))[0] == 1
 
 
 def test_null_context_calls(lib):
     assert lib.muonbp_step(None, None, None, 0) == 1
     assert lib.muonbp_set_lr(None, 0.1, 0.1) == 1
+    assert lib.muonbp_set_period(None, 3) == 1
     assert lib.muonbp_synchronize(None) == 1
     assert lib.muonbp_get_update(None, 0, None) == 1
 
@@ -202,3 +209,13 @@ def test_k_split_applies_to_dma_pipeline_only(lib):
         for full in (False, True):
             info = mb.describe_plan(W.workload_matrices(name), full)
             assert list(info.gemm_split) == [1, 1, 1]
+
+
+def test_coefficient_table_plans_one_polynomial_per_entry(lib):
+    """A per-iteration table changes only the polynomial descriptors: the
+    same tiles, launches and flops as the constant quintic."""
+    mats = W.workload_matrices("qkv-2048x6144-bf16")
+    base = mb.describe_plan(mats, False)
+    tab = mb.describe_plan(mats, False, mb.options_default(coeffs=[(3.0, -3.2, 1.2)] * 3))
+    assert list(base.gemm_tiles) == list(tab.gemm_tiles)
+    assert base.gemm_launches == tab.gemm_launches and base.ns_flops == tab.ns_flops

@@ -155,6 +155,33 @@ def test_nesterov_rms_scaling_and_zero_gradient():
     _check(res, F32_TOL, free_u_tol=F32_TOL)
 
 
+# Per-iteration quintics (one tuned for fast growth of small singular
+# values first, the printed one last; the last entry repeats).
+COEFF_TABLE = [(3.4445, -4.7750, 2.0315), (3.0, -3.2, 1.2), (2.0, -1.5, 0.5)]
+
+
+@pytest.mark.parametrize("ns", ["bf16", "f32"])
+def test_per_iteration_coefficients(ns):
+    """Iteration k uses its own (a_k, b_k, c_k) (the polynomial launches
+    read one descriptor per table entry), against the oracle's table."""
+    announce(f"per-iteration coefficients ns={ns}")
+    st = "f32" if ns == "f32" else "bf16"
+    res = run_case(Case(mats=ALIGNED + RAGGED[2:3], period=2, steps=3, param=st, state=st, ns=ns,
+                        coeffs=COEFF_TABLE))
+    _check(res, F32_TOL if ns == "f32" else BF16_TOL)
+
+
+def test_period_schedule():
+    """set_period between steps (a period that grows during training): the
+    full / block decision of each step follows the period in force."""
+    announce("period schedule")
+    sched = {0: 1, 2: 3, 5: 0}
+    res = run_case(Case(mats=[(256, 384, 2, 3)], steps=7, period=1, param="f32", state="f32",
+                        ns="f32", period_schedule=sched))
+    assert res.fulls == [True, True, False, True, False, False, False]
+    _check(res, F32_TOL, free_u_tol=F32_TOL)
+
+
 def test_zero_ns_steps_gives_normalised_momentum():
     announce("K = 0")
     res = run_case(Case(mats=RAGGED[:2], ns_steps=0, period=2, steps=2, param="f32", state="f32",

@@ -62,6 +62,28 @@ def test_ns_closed_form_other_coefficients():
     assert _rel(got, _svd_closed_form(Z, 4, coeffs=coeffs)) <= 1e-12
 
 
+def test_ns_closed_form_per_iteration_coefficients():
+    """Iteration k with its own (a_k, b_k, c_k): each step is still an odd
+    matrix polynomial, so the closed form composes p_K o ... o p_1 on the
+    singular values.  A table shorter than K repeats its last entry; a table
+    of one entry is the constant quintic."""
+    rng = np.random.default_rng(7)
+    Z = rng.standard_normal((9, 14))
+    table = [(4.0, -5.0, 1.5), (3.4445, -4.7750, 2.0315), (2.0, -1.5, 0.5)]
+    U, s, Vt = np.linalg.svd(Z, full_matrices=False)
+    x = s / (np.linalg.norm(s) + O.NS_EPS)
+    for a, b, c in table + [table[-1]] * 2:  # K = 5: the last entry twice more
+        x = a * x + b * x ** 3 + c * x ** 5
+    want = (U * x) @ Vt
+    assert _rel(O.orthogonalize_via_ns(Z, K=5, coeffs=table), want) <= 1e-12
+    # Order matters (the p_k do not commute), so a reversed table differs.
+    assert _rel(O.orthogonalize_via_ns(Z, K=5, coeffs=table[::-1]), want) > 1e-3
+    assert np.array_equal(O.orthogonalize_via_ns(Z, K=3, coeffs=[(2.0, -1.5, 0.5)]),
+                          O.orthogonalize_via_ns(Z, K=3))
+    with pytest.raises(ValueError):
+        O.ns_coefficients([(1.0, 2.0)], 2)
+
+
 def test_ns_singular_value_band():
     """p(x) = 2x - 1.5x^3 + 0.5x^5 has p(1) = 1, p'(1) = 0 and its maximum on
     [0, 1] at x^2 = 0.8, where p = 1.12 sqrt(0.8).  The Frobenius
