@@ -15,9 +15,10 @@ before timing starts.  Printed: ONE JSON line.
     python bench.py [--gpus 1] [--steps 100] [--warmup 5] [--workload NAME]
                     [--period P] [--no-cpu-baseline]
 
-Counter support (the roofline's `traffic`): `--copy-probe MIB` runs only a
-streaming kernel of known size, and `--ingest-traffic` turns six rocprofv3
---pmc runs into profiles/k_ns_gemm_traffic_<workload>.md, which later runs
+Counter support (the roofline's `traffic` and MFMA utilisation):
+`--copy-probe MIB` runs only a streaming kernel of known size, `--mfma-probe`
+only a bf16 product of known flops, and `--ingest-counters` turns nine
+rocprofv3 --pmc runs into profiles/counters_<workload>.md, which later runs
 read as long as the kernel sources are unchanged.
 """
 
@@ -109,17 +110,16 @@ def kernel_source_digest():
 
 
 def traffic_file(workload):
-    return os.path.join(PROFILES, f"k_ns_gemm_traffic_{workload}.md")
+    return os.path.join(PROFILES, f"counters_{workload}.md")
 
 
 TRAFFIC_TAG = "traffic-json:"
 
 
-def measured_traffic(workload, launches_of):
-    """HBM bytes per k_ns_gemm launch from the committed rocprofv3 counter
-    summary (FETCH_SIZE + WRITE_SIZE, scaled by a copy of known size),
-    weighted by this run's launches of each step kind.  None when no summary
-    exists or the kernel sources changed since the counters were taken."""
+def counter_record(workload):
+    """The committed rocprofv3 counter record of a workload (written by
+    --ingest-counters), or None with the reason: no summary, or the kernel
+    sources changed since the counters were taken."""
     path = traffic_file(workload)
     if not os.path.exists(path):
         return None, "no counter summary for this workload"
@@ -132,17 +132,36 @@ def measured_traffic(workload, launches_of):
         return None, "counter summary has no traffic record"
     if rec.get("kernel_source_sha256") != kernel_source_digest():
         return None, "kernel sources changed since the counters were taken"
-    tot = n = 0
+    return rec, os.path.relpath(path, ROOT)
+
+
+def measured_counters(workload, launches_of):
+    """From the counter record, weighted by this run's NS GEMM launches of
+    each step kind: HBM bytes per launch (FETCH_SIZE + WRITE_SIZE scaled by a
+    copy of known size), executed MFMA flops per launch and the mean MFMA
+    utilisation.  (None, None, reason) when no valid record covers the run."""
+    rec, note = counter_record(workload)
+    if rec is None:
+        return None, None, note
+    n = sum(launches_of.values())
     for kind, cnt in launches_of.items():
-        if cnt and kind not in rec["bytes_per_launch"]:
-            return None, f"no counters for {kind} steps"
-        if cnt:
-            tot += rec["bytes_per_launch"][kind] * cnt
-            n += cnt
-    return (tot / n if n else None), os.path.relpath(path, ROOT)
+        if cnt and (kind not in rec["bytes_per_launch"] or kind not in rec.get("mfma", {})):
+            return None, None, f"no counters for {kind} steps"
+    if n == 0:
+        return None, None, "no NS GEMM launches"
+
+    def avg(get):
+        return sum(get(k) * c for k, c in launches_of.items() if c) / n
+
+    traffic = avg(lambda k: rec["bytes_per_launch"][k])
+    mfma = {"executed_flops_per_launch": avg(lambda k: rec["mfma"][k]["executed_flops_per_launch"]),
+            "mfma_util_pct": avg(lambda k: rec["mfma"][k]["mfma_util_pct"]),
+            "by_step_kind": rec["mfma"], "source": note}
+    return traffic, mfma, note
 
 
 COPY_KERNEL_MATCH = "neg_kernel"
+MFMA_PROBE_N = 4096
 
 
 def copy_probe(mib):
@@ -162,64 +181,203 @@ def copy_probe(mib):
           flush=True)
 
 
-def _pmc_rows(run_dir):
-    """(kernel name, counter, value) rows of a rocprofv3 --pmc csv run."""
+def mfma_probe():
+    """Check of the MFMA flop counter: three bf16 products of two 4096 x 4096
+    matrices (torch's library GEMM), 2 * 4096^3 flops each."""
+    import torch
+    n = MFMA_PROBE_N
+    a = torch.randn(n, n, device="cuda").to(torch.bfloat16)
+    b = torch.randn(n, n, device="cuda").to(torch.bfloat16)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        torch.mm(a, b)
+    torch.cuda.synchronize()
+    print(json.dumps({"mfma_probe_flops": 2 * n ** 3, "reps": 3}), flush=True)
+
+
+def _pmc_dispatches(run_dir):
+    """Dispatches of a rocprofv3 --pmc csv run: {dispatch id: {"name", "ns"
+    (duration), counter: value, ...}}."""
     import csv
     import glob
-    rows = []
+    out = {}
     for f in glob.glob(os.path.join(run_dir, "**", "*counter_collection.csv"), recursive=True):
         with open(f) as fh:
             for r in csv.DictReader(fh):
-                rows.append((r["Kernel_Name"], r["Counter_Name"], float(r["Counter_Value"])))
-    if not rows:
+                d = out.setdefault((f, r["Dispatch_Id"]), {
+                    "name": r["Kernel_Name"],
+                    "ns": int(r["End_Timestamp"]) - int(r["Start_Timestamp"])})
+                d[r["Counter_Name"]] = float(r["Counter_Value"])
+    if not out:
         raise SystemExit(f"no counter_collection.csv under {run_dir}")
-    return rows
+    return list(out.values())
 
 
-def _mean_kib(rows, counter, name_part):
-    v = [x for k, c, x in rows if c == counter and name_part in k]
-    if not v:
-        raise SystemExit(f"no {counter} rows for kernels matching {name_part!r}")
-    return sum(v) / len(v), len(v)
+def _kernel_label(name):
+    """Short label of one of the library's kernels (None for others)."""
+    import re
+    if "muonbp" not in name:
+        return None
+    m = re.search(r"(k_[a-z_]+)(<\d+, ?\d+>)?", name)
+    return (m.group(1) + (m.group(2) or "").replace(" ", "")) if m else None
 
 
-def ingest_traffic(workload, dirs, command):
-    """Write the traffic summary from six rocprofv3 --pmc runs: FETCH_SIZE and
-    WRITE_SIZE of the copy probe, of a run of block steps only (--period 0)
-    and of full steps only (--period 1).  dirs: copy_fetch, copy_write,
-    block_fetch, block_write, full_fetch, full_write."""
-    d = dict(zip(("copy_fetch", "copy_write", "block_fetch", "block_write", "full_fetch",
-                  "full_write"), dirs))
-    copy_kib = None
-    for line in open(os.path.join(d["copy_fetch"], "copy_probe.json")):
+def _by_label(rows, counter):
+    """Mean counter value and duration per kernel label."""
+    acc = {}
+    for r in rows:
+        lab = _kernel_label(r["name"])
+        if lab is None or counter not in r:
+            continue
+        a = acc.setdefault(lab, [0.0, 0.0, 0])
+        a[0] += r[counter]
+        a[1] += r["ns"]
+        a[2] += 1
+    return {k: {"value": v[0] / v[2], "us": v[1] / v[2] / 1e3, "n": v[2]} for k, v in acc.items()}
+
+
+def _json_line(path, key):
+    for line in open(path):
         if line.startswith("{"):
-            copy_kib = json.loads(line)["copy_probe_bytes"] / 1024.0
-    cf, _ = _mean_kib(_pmc_rows(d["copy_fetch"]), "FETCH_SIZE", COPY_KERNEL_MATCH)
-    cw, _ = _mean_kib(_pmc_rows(d["copy_write"]), "WRITE_SIZE", COPY_KERNEL_MATCH)
+            rec = json.loads(line)
+            if key in rec:
+                return rec
+    raise SystemExit(f"no JSON line with {key!r} in {path}")
+
+
+INGEST_DIRS = ("copy_fetch", "copy_write", "mfma_probe", "block_fetch", "block_write",
+               "block_mfma", "full_fetch", "full_write", "full_mfma")
+MFMA_COUNTERS = ("SQ_INSTS_VALU_MFMA_MOPS_BF16", "MfmaUtil", "GRBM_GUI_ACTIVE")
+# Bytes per element the elementwise kernels must move (bf16 storage):
+# momentum reads M and G and writes M; pack reads M and writes Z and Z^T;
+# update reads X and U and writes X.
+ELEMENTWISE_BYTES = {"k_momentum": 6, "k_pack": 6, "k_update": 6}
+
+
+def ingest_counters(workload, dirs, command):
+    """Write profiles/counters_<workload>.md from nine rocprofv3 --pmc runs
+    (one folder each, in INGEST_DIRS order): FETCH_SIZE and WRITE_SIZE of
+    the copy probe; the MFMA counters of the MFMA probe; then FETCH_SIZE,
+    WRITE_SIZE and the MFMA counters (MFMA_COUNTERS) of a run of block steps
+    only (--period 0) and of full steps only (--period 1), each with its
+    bench.py JSON line in b.json.
+
+    Per kernel and step kind: HBM bytes per dispatch (FETCH_SIZE and
+    WRITE_SIZE scaled by the copy probe) and the resulting GB/s; executed
+    bf16 MFMA flops per dispatch (the counter's unit is 512 flops, checked
+    against the probe's known flops) and TFLOP/s; MFMA utilisation (busy
+    MFMA cycles over active cycles times SIMDs, rocprofv3's MfmaUtil).
+    Durations are those of the counter runs' own dispatches."""
+    d = dict(zip(INGEST_DIRS, dirs))
+    copy_kib = _json_line(os.path.join(d["copy_fetch"], "copy_probe.json"),
+                          "copy_probe_bytes")["copy_probe_bytes"] / 1024.0
+
+    def probe_mean(run, counter, pick):
+        v = [r[counter] for r in _pmc_dispatches(d[run]) if counter in r and pick(r)]
+        if not v:
+            raise SystemExit(f"no {counter} dispatches in {d[run]}")
+        return v
+
+    cf = probe_mean("copy_fetch", "FETCH_SIZE", lambda r: COPY_KERNEL_MATCH in r["name"])
+    cw = probe_mean("copy_write", "WRITE_SIZE", lambda r: COPY_KERNEL_MATCH in r["name"])
+    cf, cw = sum(cf) / len(cf), sum(cw) / len(cw)
     sf, sw = copy_kib / cf, copy_kib / cw
-    per, detail = {}, {}
+    probe_flops = _json_line(os.path.join(d["mfma_probe"], "mfma_probe.json"),
+                             "mfma_probe_flops")["mfma_probe_flops"]
+    # The probe's product is the dispatch with the most MFMA work.
+    pm = max(probe_mean("mfma_probe", "SQ_INSTS_VALU_MFMA_MOPS_BF16", lambda r: True))
+    mops_unit = 512.0
+    probe_ratio = pm * mops_unit / probe_flops
+
+    tables, per_launch, mfma_rec = {}, {}, {}
     for kind in ("block", "full"):
-        f, nf = _mean_kib(_pmc_rows(d[f"{kind}_fetch"]), "FETCH_SIZE", "k_ns_gemm")
-        w, nw = _mean_kib(_pmc_rows(d[f"{kind}_write"]), "WRITE_SIZE", "k_ns_gemm")
-        per[kind] = (f * sf + w * sw) * 1024.0
-        detail[kind] = {"fetch_kib_raw": f, "write_kib_raw": w, "dispatches": [nf, nw]}
-    rec = {"kernel_source_sha256": kernel_source_digest(), "bytes_per_launch": per,
+        bj = _json_line(os.path.join(d[f"{kind}_mfma"], "b.json"), "metric")
+        n_el = bj["config"]["params"]
+        kstats = bj[kind]
+        alg_flops_launch = kstats["ns_flops_per_step"] / kstats["ns_gemm_launches_per_step"]
+        fetch = _by_label(_pmc_dispatches(d[f"{kind}_fetch"]), "FETCH_SIZE")
+        write = _by_label(_pmc_dispatches(d[f"{kind}_write"]), "WRITE_SIZE")
+        mrows = _pmc_dispatches(d[f"{kind}_mfma"])
+        mops = _by_label(mrows, "SQ_INSTS_VALU_MFMA_MOPS_BF16")
+        util = _by_label(mrows, "MfmaUtil")
+        gui = _by_label(mrows, "GRBM_GUI_ACTIVE")
+        rows = []
+        for lab in sorted(set(fetch) | set(mops)):
+            f, w = fetch.get(lab), write.get(lab)
+            byt = (f["value"] * sf + w["value"] * sw) * 1024.0 if f and w else None
+            us = f["us"] if f else mops[lab]["us"]
+            flops = mops[lab]["value"] * mops_unit if lab in mops else None
+            alg = (n_el * ELEMENTWISE_BYTES[lab]) if lab in ELEMENTWISE_BYTES else None
+            rows.append({
+                "kernel": lab, "dispatches": f["n"] if f else mops[lab]["n"], "us": us,
+                "hbm_bytes": byt, "hbm_gbs": byt / (us * 1e3) if byt else None,
+                "alg_bytes": alg, "alg_gbs": alg / (us * 1e3) if alg else None,
+                "mfma_flops": flops, "mfma_us": mops[lab]["us"] if lab in mops else None,
+                "mfma_tflops": (flops / (mops[lab]["us"] * 1e-6) / 1e12) if flops else None,
+                "mfma_util": util[lab]["value"] if lab in util else None,
+                "gui_active": gui[lab]["value"] if lab in gui else None})
+        tables[kind] = rows
+        g = [r for r in rows if r["kernel"].startswith("k_ns_gemm")]
+        nf = sum(r["dispatches"] for r in g)
+        per_launch[kind] = sum(r["hbm_bytes"] * r["dispatches"] for r in g) / nf
+        nm = sum(r["dispatches"] for r in g if r["mfma_flops"] is not None)
+        ex = sum(r["mfma_flops"] * r["dispatches"] for r in g if r["mfma_flops"] is not None) / nm
+        ut = sum(r["mfma_util"] * r["dispatches"] for r in g if r["mfma_util"] is not None) / nm
+        mfma_rec[kind] = {"executed_flops_per_launch": ex, "algorithmic_flops_per_launch":
+                          alg_flops_launch, "mfma_util_pct": ut}
+
+    rec = {"kernel_source_sha256": kernel_source_digest(), "bytes_per_launch": per_launch,
            "scale": {"fetch": sf, "write": sw}, "copy_kib": copy_kib,
-           "copy_raw_kib": {"fetch": cf, "write": cw}, "detail": detail}
+           "copy_raw_kib": {"fetch": cf, "write": cw}, "mfma": mfma_rec,
+           "mfma_probe_ratio": probe_ratio}
     path = traffic_file(workload)
+
+    def fmt(x, spec):
+        return "" if x is None else format(x, spec)
+
     with open(path, "w") as fh:
-        fh.write(f"# k_ns_gemm HBM traffic, {workload}\n\n")
-        fh.write("rocprofv3 counter runs (each on its own, FETCH_SIZE then WRITE_SIZE, KiB per "
-                 "dispatch), averaged over every k_ns_gemm dispatch of the run and scaled by what "
-                 "the same counter reads for a plain copy of known size.\n\n")
+        fh.write(f"# rocprofv3 counters per kernel, {workload}\n\n")
+        fh.write("Counter runs, one counter set per run: FETCH_SIZE, WRITE_SIZE, and the MFMA "
+                 "set (SQ_INSTS_VALU_MFMA_MOPS_BF16, MfmaUtil, GRBM_GUI_ACTIVE).  Block steps "
+                 "only (--period 0) and full steps only (--period 1); every dispatch of the run "
+                 "is averaged per kernel.  Durations are those of the counter runs' dispatches "
+                 "(serialised by the counter collection).\n\n")
         fh.write("Commands:\n\n```\n" + command.strip() + "\n```\n\n")
-        fh.write("| | copy probe | block-step launches | full-step launches |\n|---|---|---|---|\n")
-        fh.write(f"| FETCH_SIZE KiB/dispatch (raw) | {cf:.0f} | {detail['block']['fetch_kib_raw']:.0f} | "
-                 f"{detail['full']['fetch_kib_raw']:.0f} |\n")
-        fh.write(f"| WRITE_SIZE KiB/dispatch (raw) | {cw:.0f} | {detail['block']['write_kib_raw']:.0f} | "
-                 f"{detail['full']['write_kib_raw']:.0f} |\n")
-        fh.write(f"| scale (copy bytes / counter) | fetch {sf:.3f}, write {sw:.3f} | | |\n")
-        fh.write(f"| HBM bytes per launch (scaled) | | {per['block']:.4g} | {per['full']:.4g} |\n\n")
+        fh.write("Calibration:\n\n")
+        fh.write(f"* HBM bytes: a streaming kernel reading and writing {copy_kib / 1024:.0f} MiB "
+                 f"reads FETCH_SIZE {cf:.0f} KiB, WRITE_SIZE {cw:.0f} KiB per dispatch: scale "
+                 f"fetch {sf:.3f}, write {sw:.3f}.\n")
+        fh.write(f"* MFMA flops: SQ_INSTS_VALU_MFMA_MOPS_BF16 counts units of 512 flops; the "
+                 f"{MFMA_PROBE_N}^3 bf16 product of the probe reads {pm * mops_unit:.4g} flops "
+                 f"against {probe_flops:.4g} (ratio {probe_ratio:.3f}).\n")
+        fh.write("* MfmaUtil = busy MFMA cycles summed over SIMDs / (active GPU cycles x SIMDs), "
+                 "in percent.  Its active cycles (GRBM_GUI_ACTIVE) span the counter collection "
+                 "window, a few microseconds longer than the dispatch itself (a 3 us kernel "
+                 "reads as about 10 us of active cycles at the 2.4 GHz clock), so it understates "
+                 "the utilisation of short dispatches; the TFLOP/s column divides the counted "
+                 "flops by the dispatch's own duration instead.\n\n")
+        for kind in ("block", "full"):
+            m = mfma_rec[kind]
+            fh.write(f"## {kind} steps\n\n")
+            fh.write(f"NS GEMM launches: {per_launch[kind]:.4g} HBM bytes, "
+                     f"{m['executed_flops_per_launch']:.4g} executed MFMA flops "
+                     f"({m['algorithmic_flops_per_launch']:.4g} algorithmic, ratio "
+                     f"{m['executed_flops_per_launch'] / m['algorithmic_flops_per_launch']:.3f}), "
+                     f"MfmaUtil {m['mfma_util_pct']:.1f}% per launch on average.\n\n")
+            fh.write("| kernel | dispatches | us | HBM MB | HBM GB/s | % of 8 TB/s | algorithmic "
+                     "GB/s | MFMA GFLOP | MFMA TFLOP/s | % of 2.5 PF | MfmaUtil % |\n"
+                     "|---|---|---|---|---|---|---|---|---|---|---|\n")
+            for r in tables[kind]:
+                fh.write(f"| `{r['kernel']}` | {r['dispatches']} | {r['us']:.2f} | "
+                         f"{fmt(r['hbm_bytes'] and r['hbm_bytes'] / 1e6, '.2f')} | "
+                         f"{fmt(r['hbm_gbs'], '.0f')} | "
+                         f"{fmt(r['hbm_gbs'] and 100 * r['hbm_gbs'] / HBM_PEAK_GBS, '.1f')} | "
+                         f"{fmt(r['alg_gbs'], '.0f')} | "
+                         f"{fmt(r['mfma_flops'] and r['mfma_flops'] / 1e9, '.2f')} | "
+                         f"{fmt(r['mfma_tflops'], '.0f')} | "
+                         f"{fmt(r['mfma_tflops'] and 100 * r['mfma_tflops'] / BF16_PEAK_TFLOPS, '.1f')} | "
+                         f"{fmt(r['mfma_util'], '.1f')} |\n")
+            fh.write("\n")
         fh.write(TRAFFIC_TAG + " " + json.dumps(rec) + "\n")
     print(path)
 
@@ -278,10 +436,11 @@ def ingest_kernel_trace(workload, run_dir, command):
 
 
 def make_inputs(mats, rank):
-    """Params (one per matrix) and grads.  Small workloads: the exact seeded
-    host inputs.  Large ones: GPU-drawn timing-only inputs, one gradient
-    tensor per distinct shape shared by its matrices (grads are read-only and
-    the step's cost does not depend on their values)."""
+    """Params and grads, one tensor each per matrix.  Small workloads: the
+    exact seeded host inputs.  Large ones: GPU-drawn timing-only inputs (the
+    step's cost does not depend on their values).  Every matrix has its own
+    gradient in its own memory, so no step reads a gradient another matrix
+    has just pulled into the caches."""
     import torch
     from paper_2510_16981_amd import workload as W
     n_el = sum(r * c for r, c, _, _ in mats)
@@ -291,14 +450,9 @@ def make_inputs(mats, rank):
                  for k, (r, c, _, _) in enumerate(mats)]
         return params, grads, "synthetic (seeded host draws)"
     params = [W.device_param(r, c, 0, k) for k, (r, c, _, _) in enumerate(mats)]
-    by_shape = {}
-    grads = []
-    for k, (r, c, _, _) in enumerate(mats):
-        if (r, c) not in by_shape:
-            by_shape[(r, c)] = W.device_grad(r, c, rank, 0, k)
-        grads.append(by_shape[(r, c)])
+    grads = [W.device_grad(r, c, rank, 0, k) for k, (r, c, _, _) in enumerate(mats)]
     torch.cuda.synchronize()
-    return params, grads, "synthetic (GPU-drawn, one gradient per distinct shape)"
+    return params, grads, "synthetic (GPU-drawn, one gradient per matrix)"
 
 
 def main():
@@ -311,17 +465,20 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", type=int, metavar="MIB", default=None,
                     help="only run a plain copy of MIB MiB (counter calibration) and exit")
-    ap.add_argument("--ingest-traffic", nargs=6, metavar="DIR", default=None,
-                    help="write the traffic summary of --workload from six rocprofv3 --pmc "
-                         "csv runs: copy FETCH, copy WRITE, block FETCH, block WRITE, full "
-                         "FETCH, full WRITE (no GPU use)")
+    ap.add_argument("--mfma-probe", action="store_true",
+                    help="only run three 4096^3 bf16 products (MFMA counter check) and exit")
+    ap.add_argument("--ingest-counters", nargs=9, metavar="DIR", default=None,
+                    help="write the per-kernel counter summary of --workload from nine "
+                         "rocprofv3 --pmc csv runs: copy FETCH, copy WRITE, MFMA probe, then "
+                         "FETCH, WRITE and MFMA counters of block steps and of full steps "
+                         "(no GPU use)")
     ap.add_argument("--ingest-kernel-trace", metavar="DIR", default=None,
                     help="write the kernel summary of --workload from a rocprofv3 --kernel-trace "
                          "--stats csv run of bench.py whose JSON line is DIR/bench.json (no GPU use)")
     ap.add_argument("--command", default="", help="with --ingest-*: the commands that made the runs")
     args = ap.parse_args()
-    if args.ingest_traffic:
-        ingest_traffic(args.workload, args.ingest_traffic, args.command)
+    if args.ingest_counters:
+        ingest_counters(args.workload, args.ingest_counters, args.command)
         return
     if args.ingest_kernel_trace:
         ingest_kernel_trace(args.workload, args.ingest_kernel_trace, args.command)
@@ -332,9 +489,12 @@ def main():
         sys.exit(2)
 
     import torch
-    if args.copy_probe:
+    if args.copy_probe or args.mfma_probe:
         torch.cuda.set_device(0)
-        copy_probe(args.copy_probe)
+        if args.copy_probe:
+            copy_probe(args.copy_probe)
+        else:
+            mfma_probe()
         return
     from paper_2510_16981_amd import muonbp as mb
     from paper_2510_16981_amd import workload as W
@@ -460,11 +620,11 @@ def main():
     launches = sum(timed_prof[k]["ns_span"][1] for k in kinds)
     achieved = tot_flops / (tot_ms * 1e-3) / 1e12
     launches_of = {k: timed_prof[k]["ns_span"][1] for k in kinds}
-    traffic, traffic_note = measured_traffic(name, launches_of)
+    traffic, mfma_counters, traffic_note = measured_counters(name, launches_of)
     roofline = {"kernel": "k_ns_gemm (bf16, all tile shapes)", "bound": "mfma",
                 "achieved": achieved, "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                 "frac": achieved / BF16_PEAK_TFLOPS, "traffic": traffic,
-                "traffic_note": traffic_note,
+                "traffic_note": traffic_note, "mfma_counters": mfma_counters,
                 "launches": launches, "avg_launch_us": tot_ms * 1e3 / launches,
                 "avg_flops_per_launch": tot_flops / launches,
                 "timing": ("HIP events on the library stream around each step's back-to-back "

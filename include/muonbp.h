@@ -95,6 +95,13 @@ typedef struct {
                                coeff_table[min(k, coeff_count - 1)] (tuned or
                                per-iteration quintics, Sec. 2.2). */
   float coeff_table[3 * MUONBP_MAX_COEFFS];  /* (a_k, b_k, c_k) triples */
+  int32_t stream_hint;      /* cache policy of the momentum and update
+                               kernels' streamed reads and writes: 0 = chosen
+                               from the step's size (nontemporal when
+                               params x (2 param + 1 state elements) exceed
+                               256 MiB, the last-level cache; plain below,
+                               where the data stays cached between the
+                               step's kernels); 1 = plain; 2 = nontemporal. */
 } muonbp_options;
 
 /* Fill *opt with the defaults above.  NULL is ignored. */

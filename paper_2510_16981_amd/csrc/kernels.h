@@ -11,7 +11,7 @@ enum class DType { F32 = 0, BF16 = 1 };
 
 // M <- mu M + G over every block segment (eq. NTR); partials[seg] = sum of
 // squares of the NS input of that segment (M, or G + mu M with Nesterov).
-hipError_t launch_momentum(DType grad_t, DType mom_t, bool vec, int n_segs,
+hipError_t launch_momentum(DType grad_t, DType mom_t, bool vec, bool nt, int n_segs,
                            const SegDesc* segs, const BlockDesc* blocks,
                            const MatPtrs* mats, void* mom, float mu,
                            int nesterov, float* partials, hipStream_t s);
@@ -39,7 +39,7 @@ hipError_t launch_ns_gemm(DType ns_t, int variant, int n_tiles, const GemmDesc* 
                           hipStream_t s);
 
 // X <- X (1 - eta lambda) - eta s_b U_b over every block segment.
-hipError_t launch_update(DType param_t, DType ns_t, bool vec, int n_segs,
+hipError_t launch_update(DType param_t, DType ns_t, bool vec, bool nt, int n_segs,
                          const SegDesc* segs, const BlockDesc* blocks,
                          const MatPtrs* mats, const UpdDesc* upd, float eta,
                          float lambda, hipStream_t s);

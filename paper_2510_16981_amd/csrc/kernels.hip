@@ -68,6 +68,63 @@ __device__ __forceinline__ void store8(float* p, const float f[8]) {
   reinterpret_cast<float4*>(p)[1] = make_float4(f[4], f[5], f[6], f[7]);
 }
 
+// Eight consecutive elements as raw 16-byte words.  NT: loaded and stored
+// with the nontemporal hint, for steps whose streamed data (read once or
+// written once per step) is far larger than the last-level cache; smaller
+// steps keep plain accesses, whose data stays cache-resident between the
+// kernels of a step.
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+template <typename T> struct Raw8 {
+  u32x4_t w[sizeof(T) / 2];
+};
+template <bool NT, typename T> __device__ __forceinline__ Raw8<T> load8r(const T* p) {
+  Raw8<T> r;
+  const u32x4_t* q = reinterpret_cast<const u32x4_t*>(p);
+#pragma unroll
+  for (int i = 0; i < int(sizeof(T) / 2); ++i) r.w[i] = NT ? __builtin_nontemporal_load(q + i) : q[i];
+  return r;
+}
+__device__ __forceinline__ void unpack8(const Raw8<bf16>& r, float f[8]) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    f[2 * i] = __uint_as_float(r.w[0][i] << 16);
+    f[2 * i + 1] = __uint_as_float(r.w[0][i] & 0xffff0000u);
+  }
+}
+__device__ __forceinline__ void unpack8(const Raw8<float>& r, float f[8]) {
+#pragma unroll
+  for (int i = 0; i < 8; ++i) f[i] = __uint_as_float(r.w[i >> 2][i & 3]);
+}
+template <bool NT> __device__ __forceinline__ void store_w(u32x4_t* p, u32x4_t v) {
+  if (NT)
+    __builtin_nontemporal_store(v, p);
+  else
+    *p = v;
+}
+template <bool NT> __device__ __forceinline__ void store8r(bf16* p, const float f[8]) {
+  union {
+    bf16 h[8];
+    u32x4_t v;
+  } u;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) u.h[i] = bf16(f[i]);
+  store_w<NT>(reinterpret_cast<u32x4_t*>(p), u.v);
+}
+template <bool NT> __device__ __forceinline__ void store8r(float* p, const float f[8]) {
+  u32x4_t* q = reinterpret_cast<u32x4_t*>(p);
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    u32x4_t v;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) v[k] = __float_as_uint(f[4 * i + k]);
+    store_w<NT>(q + i, v);
+  }
+}
+
+// Chunks of 8 elements each thread of an elementwise kernel loads before it
+// does any arithmetic (memory-level parallelism of the streaming loops).
+constexpr int kStreamUnroll = 4;
+
 // Deterministic workgroup sum (fixed butterfly inside each wave, fixed
 // wave order across the workgroup).
 __device__ __forceinline__ float block_sum(float v) {
@@ -84,7 +141,7 @@ __device__ __forceinline__ float block_sum(float v) {
 
 // ---------------------------------------------------------------- momentum
 
-template <typename TG, typename TM, bool VEC>
+template <typename TG, typename TM, bool VEC, bool NT>
 __global__ __launch_bounds__(kThreads) void k_momentum(
     const SegDesc* __restrict__ segs, const BlockDesc* __restrict__ blocks,
     const MatPtrs* __restrict__ mats, TM* __restrict__ mom, float mu,
@@ -99,20 +156,36 @@ __global__ __launch_bounds__(kThreads) void k_momentum(
   if (VEC) {
     const int vpr = cols >> 3;
     const int nv = sd.nrows * vpr;
-    for (int v = threadIdx.x; v < nv; v += kThreads) {
-      const int r = v / vpr;
-      const int64_t o = int64_t(r) * bd.ld + ((v - r * vpr) << 3);
-      float gf[8], mf[8];
-      load8(g + o, gf);
-      load8(m + o, mf);
+    for (int v0 = threadIdx.x; v0 < nv; v0 += kThreads * kStreamUnroll) {
+      Raw8<TG> gr[kStreamUnroll];
+      Raw8<TM> mr[kStreamUnroll];
+      int64_t o[kStreamUnroll];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) mf[i] = fmaf(mu, mf[i], gf[i]);
-      store8(m + o, mf);
+      for (int u = 0; u < kStreamUnroll; ++u) {
+        const int v = v0 + kThreads * u;
+        if (v < nv) {
+          const int r = v / vpr;
+          o[u] = int64_t(r) * bd.ld + ((v - r * vpr) << 3);
+          gr[u] = load8r<NT>(g + o[u]);
+          mr[u] = load8r<NT>(m + o[u]);
+        }
+      }
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const float mr = rt<TM>(mf[i]);
-        const float y = nesterov ? fmaf(mu, mr, gf[i]) : mr;
-        acc = fmaf(y, y, acc);
+      for (int u = 0; u < kStreamUnroll; ++u) {
+        if (v0 + kThreads * u < nv) {
+          float gf[8], mf[8];
+          unpack8(gr[u], gf);
+          unpack8(mr[u], mf);
+#pragma unroll
+          for (int i = 0; i < 8; ++i) mf[i] = fmaf(mu, mf[i], gf[i]);
+          store8r<NT>(m + o[u], mf);
+#pragma unroll
+          for (int i = 0; i < 8; ++i) {
+            const float mq = rt<TM>(mf[i]);
+            const float y = nesterov ? fmaf(mu, mq, gf[i]) : mq;
+            acc = fmaf(y, y, acc);
+          }
+        }
       }
     }
   } else {
@@ -996,7 +1069,7 @@ __global__ __launch_bounds__(kThreads) void k_ns_gemm_dmap(const GemmDesc* __res
 
 // ---------------------------------------------------------------- update
 
-template <typename TP, typename TU, bool VEC>
+template <typename TP, typename TU, bool VEC, bool NT>
 __global__ __launch_bounds__(kThreads) void k_update(
     const SegDesc* __restrict__ segs, const BlockDesc* __restrict__ blocks,
     const MatPtrs* __restrict__ mats, const UpdDesc* __restrict__ upd, float eta,
@@ -1011,15 +1084,31 @@ __global__ __launch_bounds__(kThreads) void k_update(
   if (VEC) {
     const int vpr = cols >> 3;
     const int nv = sd.nrows * vpr;
-    for (int v = threadIdx.x; v < nv; v += kThreads) {
-      const int r = v / vpr, c = (v - r * vpr) << 3;
-      const int64_t ox = int64_t(r) * bd.ld + c, ou = int64_t(r) * ud.ldu + c;
-      float xf[8], uf[8];
-      load8(x + ox, xf);
-      load8(u + ou, uf);
+    for (int v0 = threadIdx.x; v0 < nv; v0 += kThreads * kStreamUnroll) {
+      Raw8<TP> xr[kStreamUnroll];
+      Raw8<TU> ur[kStreamUnroll];
+      int64_t ox[kStreamUnroll];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) xf[i] = fmaf(decay, xf[i], -step * uf[i]);
-      store8(x + ox, xf);
+      for (int k = 0; k < kStreamUnroll; ++k) {
+        const int v = v0 + kThreads * k;
+        if (v < nv) {
+          const int r = v / vpr, c = (v - r * vpr) << 3;
+          ox[k] = int64_t(r) * bd.ld + c;
+          xr[k] = load8r<NT>(x + ox[k]);
+          ur[k] = load8r<NT>(u + int64_t(r) * ud.ldu + c);
+        }
+      }
+#pragma unroll
+      for (int k = 0; k < kStreamUnroll; ++k) {
+        if (v0 + kThreads * k < nv) {
+          float xf[8], uf[8];
+          unpack8(xr[k], xf);
+          unpack8(ur[k], uf);
+#pragma unroll
+          for (int i = 0; i < 8; ++i) xf[i] = fmaf(decay, xf[i], -step * uf[i]);
+          store8r<NT>(x + ox[k], xf);
+        }
+      }
     }
   } else {
     const int n = sd.nrows * cols;
@@ -1041,7 +1130,7 @@ hipError_t dispatch1(DType a, F&& f) {
 }
 }  // namespace
 
-hipError_t launch_momentum(DType grad_t, DType mom_t, bool vec, int n_segs,
+hipError_t launch_momentum(DType grad_t, DType mom_t, bool vec, bool nt, int n_segs,
                            const SegDesc* segs, const BlockDesc* blocks,
                            const MatPtrs* mats, void* mom, float mu, int nesterov,
                            float* partials, hipStream_t s) {
@@ -1050,12 +1139,15 @@ hipError_t launch_momentum(DType grad_t, DType mom_t, bool vec, int n_segs,
     return dispatch1(mom_t, [&](auto m) {
       using TG = decltype(g);
       using TM = decltype(m);
-      if (vec)
-        hipLaunchKernelGGL((k_momentum<TG, TM, true>), dim3(n_segs), dim3(kThreads), 0, s, segs,
-                           blocks, mats, static_cast<TM*>(mom), mu, nesterov, partials);
+      if (vec && nt)
+        hipLaunchKernelGGL((k_momentum<TG, TM, true, true>), dim3(n_segs), dim3(kThreads), 0, s,
+                           segs, blocks, mats, static_cast<TM*>(mom), mu, nesterov, partials);
+      else if (vec)
+        hipLaunchKernelGGL((k_momentum<TG, TM, true, false>), dim3(n_segs), dim3(kThreads), 0, s,
+                           segs, blocks, mats, static_cast<TM*>(mom), mu, nesterov, partials);
       else
-        hipLaunchKernelGGL((k_momentum<TG, TM, false>), dim3(n_segs), dim3(kThreads), 0, s, segs,
-                           blocks, mats, static_cast<TM*>(mom), mu, nesterov, partials);
+        hipLaunchKernelGGL((k_momentum<TG, TM, false, false>), dim3(n_segs), dim3(kThreads), 0, s,
+                           segs, blocks, mats, static_cast<TM*>(mom), mu, nesterov, partials);
       return hipGetLastError();
     });
   });
@@ -1162,7 +1254,8 @@ hipError_t launch_ns_gemm(DType ns_t, int variant, int n_tiles, const GemmDesc* 
   });
 }
 
-hipError_t launch_update(DType param_t, DType ns_t, bool vec, int n_segs, const SegDesc* segs,
+hipError_t launch_update(DType param_t, DType ns_t, bool vec, bool nt, int n_segs,
+                         const SegDesc* segs,
                          const BlockDesc* blocks, const MatPtrs* mats, const UpdDesc* upd,
                          float eta, float lambda, hipStream_t s) {
   if (n_segs <= 0) return hipSuccess;
@@ -1170,12 +1263,15 @@ hipError_t launch_update(DType param_t, DType ns_t, bool vec, int n_segs, const 
     return dispatch1(ns_t, [&](auto n) {
       using TP = decltype(p);
       using TU = decltype(n);
-      if (vec)
-        hipLaunchKernelGGL((k_update<TP, TU, true>), dim3(n_segs), dim3(kThreads), 0, s, segs,
-                           blocks, mats, upd, eta, lambda);
+      if (vec && nt)
+        hipLaunchKernelGGL((k_update<TP, TU, true, true>), dim3(n_segs), dim3(kThreads), 0, s,
+                           segs, blocks, mats, upd, eta, lambda);
+      else if (vec)
+        hipLaunchKernelGGL((k_update<TP, TU, true, false>), dim3(n_segs), dim3(kThreads), 0, s,
+                           segs, blocks, mats, upd, eta, lambda);
       else
-        hipLaunchKernelGGL((k_update<TP, TU, false>), dim3(n_segs), dim3(kThreads), 0, s, segs,
-                           blocks, mats, upd, eta, lambda);
+        hipLaunchKernelGGL((k_update<TP, TU, false, false>), dim3(n_segs), dim3(kThreads), 0, s,
+                           segs, blocks, mats, upd, eta, lambda);
       return hipGetLastError();
     });
   });

@@ -73,6 +73,7 @@ struct muonbp_ctx {
   bool ptrs_valid = false;
 
   bool vec_layout = false;
+  bool stream_nt = false;  // nontemporal momentum / update accesses
   int last_plan = -1;
   bool poisoned = false;
   std::string err;
@@ -126,6 +127,7 @@ std::string validate_opts(const muonbp_options& o) {
   if (o.tile_policy < 0 || o.tile_policy > kNumGemmVariants) return "tile_policy out of range";
   if (o.k_split < 0 || o.k_split > kMaxKSplit) return "k_split out of range";
   if (o.coeff_count < 0 || o.coeff_count > MUONBP_MAX_COEFFS) return "coeff_count out of range";
+  if (o.stream_hint < 0 || o.stream_hint > 2) return "stream_hint out of range";
   for (int i = 0; i < 3 * o.coeff_count; ++i)
     if (!std::isfinite(o.coeff_table[i])) return "coefficients must be finite";
   return "";
@@ -453,6 +455,11 @@ muonbp_status muonbp_create(const muonbp_matrix* mats, int32_t n_mats, int64_t p
     vec = vec && b.cols % 8 == 0 && b.col0 % 8 == 0 && m.cols % 8 == 0 && c->lay.mat_off[b.mat] % 8 == 0;
   }
   c->vec_layout = vec;
+  // Nontemporal streaming once a step's momentum and update data cannot stay
+  // in the last-level cache anyway.
+  const int64_t streamed = c->lay.total_elems * int64_t(2 * dtype_size(o.param_dtype) +
+                                                       dtype_size(o.state_dtype));
+  c->stream_nt = o.stream_hint == 2 || (o.stream_hint == 0 && streamed > kStreamNtBytes);
 
   hipError_t e = hipGetDevice(&c->device);
   if (e != hipSuccess) {
@@ -547,8 +554,8 @@ muonbp_status muonbp_step(muonbp_ctx* c, void* const* params, const void* const*
   c->prof_full = full;
 
   e = timed(c, 0, [&] {
-    return launch_momentum(tp, tm, aligned, nsegs, c->segs, c->blocks, mats, c->mom, c->mu,
-                           o.nesterov, c->partials, s);
+    return launch_momentum(tp, tm, aligned, c->stream_nt, nsegs, c->segs, c->blocks, mats, c->mom,
+                           c->mu, o.nesterov, c->partials, s);
   });
   if (e != hipSuccess) return hip_fail(c, e, "momentum");
   e = timed(c, 1, [&] {
@@ -574,7 +581,8 @@ muonbp_status muonbp_step(muonbp_ctx* c, void* const* params, const void* const*
   const float eta = full ? c->lr_full : c->lr_block;
   bool upd_vec = aligned;
   e = timed(c, 6, [&] {
-    return launch_update(tp, tn, upd_vec, nsegs, c->segs, c->blocks, mats, pd.upd, eta, c->wd, s);
+    return launch_update(tp, tn, upd_vec, c->stream_nt, nsegs, c->segs, c->blocks, mats, pd.upd, eta,
+                         c->wd, s);
   });
   if (e != hipSuccess) return hip_fail(c, e, "update");
   c->last_plan = full;

@@ -18,6 +18,7 @@ constexpr int kNumXCDs = 8;             // dies; workgroups are dealt round-robi
 constexpr int64_t kSegTarget = 16384;   // elements per elementwise workgroup
 constexpr int64_t kWsAlignBytes = 256;  // alignment of every workspace buffer
 constexpr int kMaxKSplit = 8;           // workgroups that may share one tile's K loop
+constexpr int64_t kStreamNtBytes = int64_t(256) << 20;  // last-level cache (MALL) size
 
 struct MatrixShape {
   int64_t rows, cols;

@@ -42,7 +42,7 @@ class Options(ctypes.Structure):
                 ("param_dtype", ctypes.c_int), ("state_dtype", ctypes.c_int),
                 ("ns_dtype", ctypes.c_int), ("tile_policy", ctypes.c_int32),
                 ("k_split", ctypes.c_int32), ("coeff_count", ctypes.c_int32),
-                ("coeff_table", ctypes.c_float * (3 * 16))]
+                ("coeff_table", ctypes.c_float * (3 * 16)), ("stream_hint", ctypes.c_int32)]
 
 
 class PlanInfo(ctypes.Structure):

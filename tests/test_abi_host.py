@@ -91,6 +91,8 @@ def test_create_rejects_bad_arguments_before_gpu(lib):
     bad.coeff_table[1] = float("nan")
     assert _create(lib, [(8, 8, 1, 1)], opt=bad)[0] == 1
     assert _create(lib, [(8, 8, 1, 1)], opt=mb.options_default(tile_policy=14))[0] == 1
+    assert _create(lib, [(8, 8, 1, 1)], opt=mb.options_default(stream_hint=3))[0] == 1
+    assert _create(lib, [(8, 8, 1, 1)], opt=mb.options_default(stream_hint=-1))[0] == 1
 
 
 def test_null_context_calls(lib):

@@ -137,6 +137,17 @@ def test_k_split_deterministic():
         assert np.array_equal(x, y)
 
 
+@pytest.mark.parametrize("hint", [1, 2], ids=["plain", "nontemporal"])
+@pytest.mark.parametrize("param,state,ns", [("bf16", "bf16", "bf16"), ("f32", "f32", "f32")])
+def test_stream_hints(hint, param, state, ns):
+    """Momentum and update kernels with plain and with nontemporal accesses
+    (the choice large steps make), on vector-path and scalar-path shapes."""
+    announce(f"stream hint {hint} {param}/{state}/{ns}")
+    res = run_case(Case(mats=RAGGED[:2] + SCALAR[:1], period=2, steps=3, param=param, state=state,
+                        ns=ns, stream_hint=hint))
+    _check(res, F32_TOL if ns == "f32" else BF16_TOL)
+
+
 @pytest.mark.parametrize("param,state,ns", [("bf16", "f32", "bf16"), ("f32", "f32", "bf16"),
                                             ("f32", "bf16", "f32"), ("bf16", "bf16", "f32")])
 def test_dtype_combinations(param, state, ns):
