@@ -204,13 +204,23 @@ def _pmc_dispatches(run_dir):
     for f in glob.glob(os.path.join(run_dir, "**", "*counter_collection.csv"), recursive=True):
         with open(f) as fh:
             for r in csv.DictReader(fh):
-                d = out.setdefault((f, r["Dispatch_Id"]), {
+                d = out.setdefault((f, int(r["Dispatch_Id"])), {
                     "name": r["Kernel_Name"],
                     "ns": int(r["End_Timestamp"]) - int(r["Start_Timestamp"])})
                 d[r["Counter_Name"]] = float(r["Counter_Value"])
     if not out:
         raise SystemExit(f"no counter_collection.csv under {run_dir}")
-    return list(out.values())
+    rows = [out[k] for k in sorted(out)]
+    # Name each NS GEMM dispatch after its product: a step launches pack,
+    # then (Gram, polynomial, apply) once per iteration, then the update.
+    i = 0
+    for r in rows:
+        if "k_pack" in r["name"]:
+            i = 0
+        elif "k_ns_gemm" in r["name"]:
+            r["product"] = ("gram", "poly", "apply")[i % 3]
+            i += 1
+    return rows
 
 
 def _kernel_label(name):
@@ -222,11 +232,16 @@ def _kernel_label(name):
     return (m.group(1) + (m.group(2) or "").replace(" ", "")) if m else None
 
 
+def _row_label(r):
+    lab = _kernel_label(r["name"])
+    return f"{lab} {r['product']}" if lab and "product" in r else lab
+
+
 def _by_label(rows, counter):
     """Mean counter value and duration per kernel label."""
     acc = {}
     for r in rows:
-        lab = _kernel_label(r["name"])
+        lab = _row_label(r)
         if lab is None or counter not in r:
             continue
         a = acc.setdefault(lab, [0.0, 0.0, 0])
@@ -463,6 +478,8 @@ def main():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--period", type=int, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--apply-mode", type=int, default=0,
+                    help="library option apply_mode (0: apply reads Z row-major, 1: keeps Z^T)")
     ap.add_argument("--copy-probe", type=int, metavar="MIB", default=None,
                     help="only run a plain copy of MIB MiB (counter calibration) and exit")
     ap.add_argument("--mfma-probe", action="store_true",
@@ -514,7 +531,8 @@ def main():
 
     log(f"workload {name}: {len(mats)} matrices, {n_el / 1e6:.1f} M params; generating inputs")
     params, grads, data = make_inputs(mats, rank)
-    opt = mb.MuonBP(mats, period, lr_block, LR_FULL, MU, WD, options=mb.options_default(ns_steps=K_NS))
+    opt = mb.MuonBP(mats, period, lr_block, LR_FULL, MU, WD,
+                    options=mb.options_default(ns_steps=K_NS, apply_mode=args.apply_mode))
     torch.cuda.synchronize()
 
     t = 0

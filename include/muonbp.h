@@ -102,6 +102,11 @@ typedef struct {
                                256 MiB, the last-level cache; plain below,
                                where the data stays cached between the
                                step's kernels); 1 = plain; 2 = nontemporal. */
+  int32_t apply_mode;       /* apply product Z <- (a I + B) Z of each NS
+                               iteration: 0 = reads Z row-major through LDS
+                               transpose reads wherever the interleaved DMA
+                               kernel runs it (no Z^T kept between
+                               iterations); 1 = keeps Z^T and reads it. */
 } muonbp_options;
 
 /* Fill *opt with the defaults above.  NULL is ignored. */
@@ -177,6 +182,7 @@ typedef struct {
   double elementwise_bytes;/* algorithmic HBM bytes of the non-NS kernels    */
   int64_t workspace_bytes; /* NS workspace this plan needs                  */
   int32_t gemm_split[3];   /* workgroups sharing one tile's K loop (1 = none) */
+  int32_t apply_nn;        /* 1: the apply products read Z row-major (no Z^T) */
 } muonbp_plan_info;
 
 /* Plan description for a set of matrices without creating a context

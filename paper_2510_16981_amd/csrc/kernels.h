@@ -30,11 +30,14 @@ hipError_t launch_pack(DType mom_t, DType grad_t, DType ns_t, bool vec, int n_ti
 // Grouped C = alpha X Y^T + beta D + gamma I (+ transposed copy) over a
 // tile list whose tile shape is `variant` (GemmVariant in device_types.h);
 // each tile names its problem descriptor, which carries the coefficients.
+// nn (interleaved DMA variants only): Y is K x N row-major instead, so C =
+// alpha X Y + ...; C may then be NULL when only the transposed copy is
+// wanted.
 // nsplit > 1 (interleaved DMA variants only): n_tiles workgroups share
 // their tiles' K loops as the tile table says; ksum holds the fp32 partial
 // sums (tiles x nsplit x tile area floats) and kcount one zeroed counter per
 // tile (left zeroed on return).
-hipError_t launch_ns_gemm(DType ns_t, int variant, int n_tiles, const GemmDesc* probs,
+hipError_t launch_ns_gemm(DType ns_t, int variant, bool nn, int n_tiles, const GemmDesc* probs,
                           const TileRef* tiles, int nsplit, float* ksum, int* kcount,
                           hipStream_t s);
 

@@ -3,7 +3,7 @@
 //  * k_momentum  -- M <- mu M + G (eq. NTR / Algorithm 1), fused with the
 //                   per-segment sum of squares of the NS input.
 //  * k_scale     -- 1 / (||Y||_F + eps) per orthogonalized unit (Algorithm 2).
-//  * k_pack      -- scaled NS input, written row-major and transposed.
+//  * k_pack      -- scaled NS input, written row-major and/or transposed.
 //  * k_ns_gemm   -- grouped MFMA GEMM C = alpha X Y^T + beta D used for the
 //                   three products of every NS iteration (Algorithm 2):
 //                   A = Z Z^T, B = b A + c A A, Z' = a Z + B Z.
@@ -257,7 +257,7 @@ __global__ __launch_bounds__(kThreads) void k_pack(
         }
 #pragma unroll
         for (int e = 0; e < 8; ++e) y[e] *= s;
-        store8(ds + int64_t(r) * d.ld_s + c, y);
+        if (ds) store8(ds + int64_t(r) * d.ld_s + c, y);
       } else {
 #pragma unroll
         for (int e = 0; e < 8; ++e) y[e] = 0.f;
@@ -265,6 +265,7 @@ __global__ __launch_bounds__(kThreads) void k_pack(
 #pragma unroll
       for (int e = 0; e < 8; ++e) tile[rr][8 * ch + e] = y[e];
     }
+    if (!dt) return;  // uniform: no transposed copy wanted
     __syncthreads();
     // Transposed copy: Z^T rows c0 .. c0 + 63, chunks of 8 rows of Y.
 #pragma unroll
@@ -295,10 +296,11 @@ __global__ __launch_bounds__(kThreads) void k_pack(
       y = to_f<TM>(m[o]);
       if (nesterov) y = fmaf(mu, y, to_f<TG>(g[o]));
       y *= s;
-      ds[int64_t(r) * d.ld_s + c] = from_f<TN>(y);
+      if (ds) ds[int64_t(r) * d.ld_s + c] = from_f<TN>(y);
     }
     tile[lr + 4 * i][lc] = y;
   }
+  if (!dt) return;  // uniform: no transposed copy wanted
   __syncthreads();
 #pragma unroll 4
   for (int i = 0; i < 16; ++i) {
@@ -442,6 +444,7 @@ __device__ __forceinline__ void gemm_epilogue(f32x16_t (&acc)[TM][TN], float* st
   // their latency overlaps the previous pass.  D is added to the staged
   // rows in place, and the Ct chunks are read after that, so the transposed
   // tile needs no loads of its own (D is symmetric whenever Ct is written).
+  // C == NULL: only the transposed copy is written.
   // 32x32 accumulator layout: lane l holds column l % 32 and, for register
   // v, row 8 (v / 4) + 4 (l / 32) + v % 4.
   constexpr int P = 32 * TN + 1;
@@ -484,7 +487,7 @@ __device__ __forceinline__ void gemm_epilogue(f32x16_t (&acc)[TM][TN], float* st
       for (int e = 0; e < 8; ++e) f[e] = st[r * P + 8 * ch + e];
       if (has_d) add8<T>(f, dv[i & 1][c], beta);
       if (gamma != 0.f) add_diag(f, r0 + r, wc0 + 8 * ch, gamma);
-      store_chunk<T>(C, d.ldc, r0 + r, wc0 + 8 * ch, d.M, d.N, f);
+      if (C) store_chunk<T>(C, d.ldc, r0 + r, wc0 + 8 * ch, d.M, d.N, f);
       if (mirror && has_d) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) st[r * P + 8 * ch + e] = f[e];
@@ -742,6 +745,21 @@ __device__ __forceinline__ u32x4_t lds_read16(uint32_t addr) {
   return v;
 }
 
+typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
+
+// LDS transpose read (gfx950 ds_read_b64_tr_b16), issued without a
+// compiler-inserted wait like lds_read16.  Each group of 16 lanes reads a 4 x
+// 16 block of 16-bit elements: lane i of the group supplies the address of
+// elements 4 (i % 4) .. 4 (i % 4) + 3 of row i / 4, and receives column i of
+// the block, rows 0..3 (measured lane layout).  With a row-major K x N tile
+// that gives each lane four consecutive k of one n: half of an MFMA B
+// operand.
+__device__ __forceinline__ u32x2_t lds_read8_tr(uint32_t addr) {
+  u32x2_t v;
+  asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(v) : "v"(addr));
+  return v;
+}
+
 template <int N>
 __device__ __forceinline__ void lds_wait(u32x4_t (&f)[N]) {
   static_assert(N >= 4 && N <= 8, "fragment count");
@@ -897,7 +915,14 @@ __global__ __launch_bounds__(kThreads) void k_ns_gemm_dma(const GemmDesc* __rest
 // share order (the result does not depend on the arrival order), resets
 // the counter for the next launch and runs the epilogue; the others exit.
 // No workgroup waits for another.
-template <int BM, int BN>
+//
+// NN (Y row-major K x N, ldy its row pitch; the apply product reads Z this
+// way, so no transposed copy of Z is needed): a stage holds the Y slice as
+// 32 k-rows of BN elements, 16-byte chunk c of k-row r stored at position
+// c ^ 2 (r % 4), and the B operands come from LDS transpose reads, two per
+// fragment (k 0..3 and 4..7 of the lane's 8).  Y chunks past N and k-rows
+// past K are copied as zeros.
+template <int BM, int BN, bool NN>
 __global__ __launch_bounds__(kThreads) void k_ns_gemm_dmap(const GemmDesc* __restrict__ probs,
                                                            const TileRef* __restrict__ tiles,
                                                            int nsplit, float* __restrict__ ksum,
@@ -907,6 +932,13 @@ __global__ __launch_bounds__(kThreads) void k_ns_gemm_dmap(const GemmDesc* __res
   using T = bf16;
   constexpr int TM = G::TM, TN = G::TN, LPW = G::LPW, ES = 2, NF = TM + TN;
   constexpr int NM = TM * TN;  // MFMAs per K step
+  // LDS read instructions per K step: one per X fragment; one per Y
+  // fragment (NT) or two (NN).
+  constexpr int NR = NN ? TM + 2 * TN : NF;
+  constexpr int RPM = (NR + NM - 1) / NM;  // reads issued after each MFMA of a step
+  constexpr int CPR = BN / 8;  // NN: 16-byte chunks per staged k-row
+  static_assert(!NN || CPR % 8 == 0, "NN chunk swizzle needs BN % 64 == 0");
+  static_assert(BM % 64 == 0, "copy jj holds X rows iff jj < BM / 64");
   // MFMAs of the second step issued before the barrier: one keeps the
   // matrix pipeline busy while the barrier resolves, and leaves the rest of
   // the step to hide the next slice's reads (measured: 2-4% faster than
@@ -922,18 +954,26 @@ __global__ __launch_bounds__(kThreads) void k_ns_gemm_dmap(const GemmDesc* __res
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
 
-  const int xbytes = d.M * d.ldx * ES, ybytes = d.N * d.ldy * ES;
+  const int xbytes = d.M * d.ldx * ES, ybytes = (NN ? d.K : d.N) * d.ldy * ES;
   const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(d.X), 0, xbytes, kBufferWord3);
   const __amdgpu_buffer_rsrc_t yr = __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(d.Y), 0, ybytes, kBufferWord3);
 
+  // chunk[jj]: K chunk of an X (or NT Y) row; NN Y: the k-row in the slice.
   int voff[LPW], chunk[LPW];
 #pragma unroll
   for (int jj = 0; jj < LPW; ++jj) {
     const int u = wave + 4 * jj;
-    const int row = 16 * u + (lane >> 2);
-    const int c = (lane & 3) ^ swz(row);
-    chunk[jj] = c;
-    voff[jj] = row < BM ? ((m0 + row) * d.ldx + 8 * c) * ES : ((n0 + row - BM) * d.ldy + 8 * c) * ES;
+    if (NN && jj >= BM / 64) {  // Y slice copy (u >= BM / 16)
+      const int q = 64 * (u - BM / 16) + lane, kr = q / CPR;
+      const int cn = (q - kr * CPR) ^ (2 * (kr & 3));
+      chunk[jj] = kr;
+      voff[jj] = n0 + 8 * cn < d.N ? (kr * d.ldy + n0 + 8 * cn) * ES : ybytes;
+    } else {
+      const int row = 16 * u + (lane >> 2);
+      const int c = (lane & 3) ^ swz(row);
+      chunk[jj] = c;
+      voff[jj] = row < BM ? ((m0 + row) * d.ldx + 8 * c) * ES : ((n0 + row - BM) * d.ldy + 8 * c) * ES;
+    }
   }
   const int nk_all = (d.K + 31) / 32;
   const int kb = nsplit > 1 ? t.part * nk_all / nsplit : 0;
@@ -942,12 +982,22 @@ __global__ __launch_bounds__(kThreads) void k_ns_gemm_dmap(const GemmDesc* __res
   auto copy = [&](int kt, int jj) {
     unsigned char* base = lds + (kt % NS) * G::STAGE;
     const int k0 = kt * 32;
-    const bool kin = kt < ke && k0 + 8 * chunk[jj] < d.K;
     lds_void_t* dst = (lds_void_t*)(base + (wave + 4 * jj) * 1024);
-    if (wave + 4 * jj < BM / 16)  // uniform: X rows
-      dma16(xr, dst, kin ? voff[jj] : xbytes, k0 * ES);
-    else
-      dma16(yr, dst, kin ? voff[jj] : ybytes, k0 * ES);
+    if constexpr (NN) {
+      if (jj < BM / 64) {  // X rows (wave + 4 jj < BM / 16 for every wave)
+        const bool kin = kt < ke && k0 + 8 * chunk[jj] < d.K;
+        dma16(xr, dst, kin ? voff[jj] : xbytes, k0 * ES);
+      } else {
+        const bool kin = kt < ke && k0 + chunk[jj] < d.K;
+        dma16(yr, dst, kin ? voff[jj] : ybytes, k0 * d.ldy * ES);
+      }
+    } else {
+      const bool kin = kt < ke && k0 + 8 * chunk[jj] < d.K;
+      if (wave + 4 * jj < BM / 16)  // uniform: X rows
+        dma16(xr, dst, kin ? voff[jj] : xbytes, k0 * ES);
+      else
+        dma16(yr, dst, kin ? voff[jj] : ybytes, k0 * ES);
+    }
   };
 
   f32x16_t acc[TM][TN];
@@ -966,12 +1016,62 @@ __global__ __launch_bounds__(kThreads) void k_ns_gemm_dmap(const GemmDesc* __res
     fa[f] = lds_addr(lds) + r * kDmaRow;
     fsw[f] = swz(r);
   }
+  if (NN) {
+    // Y fragment j: n = wn 32 TN + 32 j + 16 ((lane / 16) % 2) + 4 (lane % 4)
+    // .. + 3, k-row 8 (lane / 32) + (lane % 16) / 4 (+ 16 s + 4 r); the
+    // swizzle 2 (k-row % 4) is 2 ((lane % 16) / 4).
+    const int si = lane & 15, g = lane >> 4;
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const int n = wn * 32 * TN + 32 * j + 16 * (g & 1) + 4 * (si & 3);
+      const int kr = 8 * (g >> 1) + (si >> 2);
+      fa[TM + j] = lds_addr(lds) + BM * kDmaRow + kr * (2 * BN) + (((n >> 3) ^ (2 * (si >> 2))) << 4) +
+                   8 * (si & 1);
+    }
+  }
   auto read1 = [&](int kt, int s, int f) {
     const uint32_t sbase = (kt % NS) * G::STAGE;
     const int c = 2 * s + (lane >> 5);
     return lds_read16(fa[f] + sbase + ((c ^ fsw[f]) << 4));
   };
-  auto mfma = [&](const u32x4_t (&fr)[NF], int q) {
+  // Fragments of one K step: f (X, and Y when NT) from 16-byte reads; NN Y
+  // fragments from two transpose reads each, held as halves (yl, yh) until
+  // their wait and then joined into f[TM + j].
+  constexpr int YH = NN ? TN : 1;
+  using Fr = u32x4_t[NF];
+  using Yh = u32x2_t[YH];
+  // Read instruction o (0 <= o < NR) of K step s of slice kt.
+  auto read_op = [&](Fr& f, Yh& yl, Yh& yh, int kt, int s, int o) {
+    if constexpr (!NN) {
+      f[o] = read1(kt, s, o);
+    } else {
+      if (o < TM) {
+        f[o] = read1(kt, s, o);
+      } else {
+        const int j = (o - TM) >> 1, r = (o - TM) & 1;
+        const uint32_t a = fa[TM + j] + (kt % NS) * G::STAGE + (16 * s + 4 * r) * (2 * BN);
+        if (r == 0)
+          yl[j] = lds_read8_tr(a);
+        else
+          yh[j] = lds_read8_tr(a);
+      }
+    }
+  };
+  auto frag_wait = [&](Fr& f, Yh& yl, Yh& yh) {
+    if constexpr (!NN) {
+      lds_wait(f);
+    } else {
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+      for (int i = 0; i < TM; ++i) asm volatile("" : "+v"(f[i]));
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        asm volatile("" : "+v"(yl[j]), "+v"(yh[j]));
+        f[TM + j] = __builtin_shufflevector(yl[j], yh[j], 0, 1, 2, 3);
+      }
+    }
+  };
+  auto mfma = [&](const Fr& fr, int q) {
     const int i = q / TN, j = q % TN;
     acc[i][j] = Mfma<T>::step(__builtin_bit_cast(uint4, fr[i]), __builtin_bit_cast(uint4, fr[TM + j]),
                               acc[i][j]);
@@ -985,19 +1085,21 @@ __global__ __launch_bounds__(kThreads) void k_ns_gemm_dmap(const GemmDesc* __res
   __builtin_amdgcn_s_waitcnt(vmcnt_imm((NS - 1) * LPW));
   barrier_no_fence();
   u32x4_t f0[NF], f1[NF];
+  u32x2_t y0l[YH], y0h[YH], y1l[YH], y1h[YH];
 #pragma unroll
-  for (int f = 0; f < NF; ++f) f0[f] = read1(kb, 0, f);
-  lds_wait(f0);
+  for (int o = 0; o < NR; ++o) read_op(f0, y0l, y0h, kb, 0, o);
+  frag_wait(f0, y0l, y0h);
 
   for (int kt = kb; kt < ke; ++kt) {
     // Step 0 of slice kt, with the reads of its step 1.
 #pragma unroll
     for (int q = 0; q < NM; ++q) {
       mfma(f0, q);
-      if (q < NF) f1[q] = read1(kt, 1, q);
+#pragma unroll
+      for (int o = q * RPM; o < (q + 1) * RPM && o < NR; ++o) read_op(f1, y1l, y1h, kt, 1, o);
       __builtin_amdgcn_sched_barrier(0);
     }
-    lds_wait(f1);
+    frag_wait(f1, y1l, y1h);
     // Step 1, first part.
 #pragma unroll
     for (int q = 0; q < H; ++q) {
@@ -1010,7 +1112,7 @@ __global__ __launch_bounds__(kThreads) void k_ns_gemm_dmap(const GemmDesc* __res
     __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * LPW));
     barrier_no_fence();
     // Step 1, rest, with the reads of slice kt + 1 and the refill copies.
-    constexpr int OPS = LPW + NF;
+    constexpr int OPS = LPW + NR;
 #pragma unroll
     for (int q = H; q < NM; ++q) {
       mfma(f1, q);
@@ -1018,12 +1120,12 @@ __global__ __launch_bounds__(kThreads) void k_ns_gemm_dmap(const GemmDesc* __res
       const int lo = (q - H) * OPS / R, hi = (q - H + 1) * OPS / R;
 #pragma unroll
       for (int o = lo; o < hi; ++o) {
-        if (o < NF) f0[o] = read1(kt + 1, 0, o);
-        else copy(kt + NS, o - NF);
+        if (o < NR) read_op(f0, y0l, y0h, kt + 1, 0, o);
+        else copy(kt + NS, o - NR);
       }
       __builtin_amdgcn_sched_barrier(0);
     }
-    lds_wait(f0);
+    frag_wait(f0, y0l, y0h);
   }
   // Zero-filled copies past the share may still be in flight: let them land
   // before the epilogue reuses the ring.
@@ -1183,10 +1285,11 @@ hipError_t launch_pack(DType mom_t, DType grad_t, DType ns_t, bool vec, int n_ti
   });
 }
 
-hipError_t launch_ns_gemm(DType ns_t, int variant, int n_tiles, const GemmDesc* probs,
+hipError_t launch_ns_gemm(DType ns_t, int variant, bool nn, int n_tiles, const GemmDesc* probs,
                           const TileRef* tiles, int nsplit, float* ksum, int* kcount,
                           hipStream_t s) {
   if (nsplit > 1 && (!ksum || !kcount || !gemm_is_dmap(variant))) return hipErrorInvalidValue;
+  if (nn && !gemm_is_dmap(variant)) return hipErrorInvalidValue;
   if (n_tiles <= 0) return hipSuccess;
   return dispatch1(ns_t, [&](auto n) {
     using TN = decltype(n);
@@ -1214,9 +1317,13 @@ hipError_t launch_ns_gemm(DType ns_t, int variant, int n_tiles, const GemmDesc* 
       case kGemmDmaP256x192:
       case kGemmDmaP192x192:
         if constexpr (std::is_same<TN, bf16>::value) {
-#define MUONBP_DMAP(BM_, BN_)                                                                  \
-  hipLaunchKernelGGL((k_ns_gemm_dmap<BM_, BN_>), dim3(n_tiles), dim3(kThreads), 0, s, probs, \
-                     tiles, nsplit, ksum, kcount)
+#define MUONBP_DMAP(BM_, BN_)                                                                   \
+  if (nn)                                                                                      \
+    hipLaunchKernelGGL((k_ns_gemm_dmap<BM_, BN_, true>), dim3(n_tiles), dim3(kThreads), 0, s,  \
+                       probs, tiles, nsplit, ksum, kcount);                                    \
+  else                                                                                         \
+    hipLaunchKernelGGL((k_ns_gemm_dmap<BM_, BN_, false>), dim3(n_tiles), dim3(kThreads), 0, s, \
+                       probs, tiles, nsplit, ksum, kcount)
           switch (variant) {
             case kGemmDmaP128x128: MUONBP_DMAP(128, 128); break;
             case kGemmDmaP256x128: MUONBP_DMAP(256, 128); break;

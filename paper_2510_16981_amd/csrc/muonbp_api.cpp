@@ -128,6 +128,7 @@ std::string validate_opts(const muonbp_options& o) {
   if (o.k_split < 0 || o.k_split > kMaxKSplit) return "k_split out of range";
   if (o.coeff_count < 0 || o.coeff_count > MUONBP_MAX_COEFFS) return "coeff_count out of range";
   if (o.stream_hint < 0 || o.stream_hint > 2) return "stream_hint out of range";
+  if (o.apply_mode < 0 || o.apply_mode > 1) return "apply_mode out of range";
   for (int i = 0; i < 3 * o.coeff_count; ++i)
     if (!std::isfinite(o.coeff_table[i])) return "coefficients must be finite";
   return "";
@@ -176,14 +177,16 @@ hipError_t build_plan_tables(muonbp_ctx* c, int full) {
     d.rows = int32_t(p.rows);
     d.cols = int32_t(p.cols);
     d.tiles_c = int32_t((p.cols + kPackTile - 1) / kPackTile);
-    // Z = Y (S = rows) or Y^T (S = cols); Z^T the other way round.
+    // Z = Y (S = rows) or Y^T (S = cols); Z^T the other way round, needed
+    // by the NT apply, or as U when there are no iterations.
+    const bool want_zt = !plan.nn_apply || o.ns_steps == 0;
     if (!p.trans) {
       d.dst_s = at(p.off_z[0]);
       d.ld_s = p.Lp;
-      d.dst_t = at(p.off_zt[0]);
+      d.dst_t = want_zt ? at(p.off_zt[0]) : nullptr;
       d.ld_t = p.Sp;
     } else {
-      d.dst_s = at(p.off_zt[0]);
+      d.dst_s = want_zt ? at(p.off_zt[0]) : nullptr;
       d.ld_s = p.Sp;
       d.dst_t = at(p.off_z[0]);
       d.ld_t = p.Lp;
@@ -194,10 +197,20 @@ hipError_t build_plan_tables(muonbp_ctx* c, int full) {
     for (int q = 0; q < 2; ++q)
       descs.push_back(GemmDesc{at(p.off_z[q]), at(p.off_z[q]), nullptr, at(p.off_a), at(p.off_a),
                                S, S, Lr, Lp, Lp, 0, Sp, Sp, 1.f, 0.f, 0.f, 1});
-    // Apply: Z_{1-q} = (a I + B) Z_q (= a Z_q + B Z_q), also stored transposed.
-    for (int q = 0; q < 2; ++q)
-      descs.push_back(GemmDesc{at(p.off_b), at(p.off_zt[q]), nullptr, at(p.off_z[1 - q]),
-                               at(p.off_zt[1 - q]), S, Lr, S, Sp, Sp, 0, Lp, Sp, 1.f, 0.f, 0.f, 0});
+    // Apply: Z_{1-q} = (a I + B) Z_q (= a Z_q + B Z_q).  NT: Y = Z_q^T and
+    // Z_{1-q} also stored transposed.  NN: Y = Z_q itself, and only the last
+    // apply of a transposed unit writes Z^T (as U, where the update reads it).
+    auto apply_desc = [&](int q, bool last) {
+      if (!plan.nn_apply)
+        return GemmDesc{at(p.off_b), at(p.off_zt[q]), nullptr, at(p.off_z[1 - q]), at(p.off_zt[1 - q]),
+                        S, Lr, S, Sp, Sp, 0, Lp, Sp, 1.f, 0.f, 0.f, 0};
+      const bool t_only = last && p.trans;
+      return GemmDesc{at(p.off_b), at(p.off_z[q]), nullptr, t_only ? nullptr : at(p.off_z[1 - q]),
+                      t_only ? at(p.off_zt[1 - q]) : nullptr, S, Lr, S, Sp, Lp, 0, Lp, Sp,
+                      1.f, 0.f, 0.f, 0};
+    };
+    for (int q = 0; q < 2; ++q) descs.push_back(apply_desc(q, false));
+    descs.push_back(apply_desc((o.ns_steps + 1) & 1, true));  // iteration K - 1 reads Z_{(K-1) mod 2}
     // Polynomial of iteration k: B = c_k A A^T + b_k A + a_k I (A symmetric;
     // the a I term carries Algorithm 2's a X into the apply).
     for (int k = 0; k < c->lay.poly_slots; ++k) {
@@ -381,7 +394,7 @@ muonbp_status muonbp_describe_plan(const muonbp_matrix* mats, int32_t n_mats,
   bool shape_err = false;
   try {
     if (!build_layout(shapes.data(), n_mats, int(dtype_size(o.ns_dtype)), o.ns_steps,
-                      poly_slots(o), o.tile_policy, o.k_split, &lay, &shape_err)
+                      poly_slots(o), o.tile_policy, o.k_split, o.apply_mode, &lay, &shape_err)
              .empty())
       return shape_err ? MUONBP_E_SHAPE : MUONBP_E_INVALID;
   } catch (const std::bad_alloc&) {
@@ -398,6 +411,7 @@ muonbp_status muonbp_describe_plan(const muonbp_matrix* mats, int32_t n_mats,
     out->gemm_split[k] = p.nsplit[k];
   }
   out->gemm_launches = int64_t(p.phases.size());
+  out->apply_nn = p.nn_apply ? 1 : 0;
   out->ns_flops = p.ns_flops;
   out->ns_dense_flops = p.ns_dense_flops;
   const double pb = double(dtype_size(o.param_dtype)), sb = double(dtype_size(o.state_dtype)),
@@ -431,7 +445,8 @@ muonbp_status muonbp_create(const muonbp_matrix* mats, int32_t n_mats, int64_t p
   try {
     bool shape_err = false;
     std::string msg = build_layout(shapes.data(), n_mats, int(dtype_size(o.ns_dtype)), o.ns_steps,
-                                   poly_slots(o), o.tile_policy, o.k_split, &c->lay, &shape_err);
+                                   poly_slots(o), o.tile_policy, o.k_split, o.apply_mode, &c->lay,
+                                   &shape_err);
     if (!msg.empty()) {
       free_ctx(c);
       return shape_err ? MUONBP_E_SHAPE : MUONBP_E_INVALID;
@@ -572,7 +587,7 @@ muonbp_status muonbp_step(muonbp_ctx* c, void* const* params, const void* const*
   for (int ph = 0; ph < nphases; ++ph) {
     const GemmPhase& P = plan.phases[ph];
     e = timed(c, 3 + P.kind, [&] {
-      return launch_ns_gemm(tn, P.variant, int(P.tiles.size()), pd.descs, pd.phase_tiles[ph],
+      return launch_ns_gemm(tn, P.variant, P.nn, int(P.tiles.size()), pd.descs, pd.phase_tiles[ph],
                             P.nsplit, c->ksum, c->kcount, s);
     });
     if (e != hipSuccess) return hip_fail(c, e, "NS GEMM");

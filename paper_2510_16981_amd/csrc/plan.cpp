@@ -76,11 +76,12 @@ void append_tiles(const Problem& p, GemmKind kind, int v, int32_t desc,
         if (kind == kApply || i <= j) out->push_back(TileRef{desc, int32_t((i << 16) | j)});
 }
 
-int32_t slot_of(GemmKind kind, int iter, int poly_slots) {
+int32_t slot_of(GemmKind kind, int iter, int ns_steps, int poly_slots) {
   const int q = iter & 1;
-  return kind == kGram ? kSlotGram0 + q
+  return kind == kGram   ? kSlotGram0 + q
          : kind == kPoly ? kSlotPoly0 + std::min(iter, poly_slots - 1)
-                         : kSlotApply0 + q;
+         : iter == ns_steps - 1 ? kSlotApplyLast
+                                : kSlotApply0 + q;
 }
 
 // Launch schedule of the K NS iterations: three launches per iteration
@@ -95,10 +96,11 @@ void build_phases(Plan* plan, int ns_steps, int poly_slots, int desc_per_problem
       phase.variant = plan->variant[kind];
       phase.kind = kind;
       phase.nsplit = plan->nsplit[kind];
+      phase.nn = kind == kApply && plan->nn_apply;
       std::vector<TileRef> logical;
       for (int32_t pi = 0; pi < np; ++pi)
         append_tiles(plan->probs[pi], GemmKind(kind), phase.variant,
-                     pi * desc_per_problem + slot_of(GemmKind(kind), iter, poly_slots),
+                     pi * desc_per_problem + slot_of(GemmKind(kind), iter, ns_steps, poly_slots),
                      &logical);
       if (phase.nsplit > 1) {
         // The shares of one tile are adjacent, so that the XCD order below
@@ -250,7 +252,7 @@ double ns_unit_dense_flops(int64_t S, int64_t L, int K) {
 
 std::string build_layout(const MatrixShape* mats, int32_t n_mats,
                          int ns_elem_bytes, int ns_steps, int poly_slots, int tile_policy,
-                         int k_split, Layout* out, bool* shape_error) {
+                         int k_split, int apply_mode, Layout* out, bool* shape_error) {
   *shape_error = false;
   if (!mats || n_mats <= 0) return "mats must be a non-empty array";
   if (ns_steps < 0) return "ns_steps must be >= 0";
@@ -351,6 +353,7 @@ std::string build_layout(const MatrixShape* mats, int32_t n_mats,
       if (plan.tiles_per_iter[kind] * plan.nsplit[kind] > int64_t(std::numeric_limits<int32_t>::max() / 2))
         return "too many tiles";
     }
+    plan.nn_apply = apply_mode == 0 && gemm_is_dmap(plan.variant[kApply]);
     build_phases(&plan, ns_steps, poly_slots, kSlotPoly0 + poly_slots);
     if (plan.pack_tiles.size() > size_t(std::numeric_limits<int32_t>::max() / 2))
       return "too many tiles";

@@ -52,16 +52,25 @@ struct Problem {
 enum GemmKind { kGram = 0, kPoly = 1, kApply = 2 };
 
 // GEMM descriptors per problem: Gram reading Z[0] / Z[1], apply reading
-// Z[0] / Z[1], then one polynomial per distinct iteration coefficient set
-// (kSlotPoly0 + k for iteration k, the last one repeated).  TileRef::prob
-// of a GEMM tile is problem * Layout::desc_per_problem + slot.
-enum DescSlot { kSlotGram0 = 0, kSlotGram1 = 1, kSlotApply0 = 2, kSlotApply1 = 3, kSlotPoly0 = 4 };
+// Z[0] / Z[1], the apply of the last iteration (which writes U where the
+// update reads it), then one polynomial per distinct iteration coefficient
+// set (kSlotPoly0 + k for iteration k, the last one repeated).
+// TileRef::prob of a GEMM tile is problem * Layout::desc_per_problem + slot.
+enum DescSlot {
+  kSlotGram0 = 0,
+  kSlotGram1 = 1,
+  kSlotApply0 = 2,
+  kSlotApply1 = 3,
+  kSlotApplyLast = 4,
+  kSlotPoly0 = 5
+};
 
 // One grouped GEMM launch of a step.
 struct GemmPhase {
   int32_t variant = 0;         // GemmVariant of every tile
   int32_t kind = 0;            // GemmKind
   int32_t nsplit = 1;          // workgroups per tile, each on a share of K
+  bool nn = false;             // apply reading Z row-major (no Z^T operand)
   std::vector<TileRef> tiles;  // workgroup order
 };
 
@@ -72,6 +81,10 @@ struct Plan {
   std::vector<TileRef> pack_tiles;
   int32_t variant[3] = {0, 0, 0};     // GemmVariant per GemmKind
   int32_t nsplit[3] = {1, 1, 1};      // K split per GemmKind
+  // Apply products read Z row-major through LDS transpose reads (the
+  // interleaved DMA kernel runs them): no Z^T is kept between iterations;
+  // only the last apply of a transposed unit writes Z^T, as U.
+  bool nn_apply = false;
   int64_t tiles_per_iter[3] = {0, 0, 0};
   int64_t split_floats = 0;           // fp32 partial sums of the largest split launch
   int64_t split_slots = 0;            // tiles of the largest split launch (one counter each)
@@ -86,7 +99,7 @@ struct Layout {
   std::vector<SegDesc> segs;
   int64_t total_elems = 0;
   int32_t poly_slots = 1;        // distinct polynomial descriptors per problem
-  int32_t desc_per_problem = 5;  // kSlotPoly0 + poly_slots
+  int32_t desc_per_problem = 6;  // kSlotPoly0 + poly_slots
   Plan plan[2];  // [0] block plan, [1] full plan
 };
 
@@ -99,7 +112,7 @@ struct Layout {
 // vs. argument).
 std::string build_layout(const MatrixShape* mats, int32_t n_mats,
                          int ns_elem_bytes, int ns_steps, int poly_slots, int tile_policy,
-                         int k_split,
+                         int k_split, int apply_mode,
                          Layout* out, bool* shape_error);
 
 // Tile shape the planner picks for one grouped product.

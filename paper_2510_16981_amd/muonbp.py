@@ -42,7 +42,8 @@ class Options(ctypes.Structure):
                 ("param_dtype", ctypes.c_int), ("state_dtype", ctypes.c_int),
                 ("ns_dtype", ctypes.c_int), ("tile_policy", ctypes.c_int32),
                 ("k_split", ctypes.c_int32), ("coeff_count", ctypes.c_int32),
-                ("coeff_table", ctypes.c_float * (3 * 16)), ("stream_hint", ctypes.c_int32)]
+                ("coeff_table", ctypes.c_float * (3 * 16)), ("stream_hint", ctypes.c_int32),
+                ("apply_mode", ctypes.c_int32)]
 
 
 class PlanInfo(ctypes.Structure):
@@ -53,7 +54,7 @@ class PlanInfo(ctypes.Structure):
                 ("ns_dense_flops", ctypes.c_double),
                 ("elementwise_bytes", ctypes.c_double),
                 ("workspace_bytes", ctypes.c_int64),
-                ("gemm_split", ctypes.c_int32 * 3)]
+                ("gemm_split", ctypes.c_int32 * 3), ("apply_nn", ctypes.c_int32)]
 
 
 class Profile(ctypes.Structure):

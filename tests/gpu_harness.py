@@ -50,6 +50,7 @@ class Case:
     tile_policy: int = 0
     k_split: int = 0
     stream_hint: int = 0
+    apply_mode: int = 0
     coeffs: Optional[Sequence[tuple]] = None  # per-iteration (a, b, c) table
     period_schedule: Optional[Dict[int, int]] = None  # step -> new period (set before it)
     check_steps: Optional[Sequence[int]] = None  # None = every step
@@ -100,7 +101,8 @@ def run_case(case: Case, keep_updates: bool = False) -> Result:
                               scale_mode=case.scale_mode, rms_beta=case.rms_beta,
                               param_dtype=DT[case.param], state_dtype=DT[case.state],
                               ns_dtype=DT[case.ns], tile_policy=case.tile_policy,
-                              k_split=case.k_split, stream_hint=case.stream_hint, **extra)
+                              k_split=case.k_split, stream_hint=case.stream_hint,
+                              apply_mode=case.apply_mode, **extra)
     opt = mb.MuonBP(case.mats, case.period, case.lr_block, case.lr_full, case.momentum,
                     case.weight_decay, options=opts)
     orc = O.MuonBPOracle([O.MatrixSpec(*m) for m in case.mats],

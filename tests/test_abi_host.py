@@ -93,6 +93,7 @@ def test_create_rejects_bad_arguments_before_gpu(lib):
     assert _create(lib, [(8, 8, 1, 1)], opt=mb.options_default(tile_policy=14))[0] == 1
     assert _create(lib, [(8, 8, 1, 1)], opt=mb.options_default(stream_hint=3))[0] == 1
     assert _create(lib, [(8, 8, 1, 1)], opt=mb.options_default(stream_hint=-1))[0] == 1
+    assert _create(lib, [(8, 8, 1, 1)], opt=mb.options_default(apply_mode=2))[0] == 1
 
 
 def test_null_context_calls(lib):
@@ -221,3 +222,16 @@ def test_coefficient_table_plans_one_polynomial_per_entry(lib):
     tab = mb.describe_plan(mats, False, mb.options_default(coeffs=[(3.0, -3.2, 1.2)] * 3))
     assert list(base.gemm_tiles) == list(tab.gemm_tiles)
     assert base.gemm_launches == tab.gemm_launches and base.ns_flops == tab.ns_flops
+
+
+def test_apply_reads_z_row_major_where_the_dma_kernel_runs(lib):
+    """bf16 NS with the interleaved DMA kernel on the apply: no Z^T operand;
+    apply_mode 1, fp32 NS or a register-loop tile policy keep Z^T."""
+    mats = [(2048, 6144, 1, 8)]
+    for full in (0, 1):
+        assert mb.describe_plan(mats, full, mb.options_default()).apply_nn == 1
+        assert mb.describe_plan(mats, full, mb.options_default(apply_mode=1)).apply_nn == 0
+        assert mb.describe_plan(mats, full, mb.options_default(ns_dtype=0)).apply_nn == 0
+        assert mb.describe_plan(mats, full, mb.options_default(tile_policy=3)).apply_nn == 0
+        assert mb.describe_plan(mats, full, mb.options_default(tile_policy=6)).apply_nn == 0
+        assert mb.describe_plan(mats, full, mb.options_default(tile_policy=11)).apply_nn == 1

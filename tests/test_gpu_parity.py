@@ -128,6 +128,17 @@ def test_dma_pipeline_and_k_split(policy, ksplit):
     _check(res, BF16_TOL)
 
 
+@pytest.mark.parametrize("policy", [8, 9, 10, 11, 12, 13],
+                         ids=["dmap128x128", "dmap256x128", "dmap256x256", "dmap192x256",
+                              "dmap256x192", "dmap192x192"])
+def test_apply_with_transposed_copy(policy):
+    """apply_mode 1: the interleaved DMA kernels read Z^T for the apply (the
+    layout every other kernel uses) instead of Z through transpose reads."""
+    announce(f"apply NT policy {policy}")
+    res = run_case(Case(mats=ALIGNED, period=2, steps=3, tile_policy=policy, apply_mode=1))
+    _check(res, BF16_TOL)
+
+
 def test_k_split_deterministic():
     """Shares are added in a fixed order, whichever workgroup finishes last."""
     announce("k split determinism")
