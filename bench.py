@@ -480,6 +480,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--apply-mode", type=int, default=0,
                     help="library option apply_mode (0: apply reads Z row-major, 1: keeps Z^T)")
+    ap.add_argument("--k-split", type=int, default=0,
+                    help="library option k_split (0: planner's choice)")
     ap.add_argument("--copy-probe", type=int, metavar="MIB", default=None,
                     help="only run a plain copy of MIB MiB (counter calibration) and exit")
     ap.add_argument("--mfma-probe", action="store_true",
@@ -532,7 +534,8 @@ def main():
     log(f"workload {name}: {len(mats)} matrices, {n_el / 1e6:.1f} M params; generating inputs")
     params, grads, data = make_inputs(mats, rank)
     opt = mb.MuonBP(mats, period, lr_block, LR_FULL, MU, WD,
-                    options=mb.options_default(ns_steps=K_NS, apply_mode=args.apply_mode))
+                    options=mb.options_default(ns_steps=K_NS, apply_mode=args.apply_mode,
+                                               k_split=args.k_split))
     torch.cuda.synchronize()
 
     t = 0

@@ -15,12 +15,12 @@
 #include "../../include/muonbp.h"
 #include "kernels.h"
 #include "plan.h"
+#include "ptr_ring.h"
 
 using namespace muonbp;
 
 namespace {
 
-constexpr int kPtrRing = 8;  // staging slots for per-step pointer tables
 
 size_t dtype_size(muonbp_dtype d) { return d == MUONBP_F32 ? 4 : 2; }
 DType dt(muonbp_dtype d) { return d == MUONBP_F32 ? DType::F32 : DType::BF16; }
@@ -64,13 +64,7 @@ struct muonbp_ctx {
   PlanDev pd[2];
   std::vector<void*> allocs;
 
-  MatPtrs* ptr_dev[kPtrRing] = {};
-  MatPtrs* ptr_host[kPtrRing] = {};  // pinned
-  hipEvent_t ptr_ev[kPtrRing] = {};
-  bool ptr_ev_used[kPtrRing] = {};
-  int ptr_slot = -1;
-  std::vector<MatPtrs> last_ptrs;
-  bool ptrs_valid = false;
+  PtrRing ptrs;  // caller's param / grad pointers of the current step
 
   bool vec_layout = false;
   bool stream_nt = false;  // nontemporal momentum / update accesses
@@ -251,10 +245,7 @@ hipError_t build_plan_tables(muonbp_ctx* c, int full) {
 void free_ctx(muonbp_ctx* c) {
   if (!c) return;
   for (void* p : c->allocs) (void)hipFree(p);
-  for (int i = 0; i < kPtrRing; ++i) {
-    if (c->ptr_host[i]) (void)hipHostFree(c->ptr_host[i]);
-    if (c->ptr_ev[i]) (void)hipEventDestroy(c->ptr_ev[i]);
-  }
+  c->ptrs.release();
   for (auto& r : c->prof_recs) {
     (void)hipEventDestroy(r.start);
     if (r.stop) (void)hipEventDestroy(r.stop);
@@ -312,29 +303,6 @@ hipError_t span_mark(muonbp_ctx* c, bool begin, int launches) {
   } else {
     c->prof_recs.back().stop = ev;
   }
-  return hipSuccess;
-}
-
-// Make the device pointer table for this step current (uploads only when
-// the caller's pointers changed since the last step).
-hipError_t stage_pointers(muonbp_ctx* c, void* const* params, const void* const* grads) {
-  const size_t n = c->lay.mats.size();
-  bool same = c->ptrs_valid;
-  for (size_t i = 0; same && i < n; ++i)
-    same = c->last_ptrs[i].param == params[i] && c->last_ptrs[i].grad == grads[i];
-  if (same) return hipSuccess;
-  const int slot = (c->ptr_slot + 1) % kPtrRing;
-  hipError_t e;
-  if (c->ptr_ev_used[slot] && (e = hipEventSynchronize(c->ptr_ev[slot])) != hipSuccess) return e;
-  for (size_t i = 0; i < n; ++i) c->ptr_host[slot][i] = MatPtrs{params[i], grads[i]};
-  e = hipMemcpyAsync(c->ptr_dev[slot], c->ptr_host[slot], n * sizeof(MatPtrs), hipMemcpyHostToDevice,
-                     c->stream);
-  if (e != hipSuccess) return e;
-  if ((e = hipEventRecord(c->ptr_ev[slot], c->stream)) != hipSuccess) return e;
-  c->ptr_ev_used[slot] = true;
-  c->ptr_slot = slot;
-  c->last_ptrs.assign(c->ptr_host[slot], c->ptr_host[slot] + n);
-  c->ptrs_valid = true;
   return hipSuccess;
 }
 
@@ -523,15 +491,7 @@ muonbp_status muonbp_create(const muonbp_matrix* mats, int32_t n_mats, int64_t p
   if ((e = upload(c, &c->blocks, bd)) != hipSuccess) return bail(e, "blocks");
   for (int full = 0; full < 2; ++full)
     if ((e = build_plan_tables(c, full)) != hipSuccess) return bail(e, "plan tables");
-  for (int i = 0; i < kPtrRing; ++i) {
-    if ((e = dev_alloc(c, &p, shapes.size() * sizeof(MatPtrs))) != hipSuccess) return bail(e, "pointer table");
-    c->ptr_dev[i] = static_cast<MatPtrs*>(p);
-    void* h = nullptr;
-    if ((e = hipHostMalloc(&h, shapes.size() * sizeof(MatPtrs), 0)) != hipSuccess) return bail(e, "pinned table");
-    c->ptr_host[i] = static_cast<MatPtrs*>(h);
-    if ((e = hipEventCreateWithFlags(&c->ptr_ev[i], hipEventDisableTiming)) != hipSuccess)
-      return bail(e, "event");
-  }
+  if ((e = c->ptrs.init(shapes.size())) != hipSuccess) return bail(e, "pointer tables");
   // Algorithm 1: M_{-1} = 0.
   if ((e = hipMemset(c->mom, 0, size_t(c->lay.total_elems) * sb)) != hipSuccess) return bail(e, "memset");
   if ((e = hipDeviceSynchronize()) != hipSuccess) return bail(e, "sync");
@@ -554,9 +514,9 @@ muonbp_status muonbp_step(muonbp_ctx* c, void* const* params, const void* const*
     aligned = aligned && reinterpret_cast<uintptr_t>(params[i]) % 16 == 0 &&
               reinterpret_cast<uintptr_t>(grads[i]) % 16 == 0;
   }
-  hipError_t e = stage_pointers(c, params, grads);
+  hipError_t e = c->ptrs.stage(params, grads, c->stream);
   if (e != hipSuccess) return hip_fail(c, e, "pointer upload");
-  const MatPtrs* mats = c->ptr_dev[c->ptr_slot];
+  const MatPtrs* mats = c->ptrs.current();
 
   // Algorithm 1: full orthogonalization iff t mod P = 0 (P = 0 means infinity).
   const int full = (c->period > 0 && step % c->period == 0) ? 1 : 0;
@@ -627,7 +587,7 @@ muonbp_status muonbp_set_stream(muonbp_ctx* c, void* hip_stream) {
   hipError_t e = hipStreamSynchronize(c->stream);
   if (e != hipSuccess) return hip_fail(c, e, "hipStreamSynchronize");
   c->stream = static_cast<hipStream_t>(hip_stream);
-  c->ptrs_valid = false;
+  c->ptrs.invalidate();
   return MUONBP_OK;
 }
 
