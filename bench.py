@@ -450,6 +450,46 @@ def ingest_kernel_trace(workload, run_dir, command):
     print(path)
 
 
+# Tensors the paper trains with AdamW instead of MuonBP (1D parameters and
+# the input embedding, Appendix B), at the 8B-shaped model's sizes: the
+# embedding (vocabulary 128256 x d 4096; the paper does not state its
+# vocabulary) and 2 RMSNorm vectors per layer plus the final one.
+SCALAR_SIZES = [128256 * 4096] + [4096] * (2 * 32 + 1)
+SCALAR_WORKLOAD = "adamw-embedding-128256x4096-and-65x4096-norms-bf16"
+
+
+def scalar_optimizer_bench(steps=20, warmup=3):
+    """GB/s of the AdamW step (global-norm clipping on): algorithmic bytes per
+    element = gradient read for the norm (2) + params, grads, m, v read (12)
+    + params, m, v written (10), bf16 params with fp32 moments."""
+    import torch
+    from paper_2510_16981_amd import muonbp as mb
+    g = torch.Generator(device="cuda")
+    g.manual_seed(11)
+    params = [(0.02 * torch.randn(n, generator=g, device="cuda")).to(torch.bfloat16)
+              for n in SCALAR_SIZES]
+    grads = [(1e-3 * torch.randn(n, generator=g, device="cuda")).to(torch.bfloat16)
+             for n in SCALAR_SIZES]
+    opt = mb.AdamW(SCALAR_SIZES)
+    for t in range(warmup):
+        opt.step(params, grads, t, 1e-3)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for t in range(warmup, warmup + steps):
+        opt.step(params, grads, t, 1e-3)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    n = sum(SCALAR_SIZES)
+    bpe = 24
+    gbs = n * bpe / (ms * 1e-3) / 1e9
+    opt.close()
+    del params, grads
+    torch.cuda.empty_cache()
+    return {"workload": SCALAR_WORKLOAD, "elements": n, "ms_per_step": ms, "bytes_per_elem": bpe,
+            "gbs": gbs, "frac_hbm_peak": gbs / HBM_PEAK_GBS, "steps": steps,
+            "timing": "host timer around synchronized back-to-back steps (3 launches each)"}
+
+
 def make_inputs(mats, rank):
     """Params and grads, one tensor each per matrix.  Small workloads: the
     exact seeded host inputs.  Large ones: GPU-drawn timing-only inputs (the
@@ -478,6 +518,8 @@ def main():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--period", type=int, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-scalar", action="store_true",
+                    help="skip the AdamW measurement (scalar_optimizer)")
     ap.add_argument("--apply-mode", type=int, default=0,
                     help="library option apply_mode (0: apply reads Z row-major, 1: keeps Z^T)")
     ap.add_argument("--k-split", type=int, default=0,
@@ -672,6 +714,11 @@ def main():
         out["period_sweep_note"] = ("(t_full + (P - 1) t_block) / P from the measured block and "
                                     "full step times; P = 1 is Muon, inf is BlockMuon")
     opt.close()
+    del params, grads
+    torch.cuda.empty_cache()
+    if not args.no_scalar:
+        log("scalar optimizer (AdamW) pass")
+        out["scalar_optimizer"] = scalar_optimizer_bench()
     if not args.no_cpu_baseline and not large:
         log("cpu baseline (oracle)")
         out["cpu_baseline"] = cpu_baseline(name, mats, period, rank, 3 * max(period, 1))

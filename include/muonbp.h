@@ -224,6 +224,83 @@ const char* muonbp_last_error(const muonbp_ctx* ctx);
  * NULL is a no-op. */
 void muonbp_destroy(muonbp_ctx* ctx);
 
+/* ------------------------------------------------------------------------
+ * Scalar optimizer for the parameters MuonBP does not orthogonalize.
+ *
+ * The paper trains the 1D parameters and the input embedding with AdamW,
+ * with their gradients clipped to a global norm of 1.0 and weight decay 0.1
+ * (Appendix B, experimental details).  One context covers a fixed list of
+ * tensors (any shape, seen as flat arrays of `sizes[i]` elements):
+ *   g <- g * min(1, max_grad_norm / (||g||_2 + 1e-6))   (||g|| over all tensors)
+ *   m <- beta1 m + (1 - beta1) g,   v <- beta2 v + (1 - beta2) g^2
+ *   p <- p (1 - lr wd) - lr (m / (1 - beta1^t)) / (sqrt(v / (1 - beta2^t)) + eps)
+ * with t = step + 1.  The moments are fp32 and owned by the context.
+ * The conventions of the MuonBP functions above apply (status codes,
+ * asynchrony on the context's stream, pointer alignment, thread safety).
+ * ---------------------------------------------------------------------- */
+typedef struct muonbp_adamw_ctx muonbp_adamw_ctx; /* opaque */
+
+typedef struct {
+  float beta1, beta2;       /* 0 <= beta < 1                                   */
+  float eps;                /* >= 0                                            */
+  float weight_decay;       /* decoupled, scaled by lr                         */
+  float max_grad_norm;      /* > 0: global-norm clipping; 0: off               */
+  muonbp_dtype param_dtype; /* dtype of params and grads                       */
+  int32_t stream_hint;      /* cache policy of the streamed accesses, as
+                               muonbp_options.stream_hint (0 = by size)        */
+} muonbp_adamw_options;
+
+/* Defaults: beta1 0.9, beta2 0.95, eps 1e-8, weight decay 0.1, clipping at
+ * 1.0, bf16 params.  NULL is ignored. */
+void muonbp_adamw_options_default(muonbp_adamw_options* opt);
+
+/* Create a context for n tensors of sizes[i] > 0 elements (host array,
+ * copied).  Allocates the zeroed moments (m_0 = v_0 = 0) on the current
+ * device.  Errors: E_INVALID (NULL, n <= 0, bad option), E_SHAPE (a size
+ * <= 0), E_DTYPE, E_NOMEM, E_HIP. */
+muonbp_status muonbp_adamw_create(const int64_t* sizes, int32_t n,
+                                  const muonbp_adamw_options* opt, void* hip_stream,
+                                  muonbp_adamw_ctx** out);
+
+/* One AdamW step (t = step + 1 >= 1) with learning rate lr (finite).
+ *  params  host array of n device pointers (param_dtype), updated in place.
+ *  grads   host array of n device pointers (param_dtype), read only.
+ * Enqueues: with clipping, a sum of squares per segment and one reduction
+ * to the clipping factor; then one fused update of params, m and v. */
+muonbp_status muonbp_adamw_step(muonbp_adamw_ctx* ctx, void* const* params,
+                                const void* const* grads, int64_t step, float lr);
+
+/* Global gradient norm (before clipping) of the last step, to host memory;
+ * synchronises the stream.  E_STATE if no step with clipping has run. */
+muonbp_status muonbp_adamw_grad_norm(muonbp_adamw_ctx* ctx, float* out);
+
+/* Copy tensor i's moments (fp32, sizes[i] elements) to / from device memory
+ * (checkpoint and resume).  Asynchronous on the stream; NULL skips one. */
+muonbp_status muonbp_adamw_get_state(muonbp_adamw_ctx* ctx, int32_t i, void* m_dst, void* v_dst);
+muonbp_status muonbp_adamw_set_state(muonbp_adamw_ctx* ctx, int32_t i, const void* m_src,
+                                     const void* v_src);
+
+muonbp_status muonbp_adamw_set_stream(muonbp_adamw_ctx* ctx, void* hip_stream);
+muonbp_status muonbp_adamw_synchronize(muonbp_adamw_ctx* ctx);
+const char* muonbp_adamw_last_error(const muonbp_adamw_ctx* ctx);
+void muonbp_adamw_destroy(muonbp_adamw_ctx* ctx); /* NULL is a no-op */
+
+/* ------------------------------------------------------------------------
+ * Learning-rate schedules of the paper's runs (Appendix B): cosine decay
+ * (960M and 1.2B models) and warmup-stable-decay with a linear decay to a
+ * final value (8B model; no warmup and a 20% cooldown for the 160M model).
+ * Host-only, pure functions of the step t >= 0:
+ *   both:   t < warmup: lr_max (t + 1) / warmup
+ *   cosine: lr_min + (lr_max - lr_min) (1 + cos(pi x)) / 2,
+ *           x = min(1, (t - warmup) / max(1, total - warmup))
+ *   wsd:    lr_max until total - decay, then linear to lr_min at t = total
+ *           (decay = 0: no decay); lr_min from t = total on.
+ * Feed the result to muonbp_set_lr / muonbp_adamw_step.
+ * ---------------------------------------------------------------------- */
+double muonbp_lr_cosine(int64_t t, int64_t total, double lr_max, double lr_min, int64_t warmup);
+double muonbp_lr_wsd(int64_t t, int64_t total, double lr_max, double lr_min, int64_t warmup,
+                     int64_t decay);
+
 #ifdef __cplusplus
 }
 #endif

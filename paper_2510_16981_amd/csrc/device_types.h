@@ -104,4 +104,21 @@ struct UpdDesc {
   int32_t pad;
 };
 
+// Scalar optimizer (AdamW): one workgroup's contiguous element range of one
+// tensor, and where that range's moments sit in the state arenas.
+struct ScalarSeg {
+  int32_t tensor;  // index into the pointer table
+  int32_t count;   // elements
+  int64_t begin;   // first element inside the tensor
+  int64_t state;   // arena offset of element `begin`
+};
+
+// Per-step scalars of the AdamW kernel (computed on the host in double).
+struct AdamwArgs {
+  float beta1, beta2, eps;
+  float decay;         // 1 - lr * weight_decay
+  float step;          // lr / (1 - beta1^t)
+  float inv_sqrt_bc2;  // 1 / sqrt(1 - beta2^t)
+};
+
 }  // namespace muonbp

@@ -47,4 +47,19 @@ hipError_t launch_update(DType param_t, DType ns_t, bool vec, bool nt, int n_seg
                          const MatPtrs* mats, const UpdDesc* upd, float eta,
                          float lambda, hipStream_t s);
 
+// Scalar optimizer (AdamW with global-norm clipping) over segments of the
+// tensors MuonBP does not orthogonalize.
+// partials[seg] = sum of squares of that segment's gradients.
+hipError_t launch_adamw_sumsq(DType param_t, bool vec, int n_segs, const ScalarSeg* segs,
+                              const MatPtrs* ptrs, float* partials, hipStream_t s);
+// clip[0] = min(1, max_norm / (||g|| + 1e-6)) (1 when max_norm <= 0),
+// clip[1] = ||g||, from the n partial sums.
+hipError_t launch_adamw_clip(const float* partials, int n, float max_norm, float* clip,
+                             hipStream_t s);
+// The AdamW update of params and of the fp32 moments m and v; gradients are
+// scaled by clip[0] when clip is not NULL.
+hipError_t launch_adamw(DType param_t, bool vec, bool nt, int n_segs, const ScalarSeg* segs,
+                        const MatPtrs* ptrs, float* m, float* v, const float* clip,
+                        const AdamwArgs& a, hipStream_t s);
+
 }  // namespace muonbp

@@ -1222,6 +1222,117 @@ __global__ __launch_bounds__(kThreads) void k_update(
   }
 }
 
+// ---------------------------------------------------------------- AdamW
+//
+// The parameters MuonBP does not orthogonalize (1D parameters and the input
+// embedding in the paper's training setup, Appendix B) take AdamW steps with
+// global-norm gradient clipping.  One workgroup per segment (a contiguous
+// element range of one tensor); VEC: the tensor pointers are 16-byte aligned
+// and every segment starts at a multiple of 8 elements, so full 8-element
+// chunks are 16-byte accesses (the segment's last partial chunk goes one
+// element at a time).
+
+template <typename TP, bool VEC>
+__global__ __launch_bounds__(kThreads) void k_adamw_sumsq(const ScalarSeg* __restrict__ segs,
+                                                          const MatPtrs* __restrict__ ptrs,
+                                                          float* __restrict__ partials) {
+  const ScalarSeg sg = segs[blockIdx.x];
+  const TP* g = static_cast<const TP*>(ptrs[sg.tensor].grad) + sg.begin;
+  const int n = sg.count, nv = VEC ? n >> 3 : 0;
+  float acc = 0.f;
+  for (int c = threadIdx.x; c < nv; c += kThreads) {
+    float f[8];
+    load8(g + 8 * c, f);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc = fmaf(f[i], f[i], acc);
+  }
+  for (int e = 8 * nv + threadIdx.x; e < n; e += kThreads) {
+    const float x = to_f<TP>(g[e]);
+    acc = fmaf(x, x, acc);
+  }
+  acc = block_sum(acc);
+  if (threadIdx.x == 0) partials[blockIdx.x] = acc;
+}
+
+// One workgroup: the global norm from the partial sums (in double, fixed
+// order) and the clipping factor.
+__global__ __launch_bounds__(kThreads) void k_adamw_clip(const float* __restrict__ partials, int n,
+                                                         float max_norm, float* __restrict__ clip) {
+  __shared__ double red[kThreads / 64];
+  double acc = 0.0;
+  for (int i = threadIdx.x; i < n; i += kThreads) acc += partials[i];
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) acc += __shfl_xor(acc, o);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = acc;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    double total = 0.0;
+    for (int w = 0; w < kThreads / 64; ++w) total += red[w];
+    const double norm = sqrt(total);
+    clip[0] = max_norm > 0.f ? float(fmin(1.0, double(max_norm) / (norm + 1e-6))) : 1.f;
+    clip[1] = float(norm);
+  }
+}
+
+// p <- p (1 - lr wd) - lr m_hat / (sqrt(v_hat) + eps) with the moments of
+// the clipped gradient (Adam's bias-corrected moments, decoupled decay).
+__device__ __forceinline__ void adamw_elem(float& p, float g, float& m, float& v, const AdamwArgs& a) {
+  m = fmaf(a.beta1, m, (1.f - a.beta1) * g);
+  v = fmaf(a.beta2, v, (1.f - a.beta2) * g * g);
+  p = fmaf(p, a.decay, -a.step * (m / fmaf(sqrtf(v), a.inv_sqrt_bc2, a.eps)));
+}
+
+template <typename TP, bool VEC, bool NT>
+__global__ __launch_bounds__(kThreads) void k_adamw(const ScalarSeg* __restrict__ segs,
+                                                    const MatPtrs* __restrict__ ptrs,
+                                                    float* __restrict__ m, float* __restrict__ v,
+                                                    const float* __restrict__ clip, AdamwArgs a) {
+  const ScalarSeg sg = segs[blockIdx.x];
+  TP* p = static_cast<TP*>(ptrs[sg.tensor].param) + sg.begin;
+  const TP* g = static_cast<const TP*>(ptrs[sg.tensor].grad) + sg.begin;
+  float* ms = m + sg.state;
+  float* vs = v + sg.state;
+  const float c = clip ? clip[0] : 1.f;
+  const int n = sg.count, nv = VEC ? n >> 3 : 0;
+  for (int c0 = threadIdx.x; c0 < nv; c0 += kThreads * 2) {
+    Raw8<TP> pr[2], gr[2];
+    Raw8<float> mr[2], vr[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int k = c0 + kThreads * u;
+      if (k < nv) {
+        pr[u] = load8r<NT>(p + 8 * k);
+        gr[u] = load8r<NT>(g + 8 * k);
+        mr[u] = load8r<NT>(ms + 8 * k);
+        vr[u] = load8r<NT>(vs + 8 * k);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int k = c0 + kThreads * u;
+      if (k < nv) {
+        float pf[8], gf[8], mf[8], vf[8];
+        unpack8(pr[u], pf);
+        unpack8(gr[u], gf);
+        unpack8(mr[u], mf);
+        unpack8(vr[u], vf);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) adamw_elem(pf[i], c * gf[i], mf[i], vf[i], a);
+        store8r<NT>(p + 8 * k, pf);
+        store8r<NT>(ms + 8 * k, mf);
+        store8r<NT>(vs + 8 * k, vf);
+      }
+    }
+  }
+  for (int e = 8 * nv + threadIdx.x; e < n; e += kThreads) {
+    float pf = to_f<TP>(p[e]), mf = ms[e], vf = vs[e];
+    adamw_elem(pf, c * to_f<TP>(g[e]), mf, vf, a);
+    p[e] = from_f<TP>(pf);
+    ms[e] = mf;
+    vs[e] = vf;
+  }
+}
+
 // ---------------------------------------------------------------- launchers
 
 namespace {
@@ -1381,6 +1492,46 @@ hipError_t launch_update(DType param_t, DType ns_t, bool vec, bool nt, int n_seg
                            segs, blocks, mats, upd, eta, lambda);
       return hipGetLastError();
     });
+  });
+}
+
+hipError_t launch_adamw_sumsq(DType param_t, bool vec, int n_segs, const ScalarSeg* segs,
+                              const MatPtrs* ptrs, float* partials, hipStream_t s) {
+  if (n_segs <= 0) return hipSuccess;
+  return dispatch1(param_t, [&](auto p) {
+    using TP = decltype(p);
+    if (vec)
+      hipLaunchKernelGGL((k_adamw_sumsq<TP, true>), dim3(n_segs), dim3(kThreads), 0, s, segs, ptrs,
+                         partials);
+    else
+      hipLaunchKernelGGL((k_adamw_sumsq<TP, false>), dim3(n_segs), dim3(kThreads), 0, s, segs, ptrs,
+                         partials);
+    return hipGetLastError();
+  });
+}
+
+hipError_t launch_adamw_clip(const float* partials, int n, float max_norm, float* clip,
+                             hipStream_t s) {
+  hipLaunchKernelGGL(k_adamw_clip, dim3(1), dim3(kThreads), 0, s, partials, n, max_norm, clip);
+  return hipGetLastError();
+}
+
+hipError_t launch_adamw(DType param_t, bool vec, bool nt, int n_segs, const ScalarSeg* segs,
+                        const MatPtrs* ptrs, float* m, float* v, const float* clip,
+                        const AdamwArgs& a, hipStream_t s) {
+  if (n_segs <= 0) return hipSuccess;
+  return dispatch1(param_t, [&](auto p) {
+    using TP = decltype(p);
+    if (vec && nt)
+      hipLaunchKernelGGL((k_adamw<TP, true, true>), dim3(n_segs), dim3(kThreads), 0, s, segs, ptrs,
+                         m, v, clip, a);
+    else if (vec)
+      hipLaunchKernelGGL((k_adamw<TP, true, false>), dim3(n_segs), dim3(kThreads), 0, s, segs, ptrs,
+                         m, v, clip, a);
+    else
+      hipLaunchKernelGGL((k_adamw<TP, false, false>), dim3(n_segs), dim3(kThreads), 0, s, segs,
+                         ptrs, m, v, clip, a);
+    return hipGetLastError();
   });
 }
 

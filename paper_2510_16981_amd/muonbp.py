@@ -57,6 +57,12 @@ class PlanInfo(ctypes.Structure):
                 ("gemm_split", ctypes.c_int32 * 3), ("apply_nn", ctypes.c_int32)]
 
 
+class AdamwOptions(ctypes.Structure):
+    _fields_ = [("beta1", ctypes.c_float), ("beta2", ctypes.c_float), ("eps", ctypes.c_float),
+                ("weight_decay", ctypes.c_float), ("max_grad_norm", ctypes.c_float),
+                ("param_dtype", ctypes.c_int), ("stream_hint", ctypes.c_int32)]
+
+
 class Profile(ctypes.Structure):
     _fields_ = [("ms", ctypes.c_double * 8), ("launches", ctypes.c_int64 * 8),
                 ("ms_full_steps", ctypes.c_double * 8),
@@ -96,6 +102,19 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "muonbp_status_string": (ctypes.c_char_p, [ctypes.c_int]),
         "muonbp_last_error": (ctypes.c_char_p, [P]),
         "muonbp_destroy": (None, [P]),
+        "muonbp_adamw_options_default": (None, [ctypes.POINTER(AdamwOptions)]),
+        "muonbp_adamw_create": (ctypes.c_int, [ctypes.POINTER(I64), I32, ctypes.POINTER(AdamwOptions),
+                                               P, ctypes.POINTER(P)]),
+        "muonbp_adamw_step": (ctypes.c_int, [P, ctypes.POINTER(P), ctypes.POINTER(P), I64, F]),
+        "muonbp_adamw_grad_norm": (ctypes.c_int, [P, ctypes.POINTER(F)]),
+        "muonbp_adamw_get_state": (ctypes.c_int, [P, I32, P, P]),
+        "muonbp_adamw_set_state": (ctypes.c_int, [P, I32, P, P]),
+        "muonbp_adamw_set_stream": (ctypes.c_int, [P, P]),
+        "muonbp_adamw_synchronize": (ctypes.c_int, [P]),
+        "muonbp_adamw_last_error": (ctypes.c_char_p, [P]),
+        "muonbp_adamw_destroy": (None, [P]),
+        "muonbp_lr_cosine": (ctypes.c_double, [I64, I64, ctypes.c_double, ctypes.c_double, I64]),
+        "muonbp_lr_wsd": (ctypes.c_double, [I64, I64, ctypes.c_double, ctypes.c_double, I64, I64]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -275,3 +294,109 @@ class MuonBP:
             self.close()
         except Exception:
             pass
+
+
+# ---------------------------------------------------------------- scalar optimizer
+
+def adamw_options_default(**overrides) -> AdamwOptions:
+    """Library defaults (beta1 0.9, beta2 0.95, eps 1e-8, weight decay 0.1,
+    clipping at 1.0, bf16) with fields overridden by keyword."""
+    o = AdamwOptions()
+    load_library().muonbp_adamw_options_default(ctypes.byref(o))
+    for k, v in overrides.items():
+        if not hasattr(o, k):
+            raise AttributeError(k)
+        setattr(o, k, v)
+    return o
+
+
+class AdamW:
+    """AdamW with global-norm clipping over a fixed list of tensors (the
+    parameters MuonBP does not orthogonalize)."""
+
+    def __init__(self, sizes: Sequence[int], options: Optional[AdamwOptions] = None, stream=None):
+        import torch
+        self.lib = load_library()
+        self.sizes = [int(n) for n in sizes]
+        self.options = options if options is not None else adamw_options_default()
+        if stream is None:
+            stream = torch.cuda.current_stream()
+        arr = (ctypes.c_int64 * len(self.sizes))(*self.sizes)
+        ctx = ctypes.c_void_p()
+        st = self.lib.muonbp_adamw_create(arr, len(self.sizes), ctypes.byref(self.options),
+                                          ctypes.c_void_p(stream.cuda_stream), ctypes.byref(ctx))
+        if st:
+            raise MuonBPError(st, "muonbp_adamw_create")
+        self.ctx = ctx
+        self._ptrs = (ctypes.c_void_p * len(self.sizes))()
+        self._gptrs = (ctypes.c_void_p * len(self.sizes))()
+
+    def _check(self, st: int, what: str):
+        if st:
+            detail = self.lib.muonbp_adamw_last_error(self.ctx)
+            raise MuonBPError(st, f"{what}: {detail.decode() if detail else ''}")
+
+    def _check_tensor(self, t, i, dtype):
+        if not (t.is_cuda and t.is_contiguous() and t.dtype == dtype and t.numel() == self.sizes[i]):
+            raise ValueError(f"tensor {i}: need a contiguous {dtype} CUDA tensor of "
+                             f"{self.sizes[i]} elements, got {t.dtype} {tuple(t.shape)}")
+
+    def step(self, params: List, grads: List, t: int, lr: float) -> None:
+        import torch
+        n = len(self.sizes)
+        if len(params) != n or len(grads) != n:
+            raise ValueError("one param and one grad per tensor")
+        dt = _torch_dtype(self.options.param_dtype)
+        for i in range(n):
+            self._check_tensor(params[i], i, dt)
+            self._check_tensor(grads[i], i, dt)
+            self._ptrs[i] = params[i].data_ptr()
+            self._gptrs[i] = grads[i].data_ptr()
+        self._check(self.lib.muonbp_adamw_step(self.ctx, self._ptrs, self._gptrs, int(t), float(lr)),
+                    "adamw_step")
+
+    def grad_norm(self) -> float:
+        out = ctypes.c_float()
+        self._check(self.lib.muonbp_adamw_grad_norm(self.ctx, ctypes.byref(out)), "grad_norm")
+        return float(out.value)
+
+    def get_state(self, i: int):
+        import torch
+        m = torch.empty(self.sizes[i], dtype=torch.float32, device="cuda")
+        v = torch.empty_like(m)
+        self._check(self.lib.muonbp_adamw_get_state(self.ctx, i, ctypes.c_void_p(m.data_ptr()),
+                                                    ctypes.c_void_p(v.data_ptr())), "get_state")
+        return m, v
+
+    def set_state(self, i: int, m, v) -> None:
+        import torch
+        for t in (m, v):
+            self._check_tensor(t, i, torch.float32)
+        self._check(self.lib.muonbp_adamw_set_state(self.ctx, i, ctypes.c_void_p(m.data_ptr()),
+                                                    ctypes.c_void_p(v.data_ptr())), "set_state")
+
+    def synchronize(self) -> None:
+        self._check(self.lib.muonbp_adamw_synchronize(self.ctx), "synchronize")
+
+    def close(self) -> None:
+        if getattr(self, "ctx", None):
+            self.lib.muonbp_adamw_destroy(self.ctx)
+            self.ctx = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def lr_cosine(t: int, total: int, lr_max: float, lr_min: float = 0.0, warmup: int = 0) -> float:
+    """Cosine schedule of the library (muonbp_lr_cosine)."""
+    return load_library().muonbp_lr_cosine(int(t), int(total), float(lr_max), float(lr_min), int(warmup))
+
+
+def lr_wsd(t: int, total: int, lr_max: float, lr_min: float = 0.0, warmup: int = 0,
+           decay: int = 0) -> float:
+    """Warmup-stable-decay schedule of the library (muonbp_lr_wsd)."""
+    return load_library().muonbp_lr_wsd(int(t), int(total), float(lr_max), float(lr_min), int(warmup),
+                                        int(decay))

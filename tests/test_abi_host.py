@@ -235,3 +235,47 @@ def test_apply_reads_z_row_major_where_the_dma_kernel_runs(lib):
         assert mb.describe_plan(mats, full, mb.options_default(tile_policy=3)).apply_nn == 0
         assert mb.describe_plan(mats, full, mb.options_default(tile_policy=6)).apply_nn == 0
         assert mb.describe_plan(mats, full, mb.options_default(tile_policy=11)).apply_nn == 1
+
+
+def test_schedules_match_the_oracle(lib):
+    from oracle import scalar_oracle as S
+    T = 1000
+    for t in list(range(0, 40)) + list(range(480, 520)) + list(range(780, 1010)):
+        for warm in (0, 10):
+            assert mb.lr_cosine(t, T, 3e-3, 3e-5, warm) == pytest.approx(
+                S.lr_cosine(t, T, 3e-3, 3e-5, warm), rel=1e-14, abs=1e-18)
+            for decay in (0, 200):
+                assert mb.lr_wsd(t, T, 2e-2, 4.2e-5, warm, decay) == pytest.approx(
+                    S.lr_wsd(t, T, 2e-2, 4.2e-5, warm, decay), rel=1e-14, abs=1e-18)
+
+
+def test_adamw_options_default(lib):
+    o = mb.adamw_options_default()
+    assert (o.beta1, o.beta2) == pytest.approx((0.9, 0.95))
+    assert o.eps == pytest.approx(1e-8) and o.weight_decay == pytest.approx(0.1)
+    assert o.max_grad_norm == 1.0 and o.param_dtype == mb.BF16 and o.stream_hint == 0
+
+
+def test_adamw_create_rejects_bad_arguments_before_gpu(lib):
+    def create(sizes, **kw):
+        arr = (ctypes.c_int64 * max(1, len(sizes)))(*sizes)
+        ctx = ctypes.c_void_p()
+        o = mb.adamw_options_default(**kw)
+        st = lib.muonbp_adamw_create(arr, len(sizes), ctypes.byref(o), None, ctypes.byref(ctx))
+        return st, ctx
+
+    assert create([])[0] == 1
+    assert create([10, 0])[0] == 2
+    assert create([10, -3])[0] == 2
+    assert create([10], beta1=1.0)[0] == 1
+    assert create([10], beta2=-0.1)[0] == 1
+    assert create([10], eps=-1.0)[0] == 1
+    assert create([10], max_grad_norm=-1.0)[0] == 1
+    assert create([10], weight_decay=float("nan"))[0] == 1
+    assert create([10], stream_hint=3)[0] == 1
+    assert create([10], param_dtype=7)[0] == 3
+    assert lib.muonbp_adamw_create(None, 1, None, None, ctypes.byref(ctypes.c_void_p())) == 1
+    assert lib.muonbp_adamw_step(None, None, None, 0, 0.1) == 1
+    assert lib.muonbp_adamw_grad_norm(None, None) == 1
+    assert lib.muonbp_adamw_synchronize(None) == 1
+    lib.muonbp_adamw_destroy(None)
