@@ -228,7 +228,7 @@ def _kernel_label(name):
     import re
     if "muonbp" not in name:
         return None
-    m = re.search(r"(k_[a-z_]+)(<\d+, ?\d+>)?", name)
+    m = re.search(r"(k_[a-z_]+)(<[^<>()]*>)?", name)
     return (m.group(1) + (m.group(2) or "").replace(" ", "")) if m else None
 
 
@@ -264,9 +264,9 @@ INGEST_DIRS = ("copy_fetch", "copy_write", "mfma_probe", "block_fetch", "block_w
                "block_mfma", "full_fetch", "full_write", "full_mfma")
 MFMA_COUNTERS = ("SQ_INSTS_VALU_MFMA_MOPS_BF16", "MfmaUtil", "GRBM_GUI_ACTIVE")
 # Bytes per element the elementwise kernels must move (bf16 storage):
-# momentum reads M and G and writes M; pack reads M and writes Z and Z^T;
-# update reads X and U and writes X.
-ELEMENTWISE_BYTES = {"k_momentum": 6, "k_pack": 6, "k_update": 6}
+# momentum reads M and G and writes M; pack reads M and writes Z (the apply
+# reads Z row-major, so no Z^T); update reads X and U and writes X.
+ELEMENTWISE_BYTES = {"k_momentum": 6, "k_pack": 4, "k_update": 6}
 
 
 def ingest_counters(workload, dirs, command):
@@ -322,7 +322,8 @@ def ingest_counters(workload, dirs, command):
             byt = (f["value"] * sf + w["value"] * sw) * 1024.0 if f and w else None
             us = f["us"] if f else mops[lab]["us"]
             flops = mops[lab]["value"] * mops_unit if lab in mops else None
-            alg = (n_el * ELEMENTWISE_BYTES[lab]) if lab in ELEMENTWISE_BYTES else None
+            base = lab.split("<")[0]
+            alg = (n_el * ELEMENTWISE_BYTES[base]) if base in ELEMENTWISE_BYTES else None
             rows.append({
                 "kernel": lab, "dispatches": f["n"] if f else mops[lab]["n"], "us": us,
                 "hbm_bytes": byt, "hbm_gbs": byt / (us * 1e3) if byt else None,
@@ -490,6 +491,63 @@ def scalar_optimizer_bench(steps=20, warmup=3):
             "timing": "host timer around synchronized back-to-back steps (3 launches each)"}
 
 
+def ingest_workloads(paths, out_path):
+    """Write the larger-workload summary (profiles/steps_larger_workloads.md)
+    from bench.py JSON lines, one file per workload run."""
+    from paper_2510_16981_amd import workload as W
+    kinds = ("momentum", "scale", "pack", "gram", "poly", "apply", "update")
+    lines = ["# Step and kernel times: larger workloads (one MI355X)", "",
+             "Command for each row (from the repository root), then this summary:", "", "```",
+             "python3 bench.py --workload <name> > <name>.json",
+             "python3 bench.py --ingest-workloads <name>.json ...", "```", "",
+             "`ns TFLOP/s` comes from HIP events around each step's back-to-back NS GEMM launches "
+             "in the timed region;", "per-kernel times from the detail pass (events around every "
+             "launch); step times from host timers around", "synchronized runs of one step kind.  "
+             "Inputs are GPU-drawn timing-only gradients, one per matrix (bench.py make_inputs).",
+             ""]
+    for path in paths:
+        d = None
+        for line in open(path):
+            if line.startswith("{"):
+                d = json.loads(line)
+        cfg = d["config"]
+        name = cfg["workload"]
+        mats = W.workload_matrices(name)
+        lines += [f"## {name} ({cfg['matrices']} matrices, {cfg['params'] / 1e9:.3f} B params, "
+                  f"grids {', '.join(cfg['grids'])})", "",
+                  f"Timed schedule P = {cfg['period']}: {d['value']:.3f} steps/s, "
+                  f"{d['ms_per_step']:.2f} ms/step; NS GEMM {d['roofline']['achieved']:.0f} TFLOP/s "
+                  f"= {100 * d['roofline']['frac']:.1f}% of {BF16_PEAK_TFLOPS:.0f}.", "",
+                  "| Step | ms/step | NS TFLOP/s | % bf16 peak | tiles (Gram, poly, apply) | "
+                  + " | ".join(f"{k} ms" for k in kinds) + " |",
+                  "|---|---:|---:|---:|---|" + "---:|" * len(kinds)]
+        for kind in ("block", "full"):
+            b = d.get(kind)
+            if not b:
+                continue
+            det = b["detail_kernel_ms_per_step"]
+            lines.append(f"| {kind} | {b['ms_per_step']:.2f} | {b['ns_tflops']:.1f} | "
+                         f"{100 * b['ns_frac_bf16_peak']:.1f} | {' '.join(b['gemm_tiles'])} | "
+                         + " | ".join(f"{det.get(k, 0.0):.3f}" for k in kinds) + " |")
+        ew = d["elementwise"]
+        parts = [f"{k} {v['gbs']:.0f} GB/s ({100 * v['frac_hbm_peak']:.0f}% of 8 TB/s)"
+                 for k, v in ew.items() if "gbs" in v]
+        lines += ["", f"Elementwise (6 B/element each): {', '.join(parts)}; footprint "
+                  f"{ew['momentum'].get('note', '')}.".replace("footprint footprint", "footprint"), ""]
+        sw = d.get("period_sweep_ms_per_step")
+        if sw:
+            lines += ["Period sweep, ms/step ((t_full + (P-1) t_block) / P): "
+                      + ", ".join(f"P={k}: {v:.1f}" for k, v in sw.items()), ""]
+        sc = d.get("scalar_optimizer")
+        if sc:
+            lines += [f"AdamW pass ({sc['workload']}): {sc['ms_per_step']:.3f} ms/step, "
+                      f"{sc['gbs']:.0f} GB/s ({100 * sc['frac_hbm_peak']:.0f}% of 8 TB/s).", ""]
+        del mats
+    with open(out_path, "w") as fh:
+        fh.write("\n".join(lines))
+    print(out_path)
+
+
 def make_inputs(mats, rank):
     """Params and grads, one tensor each per matrix.  Small workloads: the
     exact seeded host inputs.  Large ones: GPU-drawn timing-only inputs (the
@@ -536,10 +594,16 @@ def main():
     ap.add_argument("--ingest-kernel-trace", metavar="DIR", default=None,
                     help="write the kernel summary of --workload from a rocprofv3 --kernel-trace "
                          "--stats csv run of bench.py whose JSON line is DIR/bench.json (no GPU use)")
+    ap.add_argument("--ingest-workloads", nargs="+", metavar="JSON", default=None,
+                    help="write profiles/steps_larger_workloads.md from bench.py JSON outputs "
+                         "(no GPU use)")
     ap.add_argument("--command", default="", help="with --ingest-*: the commands that made the runs")
     args = ap.parse_args()
     if args.ingest_counters:
         ingest_counters(args.workload, args.ingest_counters, args.command)
+        return
+    if args.ingest_workloads:
+        ingest_workloads(args.ingest_workloads, os.path.join(PROFILES, "steps_larger_workloads.md"))
         return
     if args.ingest_kernel_trace:
         ingest_kernel_trace(args.workload, args.ingest_kernel_trace, args.command)

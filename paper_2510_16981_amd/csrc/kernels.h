@@ -49,11 +49,15 @@ hipError_t launch_update(DType param_t, DType ns_t, bool vec, bool nt, int n_seg
 
 // Scalar optimizer (AdamW with global-norm clipping) over segments of the
 // tensors MuonBP does not orthogonalize.
-// partials[seg] = sum of squares of that segment's gradients.
-hipError_t launch_adamw_sumsq(DType param_t, bool vec, int n_segs, const ScalarSeg* segs,
+// Workgroups of the gradient-norm pass (and partial sums it writes).
+constexpr int kAdamwNormBlocks = 1024;
+int adamw_norm_blocks(int n_segs);
+// partials[b] (b < adamw_norm_blocks(n_segs)) = sum of squares of the
+// gradients of segments b, b + nb, ...
+hipError_t launch_adamw_sumsq(DType param_t, bool vec, bool nt, int n_segs, const ScalarSeg* segs,
                               const MatPtrs* ptrs, float* partials, hipStream_t s);
 // clip[0] = min(1, max_norm / (||g|| + 1e-6)) (1 when max_norm <= 0),
-// clip[1] = ||g||, from the n partial sums.
+// clip[1] = ||g||, from the n partial sums of the norm pass.
 hipError_t launch_adamw_clip(const float* partials, int n, float max_norm, float* clip,
                              hipStream_t s);
 // The AdamW update of params and of the fp32 moments m and v; gradients are

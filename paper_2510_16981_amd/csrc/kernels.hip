@@ -1232,23 +1232,36 @@ __global__ __launch_bounds__(kThreads) void k_update(
 // chunks are 16-byte accesses (the segment's last partial chunk goes one
 // element at a time).
 
-template <typename TP, bool VEC>
+// Workgroup b sums the squares of segments b, b + gridDim.x, ... (a fixed
+// assignment, so the result does not depend on scheduling); partials[b].
+template <typename TP, bool VEC, bool NT>
 __global__ __launch_bounds__(kThreads) void k_adamw_sumsq(const ScalarSeg* __restrict__ segs,
+                                                          int n_segs,
                                                           const MatPtrs* __restrict__ ptrs,
                                                           float* __restrict__ partials) {
-  const ScalarSeg sg = segs[blockIdx.x];
-  const TP* g = static_cast<const TP*>(ptrs[sg.tensor].grad) + sg.begin;
-  const int n = sg.count, nv = VEC ? n >> 3 : 0;
   float acc = 0.f;
-  for (int c = threadIdx.x; c < nv; c += kThreads) {
-    float f[8];
-    load8(g + 8 * c, f);
+  for (int si = blockIdx.x; si < n_segs; si += gridDim.x) {
+    const ScalarSeg sg = segs[si];
+    const TP* g = static_cast<const TP*>(ptrs[sg.tensor].grad) + sg.begin;
+    const int n = sg.count, nv = VEC ? n >> 3 : 0;
+    for (int c0 = threadIdx.x; c0 < nv; c0 += kThreads * kStreamUnroll) {
+      Raw8<TP> gr[kStreamUnroll];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) acc = fmaf(f[i], f[i], acc);
-  }
-  for (int e = 8 * nv + threadIdx.x; e < n; e += kThreads) {
-    const float x = to_f<TP>(g[e]);
-    acc = fmaf(x, x, acc);
+      for (int u = 0; u < kStreamUnroll; ++u)
+        if (c0 + kThreads * u < nv) gr[u] = load8r<NT>(g + 8 * (c0 + kThreads * u));
+#pragma unroll
+      for (int u = 0; u < kStreamUnroll; ++u)
+        if (c0 + kThreads * u < nv) {
+          float f[8];
+          unpack8(gr[u], f);
+#pragma unroll
+          for (int i = 0; i < 8; ++i) acc = fmaf(f[i], f[i], acc);
+        }
+    }
+    for (int e = 8 * nv + threadIdx.x; e < n; e += kThreads) {
+      const float x = to_f<TP>(g[e]);
+      acc = fmaf(x, x, acc);
+    }
   }
   acc = block_sum(acc);
   if (threadIdx.x == 0) partials[blockIdx.x] = acc;
@@ -1282,6 +1295,8 @@ __device__ __forceinline__ void adamw_elem(float& p, float g, float& m, float& v
   p = fmaf(p, a.decay, -a.step * (m / fmaf(sqrtf(v), a.inv_sqrt_bc2, a.eps)));
 }
 
+constexpr int kAdamwUnroll = 4;  // chunks of 8 elements in flight per thread
+
 template <typename TP, bool VEC, bool NT>
 __global__ __launch_bounds__(kThreads) void k_adamw(const ScalarSeg* __restrict__ segs,
                                                     const MatPtrs* __restrict__ ptrs,
@@ -1294,11 +1309,11 @@ __global__ __launch_bounds__(kThreads) void k_adamw(const ScalarSeg* __restrict_
   float* vs = v + sg.state;
   const float c = clip ? clip[0] : 1.f;
   const int n = sg.count, nv = VEC ? n >> 3 : 0;
-  for (int c0 = threadIdx.x; c0 < nv; c0 += kThreads * 2) {
-    Raw8<TP> pr[2], gr[2];
-    Raw8<float> mr[2], vr[2];
+  for (int c0 = threadIdx.x; c0 < nv; c0 += kThreads * kAdamwUnroll) {
+    Raw8<TP> pr[kAdamwUnroll], gr[kAdamwUnroll];
+    Raw8<float> mr[kAdamwUnroll], vr[kAdamwUnroll];
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
+    for (int u = 0; u < kAdamwUnroll; ++u) {
       const int k = c0 + kThreads * u;
       if (k < nv) {
         pr[u] = load8r<NT>(p + 8 * k);
@@ -1308,7 +1323,7 @@ __global__ __launch_bounds__(kThreads) void k_adamw(const ScalarSeg* __restrict_
       }
     }
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
+    for (int u = 0; u < kAdamwUnroll; ++u) {
       const int k = c0 + kThreads * u;
       if (k < nv) {
         float pf[8], gf[8], mf[8], vf[8];
@@ -1495,17 +1510,23 @@ hipError_t launch_update(DType param_t, DType ns_t, bool vec, bool nt, int n_seg
   });
 }
 
-hipError_t launch_adamw_sumsq(DType param_t, bool vec, int n_segs, const ScalarSeg* segs,
+int adamw_norm_blocks(int n_segs) { return n_segs < kAdamwNormBlocks ? n_segs : kAdamwNormBlocks; }
+
+hipError_t launch_adamw_sumsq(DType param_t, bool vec, bool nt, int n_segs, const ScalarSeg* segs,
                               const MatPtrs* ptrs, float* partials, hipStream_t s) {
   if (n_segs <= 0) return hipSuccess;
+  const int nb = adamw_norm_blocks(n_segs);
   return dispatch1(param_t, [&](auto p) {
     using TP = decltype(p);
-    if (vec)
-      hipLaunchKernelGGL((k_adamw_sumsq<TP, true>), dim3(n_segs), dim3(kThreads), 0, s, segs, ptrs,
-                         partials);
+    if (vec && nt)
+      hipLaunchKernelGGL((k_adamw_sumsq<TP, true, true>), dim3(nb), dim3(kThreads), 0, s, segs,
+                         n_segs, ptrs, partials);
+    else if (vec)
+      hipLaunchKernelGGL((k_adamw_sumsq<TP, true, false>), dim3(nb), dim3(kThreads), 0, s, segs,
+                         n_segs, ptrs, partials);
     else
-      hipLaunchKernelGGL((k_adamw_sumsq<TP, false>), dim3(n_segs), dim3(kThreads), 0, s, segs, ptrs,
-                         partials);
+      hipLaunchKernelGGL((k_adamw_sumsq<TP, false, false>), dim3(nb), dim3(kThreads), 0, s, segs,
+                         n_segs, ptrs, partials);
     return hipGetLastError();
   });
 }

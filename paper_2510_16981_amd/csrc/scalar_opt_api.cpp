@@ -193,10 +193,11 @@ muonbp_status muonbp_adamw_step(muonbp_adamw_ctx* c, void* const* params, const 
   const DType tp = c->opt.param_dtype == MUONBP_F32 ? DType::F32 : DType::BF16;
   const bool clipping = c->opt.max_grad_norm > 0.f;
   if (clipping) {
-    if ((e = launch_adamw_sumsq(tp, aligned, c->n_segs, c->segs, c->ptrs.current(), c->partials,
-                                c->stream)) != hipSuccess)
+    if ((e = launch_adamw_sumsq(tp, aligned, c->stream_nt, c->n_segs, c->segs, c->ptrs.current(),
+                                c->partials, c->stream)) != hipSuccess)
       return hip_fail(c, e, "gradient norm");
-    if ((e = launch_adamw_clip(c->partials, c->n_segs, c->opt.max_grad_norm, c->clip, c->stream)) !=
+    if ((e = launch_adamw_clip(c->partials, adamw_norm_blocks(c->n_segs), c->opt.max_grad_norm, c->clip,
+                               c->stream)) !=
         hipSuccess)
       return hip_fail(c, e, "clipping factor");
   }
