@@ -45,6 +45,7 @@ struct PackDesc {
   void* dst_t;         // transposed copy: dst_t[c * ld_t + r] = s * Y[r][c]
   int64_t ld_s, ld_t;
   int32_t mat, rows, cols, tiles_c;  // tiles_c: 64-wide column tiles
+  int32_t seg_begin, seg_end;        // the problem's sum-of-squares partials
 };
 
 // One product of a grouped NS launch, all row-major with K contiguous:

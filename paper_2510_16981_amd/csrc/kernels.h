@@ -20,12 +20,17 @@ hipError_t launch_momentum(DType grad_t, DType mom_t, bool vec, bool nt, int n_s
 hipError_t launch_scale(int n_probs, const ScaleDesc* sd, const float* partials,
                         float* scales, float eps, hipStream_t s);
 
-// Z0 = s_p Y_p written straight and transposed into the NS workspace.
+// Z0 = s_p Y_p written straight and/or transposed into the NS workspace.
+// s_p comes from scales, or (fuse_scale) is computed in the kernel from the
+// problem's partial sums exactly as launch_scale would.
 hipError_t launch_pack(DType mom_t, DType grad_t, DType ns_t, bool vec, int n_tiles,
                        const TileRef* tiles, const PackDesc* pd,
                        const MatPtrs* mats, const void* mom,
-                       const float* scales, float mu, int nesterov,
-                       hipStream_t s);
+                       const float* scales, const float* partials, float eps,
+                       bool fuse_scale, float mu, int nesterov, hipStream_t s);
+
+// Problems up to this many partial sums get their scale inside the pack.
+constexpr int kFuseScaleMaxPartials = 1024;
 
 // Grouped C = alpha X Y^T + beta D + gamma I (+ transposed copy) over a
 // tile list whose tile shape is `variant` (GemmVariant in device_types.h);

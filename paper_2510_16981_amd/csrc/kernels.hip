@@ -225,16 +225,31 @@ __global__ __launch_bounds__(64) void k_scale(const ScaleDesc* __restrict__ sd,
 // of 8 elements and the pointers 16-byte aligned, so every access is one
 // 16-byte chunk of 8 elements (the last chunk of a Z^T row may be cut by the
 // problem's row count).
+// fuse_scale: s is computed here from the problem's partial sums, exactly
+// as k_scale computes it (same lanes, same order), instead of read from
+// scales (small problems: the separate launch costs more than the sum).
 template <typename TM, typename TG, typename TN, bool VEC>
 __global__ __launch_bounds__(kThreads) void k_pack(
     const TileRef* __restrict__ tiles, const PackDesc* __restrict__ pd,
     const MatPtrs* __restrict__ mats, const TM* __restrict__ mom,
-    const float* __restrict__ scales, float mu, int nesterov) {
+    const float* __restrict__ scales, const float* __restrict__ partials, float eps,
+    int fuse_scale, float mu, int nesterov) {
   __shared__ float tile[64][65];
+  __shared__ float s_fused;
   const TileRef t = tiles[blockIdx.x];
   const PackDesc d = pd[t.prob];
   const int r0 = (t.ij >> 16) * 64, c0 = (t.ij & 0xffff) * 64;
-  const float s = scales[t.prob];
+  if (fuse_scale) {  // uniform
+    if (threadIdx.x < 64) {
+      double acc = 0.0;
+      for (int i = d.seg_begin + int(threadIdx.x); i < d.seg_end; i += 64) acc += partials[i];
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) acc += __shfl_xor(acc, o);
+      if (threadIdx.x == 0) s_fused = float(1.0 / (sqrt(acc) + double(eps)));
+    }
+    __syncthreads();
+  }
+  const float s = fuse_scale ? s_fused : scales[t.prob];
   const TM* m = mom + d.mom_off;
   const TG* g = static_cast<const TG*>(mats[d.mat].grad) + d.in_mat_off;
   TN* ds = static_cast<TN*>(d.dst_s);
@@ -1390,8 +1405,8 @@ hipError_t launch_scale(int n_probs, const ScaleDesc* sd, const float* partials,
 
 hipError_t launch_pack(DType mom_t, DType grad_t, DType ns_t, bool vec, int n_tiles,
                        const TileRef* tiles, const PackDesc* pd, const MatPtrs* mats,
-                       const void* mom, const float* scales, float mu, int nesterov,
-                       hipStream_t s) {
+                       const void* mom, const float* scales, const float* partials, float eps,
+                       bool fuse_scale, float mu, int nesterov, hipStream_t s) {
   if (n_tiles <= 0) return hipSuccess;
   return dispatch1(mom_t, [&](auto m) {
     return dispatch1(grad_t, [&](auto g) {
@@ -1399,12 +1414,15 @@ hipError_t launch_pack(DType mom_t, DType grad_t, DType ns_t, bool vec, int n_ti
         using TM = decltype(m);
         using TG = decltype(g);
         using TN = decltype(n);
+        const int fuse = fuse_scale ? 1 : 0;
         if (vec)
           hipLaunchKernelGGL((k_pack<TM, TG, TN, true>), dim3(n_tiles), dim3(kThreads), 0, s, tiles,
-                             pd, mats, static_cast<const TM*>(mom), scales, mu, nesterov);
+                             pd, mats, static_cast<const TM*>(mom), scales, partials, eps, fuse, mu,
+                             nesterov);
         else
           hipLaunchKernelGGL((k_pack<TM, TG, TN, false>), dim3(n_tiles), dim3(kThreads), 0, s, tiles,
-                             pd, mats, static_cast<const TM*>(mom), scales, mu, nesterov);
+                             pd, mats, static_cast<const TM*>(mom), scales, partials, eps, fuse, mu,
+                             nesterov);
         return hipGetLastError();
       });
     });

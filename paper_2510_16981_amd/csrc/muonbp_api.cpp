@@ -34,6 +34,7 @@ struct PlanDev {
   std::vector<TileRef*> phase_tiles;     // one tile list per launch phase
   UpdDesc* upd = nullptr;
   std::vector<UpdDesc> upd_host;  // for muonbp_get_update
+  bool fuse_scale = false;        // the pack computes the scales (no k_scale launch)
 };
 
 struct ProfRec {
@@ -160,8 +161,10 @@ hipError_t build_plan_tables(muonbp_ctx* c, int full) {
   std::vector<ScaleDesc> sd;
   std::vector<PackDesc> pk;
   std::vector<GemmDesc> descs;
+  pd.fuse_scale = true;
   for (const Problem& p : plan.probs) {
     sd.push_back(ScaleDesc{p.seg_begin, p.seg_end});
+    pd.fuse_scale = pd.fuse_scale && p.seg_end - p.seg_begin <= kFuseScaleMaxPartials;
     const MatrixShape& m = c->lay.mats[p.mat];
     PackDesc d{};
     d.in_mat_off = p.row0 * m.cols + p.col0;
@@ -171,6 +174,8 @@ hipError_t build_plan_tables(muonbp_ctx* c, int full) {
     d.rows = int32_t(p.rows);
     d.cols = int32_t(p.cols);
     d.tiles_c = int32_t((p.cols + kPackTile - 1) / kPackTile);
+    d.seg_begin = p.seg_begin;
+    d.seg_end = p.seg_end;
     // Z = Y (S = rows) or Y^T (S = cols); Z^T the other way round, needed
     // by the NT apply, or as U when there are no iterations.
     const bool want_zt = !plan.nn_apply || o.ns_steps == 0;
@@ -533,13 +538,15 @@ muonbp_status muonbp_step(muonbp_ctx* c, void* const* params, const void* const*
                            c->mu, o.nesterov, c->partials, s);
   });
   if (e != hipSuccess) return hip_fail(c, e, "momentum");
-  e = timed(c, 1, [&] {
-    return launch_scale(int(plan.probs.size()), pd.scale, c->partials, c->scales, o.eps, s);
-  });
-  if (e != hipSuccess) return hip_fail(c, e, "scale");
+  if (!pd.fuse_scale) {
+    e = timed(c, 1, [&] {
+      return launch_scale(int(plan.probs.size()), pd.scale, c->partials, c->scales, o.eps, s);
+    });
+    if (e != hipSuccess) return hip_fail(c, e, "scale");
+  }
   e = timed(c, 2, [&] {
-    return launch_pack(tm, tp, tn, aligned, int(plan.pack_tiles.size()), pd.pack_tiles, pd.pack, mats, c->mom,
-                       c->scales, c->mu, o.nesterov, s);
+    return launch_pack(tm, tp, tn, aligned, int(plan.pack_tiles.size()), pd.pack_tiles, pd.pack, mats,
+                       c->mom, c->scales, c->partials, o.eps, pd.fuse_scale, c->mu, o.nesterov, s);
   });
   if (e != hipSuccess) return hip_fail(c, e, "pack");
   const int nphases = int(plan.phases.size());
