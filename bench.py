@@ -269,6 +269,26 @@ MFMA_COUNTERS = ("SQ_INSTS_VALU_MFMA_MOPS_BF16", "MfmaUtil", "GRBM_GUI_ACTIVE")
 ELEMENTWISE_BYTES = {"k_momentum": 6, "k_pack": 4, "k_update": 6}
 
 
+# Commands that make the runs each summary is ingested from (the default of
+# --command; all run from committed files only).
+COUNTER_COMMANDS = """\
+cd /tmp && export TMPDIR=/tmp   # R = repository root, W = workload
+rocprofv3 --pmc FETCH_SIZE -f csv -d $R/gpurun_out/prof/copy_fetch -o run -- python3 $R/bench.py --copy-probe 1024 > $R/gpurun_out/prof/copy_fetch/copy_probe.json
+rocprofv3 --pmc WRITE_SIZE -f csv -d $R/gpurun_out/prof/copy_write -o run -- python3 $R/bench.py --copy-probe 1024
+rocprofv3 --pmc SQ_INSTS_VALU_MFMA_MOPS_BF16 MfmaUtil GRBM_GUI_ACTIVE -f csv -d $R/gpurun_out/prof/mfma_probe -o run -- python3 $R/bench.py --mfma-probe > $R/gpurun_out/prof/mfma_probe/mfma_probe.json
+# kind=block with P=0, kind=full with P=1; each run's JSON line saved as b.json in its folder
+rocprofv3 --pmc FETCH_SIZE -f csv -d $R/gpurun_out/prof/$W/${kind}_fetch -o run -- python3 $R/bench.py --workload $W --period $P --steps 10 --warmup 2 --no-cpu-baseline --no-scalar
+rocprofv3 --pmc WRITE_SIZE -f csv -d $R/gpurun_out/prof/$W/${kind}_write -o run -- python3 $R/bench.py --workload $W --period $P --steps 10 --warmup 2 --no-cpu-baseline --no-scalar
+rocprofv3 --pmc SQ_INSTS_VALU_MFMA_MOPS_BF16 MfmaUtil GRBM_GUI_ACTIVE -f csv -d $R/gpurun_out/prof/$W/${kind}_mfma -o run -- python3 $R/bench.py --workload $W --period $P --steps 10 --warmup 2 --no-cpu-baseline --no-scalar
+python3 bench.py --workload $W --ingest-counters gpurun_out/prof/{copy_fetch,copy_write,mfma_probe} gpurun_out/prof/$W/{block_fetch,block_write,block_mfma,full_fetch,full_write,full_mfma}
+"""
+KERNEL_TRACE_COMMANDS = """\
+cd /tmp && export TMPDIR=/tmp   # R = repository root
+rocprofv3 --kernel-trace --stats -f csv -d $R/gpurun_out/prof/kt -o run -- python3 $R/bench.py --no-cpu-baseline > $R/gpurun_out/prof/kt/bench.json
+python3 bench.py --ingest-kernel-trace gpurun_out/prof/kt
+"""
+
+
 def ingest_counters(workload, dirs, command):
     """Write profiles/counters_<workload>.md from nine rocprofv3 --pmc runs
     (one folder each, in INGEST_DIRS order): FETCH_SIZE and WRITE_SIZE of
@@ -597,16 +617,19 @@ def main():
     ap.add_argument("--ingest-workloads", nargs="+", metavar="JSON", default=None,
                     help="write profiles/steps_larger_workloads.md from bench.py JSON outputs "
                          "(no GPU use)")
-    ap.add_argument("--command", default="", help="with --ingest-*: the commands that made the runs")
+    ap.add_argument("--command", default=None,
+                    help="with --ingest-*: the commands that made the runs (default: the standard ones)")
     args = ap.parse_args()
     if args.ingest_counters:
-        ingest_counters(args.workload, args.ingest_counters, args.command)
+        ingest_counters(args.workload, args.ingest_counters,
+                        COUNTER_COMMANDS if args.command is None else args.command)
         return
     if args.ingest_workloads:
         ingest_workloads(args.ingest_workloads, os.path.join(PROFILES, "steps_larger_workloads.md"))
         return
     if args.ingest_kernel_trace:
-        ingest_kernel_trace(args.workload, args.ingest_kernel_trace, args.command)
+        ingest_kernel_trace(args.workload, args.ingest_kernel_trace,
+                            KERNEL_TRACE_COMMANDS if args.command is None else args.command)
         return
     if args.gpus != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "

@@ -934,9 +934,21 @@ __global__ __launch_bounds__(kThreads) void k_ns_gemm_dma(const GemmDesc* __rest
 // NN (Y row-major K x N, ldy its row pitch; the apply product reads Z this
 // way, so no transposed copy of Z is needed): a stage holds the Y slice as
 // 32 k-rows of BN elements, 16-byte chunk c of k-row r stored at position
-// c ^ 2 (r % 4), and the B operands come from LDS transpose reads, two per
-// fragment (k 0..3 and 4..7 of the lane's 8).  Y chunks past N and k-rows
-// past K are copied as zeros.
+// c ^ nn_swz<BN>(r), and the B operands come from LDS transpose reads, two
+// per fragment (k 0..3 and 4..7 of the lane's 8).  Y chunks past N and
+// k-rows past K are copied as zeros.
+// Chunk swizzle of the NN Y stage.  The 32 lanes of one LDS transpose-read
+// pass fetch k-rows r0 .. r0 + 3 (r0 % 4 == 0) x four aligned 16-byte chunks
+// of each row.  With a row pitch of 512 or 256 bytes every row starts on
+// the same banks, so row r's chunks move by 4 (r % 4) (64 bytes): the 16
+// chunks land on 16 different 16-byte bank groups.  With 384 bytes odd rows
+// already start 128 bytes over, and 4 ((r % 4) / 2) separates the rest while
+// staying inside each aligned group of 8 chunks (a row has 24).
+template <int BN>
+__device__ __forceinline__ int nn_swz(int r) {
+  return BN % 128 == 0 ? 4 * (r & 3) : 4 * ((r & 3) >> 1);
+}
+
 template <int BM, int BN, bool NN>
 __global__ __launch_bounds__(kThreads) void k_ns_gemm_dmap(const GemmDesc* __restrict__ probs,
                                                            const TileRef* __restrict__ tiles,
@@ -952,7 +964,7 @@ __global__ __launch_bounds__(kThreads) void k_ns_gemm_dmap(const GemmDesc* __res
   constexpr int NR = NN ? TM + 2 * TN : NF;
   constexpr int RPM = (NR + NM - 1) / NM;  // reads issued after each MFMA of a step
   constexpr int CPR = BN / 8;  // NN: 16-byte chunks per staged k-row
-  static_assert(!NN || CPR % 8 == 0, "NN chunk swizzle needs BN % 64 == 0");
+  static_assert(!NN || (BN % 128 == 0 ? CPR % 16 == 0 : CPR % 8 == 0), "NN chunk swizzle range");
   static_assert(BM % 64 == 0, "copy jj holds X rows iff jj < BM / 64");
   // MFMAs of the second step issued before the barrier: one keeps the
   // matrix pipeline busy while the barrier resolves, and leaves the rest of
@@ -980,7 +992,7 @@ __global__ __launch_bounds__(kThreads) void k_ns_gemm_dmap(const GemmDesc* __res
     const int u = wave + 4 * jj;
     if (NN && jj >= BM / 64) {  // Y slice copy (u >= BM / 16)
       const int q = 64 * (u - BM / 16) + lane, kr = q / CPR;
-      const int cn = (q - kr * CPR) ^ (2 * (kr & 3));
+      const int cn = (q - kr * CPR) ^ nn_swz<BN>(kr);
       chunk[jj] = kr;
       voff[jj] = n0 + 8 * cn < d.N ? (kr * d.ldy + n0 + 8 * cn) * ES : ybytes;
     } else {
@@ -1034,13 +1046,13 @@ __global__ __launch_bounds__(kThreads) void k_ns_gemm_dmap(const GemmDesc* __res
   if (NN) {
     // Y fragment j: n = wn 32 TN + 32 j + 16 ((lane / 16) % 2) + 4 (lane % 4)
     // .. + 3, k-row 8 (lane / 32) + (lane % 16) / 4 (+ 16 s + 4 r); the
-    // swizzle 2 (k-row % 4) is 2 ((lane % 16) / 4).
+    // k-row % 4 the swizzle depends on is (lane % 16) / 4.
     const int si = lane & 15, g = lane >> 4;
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
       const int n = wn * 32 * TN + 32 * j + 16 * (g & 1) + 4 * (si & 3);
       const int kr = 8 * (g >> 1) + (si >> 2);
-      fa[TM + j] = lds_addr(lds) + BM * kDmaRow + kr * (2 * BN) + (((n >> 3) ^ (2 * (si >> 2))) << 4) +
+      fa[TM + j] = lds_addr(lds) + BM * kDmaRow + kr * (2 * BN) + (((n >> 3) ^ nn_swz<BN>(si >> 2)) << 4) +
                    8 * (si & 1);
     }
   }
