@@ -29,8 +29,13 @@ hipError_t launch_pack(DType mom_t, DType grad_t, DType ns_t, bool vec, int n_ti
                        const float* scales, const float* partials, float eps,
                        bool fuse_scale, float mu, int nesterov, hipStream_t s);
 
-// Problems up to this many partial sums get their scale inside the pack.
-constexpr int kFuseScaleMaxPartials = 1024;
+// The pack computes the scales itself (no separate scale launch) when its
+// workgroups would read at most this many partial sums in all: every pack
+// workgroup reads all the partials of its unit, so the cost grows with
+// tiles x partials per unit.  Measured: 0.3 M reads (2048x768 shards) add
+// 1.3 us to the pack against 6 us for the scale launch; 2.4 M reads (the
+// whole 2048x6144 matrix) add 7 us; 8.4 M add 17 us and 268 M 266 us.
+constexpr int64_t kFuseScaleMaxReads = int64_t(1) << 20;
 
 // Grouped C = alpha X Y^T + beta D + gamma I (+ transposed copy) over a
 // tile list whose tile shape is `variant` (GemmVariant in device_types.h);

@@ -161,10 +161,14 @@ hipError_t build_plan_tables(muonbp_ctx* c, int full) {
   std::vector<ScaleDesc> sd;
   std::vector<PackDesc> pk;
   std::vector<GemmDesc> descs;
-  pd.fuse_scale = true;
+  std::vector<int64_t> pack_tiles_of(plan.probs.size(), 0);
+  for (const TileRef& t : plan.pack_tiles) ++pack_tiles_of[size_t(t.prob)];
+  int64_t fused_reads = 0;
+  for (size_t i = 0; i < plan.probs.size(); ++i)
+    fused_reads += pack_tiles_of[i] * (plan.probs[i].seg_end - plan.probs[i].seg_begin);
+  pd.fuse_scale = fused_reads <= kFuseScaleMaxReads;
   for (const Problem& p : plan.probs) {
     sd.push_back(ScaleDesc{p.seg_begin, p.seg_end});
-    pd.fuse_scale = pd.fuse_scale && p.seg_end - p.seg_begin <= kFuseScaleMaxPartials;
     const MatrixShape& m = c->lay.mats[p.mat];
     PackDesc d{};
     d.in_mat_off = p.row0 * m.cols + p.col0;
