@@ -36,8 +36,9 @@ the design notes of the repository):
   X <- X - eta_t (lambda X + s U);
 * RMS matching multiplies U by beta * sqrt(max(p, q)) where p x q is the shape
   of the orthogonalized unit (block on block steps, matrix on full steps);
-* Nesterov momentum (NS input G + mu M) is an option that the paper does not
-  state -- its parity is unpinned;  it is off by default.
+* Nesterov momentum (NS input G + mu M, M after this step's update) is an
+  option that the paper does not state;  it is off by default, and its input
+  is pinned by closed forms over two steps (tests of the oracle).
 
 Every function here works in float64 on the exact values it is given.
 """

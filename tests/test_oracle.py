@@ -282,6 +282,29 @@ def test_step_composition_against_closed_forms():
     assert _rel(X1 - X2, cfg.lr_block * U1) <= 1e-12
 
 
+def test_nesterov_input_closed_form():
+    """The Nesterov variant (an opt-in reading: the paper's Alg. 1 has the
+    heavy-ball sum only): the NS input is G_t + mu M_t, M_t being the
+    momentum after this step's update.  With lambda = 0, two steps from
+    M = 0 have closed forms, Y_0 = (1 + mu) G_0 and Y_1 = (1 + mu) G_1 +
+    mu^2 G_0, each update being the SVD closed form of its input.  Taking
+    the momentum before the update (Y_1 = G_1 + mu G_0) or dropping mu fails
+    here."""
+    rng = np.random.default_rng(13)
+    spec = [O.MatrixSpec(8, 12, 1, 3)]
+    cfg = _cfg(period=2, weight_decay=0.0, nesterov=True)
+    mu = cfg.momentum
+    orc = O.MuonBPOracle(spec, cfg)
+    X0 = rng.standard_normal((8, 12))
+    G0, G1 = rng.standard_normal((8, 12)), rng.standard_normal((8, 12))
+    X1 = orc.step([X0], [G0], 0)[0]
+    assert _rel(X0 - X1, cfg.lr_full * _svd_closed_form((1 + mu) * G0, 5)) <= 1e-12
+    X2 = orc.step([X1], [G1], 1)[0]
+    Y1 = (1 + mu) * G1 + mu ** 2 * G0
+    U1 = np.hstack([_svd_closed_form(Y1[:, 4 * j:4 * j + 4], 5) for j in range(3)])
+    assert _rel(X1 - X2, cfg.lr_block * U1) <= 1e-12
+
+
 def test_period_one_is_muon_and_infinite_period_is_blockmuon():
     """Sec. 3.2: P = 1 gives Muon (every step full), P = infinity gives
     BlockMuon (every step blockwise)."""
