@@ -288,13 +288,14 @@ template <typename F>
 hipError_t timed(muonbp_ctx* c, int kind, F&& launch) {
   if (c->prof != 1) return launch();
   hipEvent_t a = take_event(c), b = take_event(c);
-  if (!a || !b) return hipErrorOutOfMemory;
-  hipError_t e = hipEventRecord(a, c->stream);
-  if (e != hipSuccess) return e;
-  e = launch();
-  if (e != hipSuccess) return e;
-  e = hipEventRecord(b, c->stream);
-  if (e != hipSuccess) return e;
+  hipError_t e = (a && b) ? hipEventRecord(a, c->stream) : hipErrorOutOfMemory;
+  if (e == hipSuccess) e = launch();
+  if (e == hipSuccess) e = hipEventRecord(b, c->stream);
+  if (e != hipSuccess) {  // the events go back to the pool
+    if (a) c->ev_pool.push_back(a);
+    if (b) c->ev_pool.push_back(b);
+    return e;
+  }
   c->prof_recs.push_back(ProfRec{kind, c->prof_full, 1, a, b});
   return hipSuccess;
 }
@@ -303,10 +304,16 @@ hipError_t timed(muonbp_ctx* c, int kind, F&& launch) {
 // launch of a step (kind 7); the launches in between run back to back.
 hipError_t span_mark(muonbp_ctx* c, bool begin, int launches) {
   if (c->prof != 2 || launches == 0) return hipSuccess;
+  // The end mark closes the open span its begin mark left last.
+  if (!begin && (c->prof_recs.empty() || c->prof_recs.back().kind != 7 || c->prof_recs.back().stop))
+    return hipErrorInvalidValue;
   hipEvent_t ev = take_event(c);
   if (!ev) return hipErrorOutOfMemory;
   hipError_t e = hipEventRecord(ev, c->stream);
-  if (e != hipSuccess) return e;
+  if (e != hipSuccess) {
+    c->ev_pool.push_back(ev);
+    return e;
+  }
   if (begin) {
     c->prof_recs.push_back(ProfRec{7, c->prof_full, launches, ev, nullptr});
   } else {
