@@ -438,18 +438,20 @@ __device__ __forceinline__ void store_chunk(T* out, int ld, int row, int col, in
 }
 
 // Epilogue shared by the NS GEMM kernels: writes the workgroup tile at
-// (m0, n0) from the accumulators of its 4 waves (2 x 2 layout, TM x TN MFMA
-// 32x32 tiles each).  st: this wave's free LDS block of 32 * (32 TN + 1)
-// floats.  gamma is added on the diagonal of C (row == column).  Waves with
+// (m0, n0) from the accumulators of its WM x WN waves (row-major layout,
+// TM x TN MFMA 32x32 tiles each; wave w sits at (w / WN, w % WN), taken
+// modulo WM WN so that the second K group of a split workgroup mirrors the
+// first).  st: this wave's free LDS block of 32 * (32 TN + 1) floats.
+// gamma is added on the diagonal of C (row == column).  Waves with
 // active == false only take part in the workgroup barriers.
-template <typename T, int TM, int TN>
+template <typename T, int TM, int TN, int WM = 2, int WN = 2>
 __device__ __forceinline__ void gemm_epilogue(f32x16_t (&acc)[TM][TN], float* st,
                                               const GemmDesc& d, int m0, int n0, bool diag,
                                               float alpha, float beta, float gamma,
                                               bool active = true) {
   constexpr int ES = sizeof(T);
-  const int lane = threadIdx.x & 63, wave = (threadIdx.x >> 6) & 3;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int lane = threadIdx.x & 63, wave = (threadIdx.x >> 6) % (WM * WN);
+  const int wm = wave / WN, wn = wave % WN;
   // One pass per MFMA row of the wave's sub-tile (32 x 32TN): alpha * acc
   // is staged in a wave-private LDS block (odd pitch), then each lane
   // writes 8-element (16-byte) chunks of C rows and, for the transposed
@@ -949,15 +951,20 @@ __device__ __forceinline__ int nn_swz(int r) {
   return BN % 128 == 0 ? 4 * (r & 3) : 4 * ((r & 3) >> 1);
 }
 
-template <int BM, int BN, bool NN>
-__global__ __launch_bounds__(kThreads) void k_ns_gemm_dmap(const GemmDesc* __restrict__ probs,
+template <int BM, int BN, bool NN, int WM, int WN>
+__global__ __launch_bounds__(64 * WM * WN) void k_ns_gemm_dmap(const GemmDesc* __restrict__ probs,
                                                            const TileRef* __restrict__ tiles,
                                                            int nsplit, float* __restrict__ ksum,
                                                            int* __restrict__ kcount) {
   constexpr int NS = 4;
   using G = DmaShape<BM, BN, NS>;
   using T = bf16;
-  constexpr int TM = G::TM, TN = G::TN, LPW = G::LPW, ES = 2, NF = TM + TN;
+  // WM x WN waves, each owning a (BM / WM) x (BN / WN) sub-tile of TM x TN
+  // MFMA tiles; every wave issues LPW of the 16-row copies of a slice.
+  constexpr int W = WM * WN;
+  constexpr int TM = BM / (32 * WM), TN = BN / (32 * WN), ES = 2, NF = TM + TN;
+  constexpr int LPW = (BM + BN) / (16 * W);
+  static_assert(TM * 32 * WM == BM && TN * 32 * WN == BN && LPW * 16 * W == BM + BN, "wave layout");
   constexpr int NM = TM * TN;  // MFMAs per K step
   // LDS read instructions per K step: one per X fragment; one per Y
   // fragment (NT) or two (NN).
@@ -965,13 +972,14 @@ __global__ __launch_bounds__(kThreads) void k_ns_gemm_dmap(const GemmDesc* __res
   constexpr int RPM = (NR + NM - 1) / NM;  // reads issued after each MFMA of a step
   constexpr int CPR = BN / 8;  // NN: 16-byte chunks per staged k-row
   static_assert(!NN || (BN % 128 == 0 ? CPR % 16 == 0 : CPR % 8 == 0), "NN chunk swizzle range");
-  static_assert(BM % 64 == 0, "copy jj holds X rows iff jj < BM / 64");
+  static_assert(BM % (16 * W) == 0, "copy jj holds X rows iff jj < BM / (16 W)");
   // MFMAs of the second step issued before the barrier: one keeps the
   // matrix pipeline busy while the barrier resolves, and leaves the rest of
   // the step to hide the next slice's reads (measured: 2-4% faster than
   // half the step on every tile shape).
   constexpr int H = 1;
-  __shared__ __attribute__((aligned(1024))) unsigned char lds[G::LDS_BYTES];
+  constexpr int EPI = W * 32 * (32 * TN + 1) * 4;  // epilogue staging, one block per wave
+  __shared__ __attribute__((aligned(1024))) unsigned char lds[NS * G::STAGE > EPI ? NS * G::STAGE : EPI];
 
   const TileRef t = tiles[blockIdx.x];
   const GemmDesc d = probs[t.prob];
@@ -979,7 +987,7 @@ __global__ __launch_bounds__(kThreads) void k_ns_gemm_dmap(const GemmDesc* __res
   const int m0 = ti * BM, n0 = tj * BN;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WN, wn = wave % WN;
 
   const int xbytes = d.M * d.ldx * ES, ybytes = (NN ? d.K : d.N) * d.ldy * ES;
   const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(d.X), 0, xbytes, kBufferWord3);
@@ -989,8 +997,8 @@ __global__ __launch_bounds__(kThreads) void k_ns_gemm_dmap(const GemmDesc* __res
   int voff[LPW], chunk[LPW];
 #pragma unroll
   for (int jj = 0; jj < LPW; ++jj) {
-    const int u = wave + 4 * jj;
-    if (NN && jj >= BM / 64) {  // Y slice copy (u >= BM / 16)
+    const int u = wave + W * jj;
+    if (NN && jj >= BM / (16 * W)) {  // Y slice copy (u >= BM / 16)
       const int q = 64 * (u - BM / 16) + lane, kr = q / CPR;
       const int cn = (q - kr * CPR) ^ nn_swz<BN>(kr);
       chunk[jj] = kr;
@@ -1009,9 +1017,9 @@ __global__ __launch_bounds__(kThreads) void k_ns_gemm_dmap(const GemmDesc* __res
   auto copy = [&](int kt, int jj) {
     unsigned char* base = lds + (kt % NS) * G::STAGE;
     const int k0 = kt * 32;
-    lds_void_t* dst = (lds_void_t*)(base + (wave + 4 * jj) * 1024);
+    lds_void_t* dst = (lds_void_t*)(base + (wave + W * jj) * 1024);
     if constexpr (NN) {
-      if (jj < BM / 64) {  // X rows (wave + 4 jj < BM / 16 for every wave)
+      if (jj < BM / (16 * W)) {  // X rows (wave + W jj < BM / 16 for every wave)
         const bool kin = kt < ke && k0 + 8 * chunk[jj] < d.K;
         dma16(xr, dst, kin ? voff[jj] : xbytes, k0 * ES);
       } else {
@@ -1020,7 +1028,7 @@ __global__ __launch_bounds__(kThreads) void k_ns_gemm_dmap(const GemmDesc* __res
       }
     } else {
       const bool kin = kt < ke && k0 + 8 * chunk[jj] < d.K;
-      if (wave + 4 * jj < BM / 16)  // uniform: X rows
+      if (wave + W * jj < BM / 16)  // uniform: X rows
         dma16(xr, dst, kin ? voff[jj] : xbytes, k0 * ES);
       else
         dma16(yr, dst, kin ? voff[jj] : ybytes, k0 * ES);
@@ -1192,8 +1200,8 @@ __global__ __launch_bounds__(kThreads) void k_ns_gemm_dmap(const GemmDesc* __res
     if (tid == 0) __hip_atomic_store(kcount + t.slot, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
   __syncthreads();
-  gemm_epilogue<T, TM, TN>(acc, reinterpret_cast<float*>(lds) + wave * 32 * (32 * TN + 1), d, m0, n0,
-                           ti == tj && d.sym, d.alpha, d.beta, d.gamma);
+  gemm_epilogue<T, TM, TN, WM, WN>(acc, reinterpret_cast<float*>(lds) + wave * 32 * (32 * TN + 1), d,
+                                   m0, n0, ti == tj && d.sym, d.alpha, d.beta, d.gamma);
 }
 
 // ---------------------------------------------------------------- update
@@ -1472,21 +1480,23 @@ hipError_t launch_ns_gemm(DType ns_t, int variant, bool nn, int n_tiles, const G
       case kGemmDmaP192x256:
       case kGemmDmaP256x192:
       case kGemmDmaP192x192:
+      case kGemmDmaP256x256W8:
         if constexpr (std::is_same<TN, bf16>::value) {
-#define MUONBP_DMAP(BM_, BN_)                                                                   \
+#define MUONBP_DMAP(BM_, BN_, WM_, WN_)                                                        \
   if (nn)                                                                                      \
-    hipLaunchKernelGGL((k_ns_gemm_dmap<BM_, BN_, true>), dim3(n_tiles), dim3(kThreads), 0, s,  \
-                       probs, tiles, nsplit, ksum, kcount);                                    \
+    hipLaunchKernelGGL((k_ns_gemm_dmap<BM_, BN_, true, WM_, WN_>), dim3(n_tiles),              \
+                       dim3(64 * WM_ * WN_), 0, s, probs, tiles, nsplit, ksum, kcount);        \
   else                                                                                         \
-    hipLaunchKernelGGL((k_ns_gemm_dmap<BM_, BN_, false>), dim3(n_tiles), dim3(kThreads), 0, s, \
-                       probs, tiles, nsplit, ksum, kcount)
+    hipLaunchKernelGGL((k_ns_gemm_dmap<BM_, BN_, false, WM_, WN_>), dim3(n_tiles),             \
+                       dim3(64 * WM_ * WN_), 0, s, probs, tiles, nsplit, ksum, kcount)
           switch (variant) {
-            case kGemmDmaP128x128: MUONBP_DMAP(128, 128); break;
-            case kGemmDmaP256x128: MUONBP_DMAP(256, 128); break;
-            case kGemmDmaP256x256: MUONBP_DMAP(256, 256); break;
-            case kGemmDmaP192x256: MUONBP_DMAP(192, 256); break;
-            case kGemmDmaP256x192: MUONBP_DMAP(256, 192); break;
-            default: MUONBP_DMAP(192, 192); break;
+            case kGemmDmaP128x128: MUONBP_DMAP(128, 128, 2, 2); break;
+            case kGemmDmaP256x128: MUONBP_DMAP(256, 128, 2, 2); break;
+            case kGemmDmaP256x256: MUONBP_DMAP(256, 256, 2, 2); break;
+            case kGemmDmaP192x256: MUONBP_DMAP(192, 256, 2, 2); break;
+            case kGemmDmaP256x192: MUONBP_DMAP(256, 192, 2, 2); break;
+            case kGemmDmaP256x256W8: MUONBP_DMAP(256, 256, 2, 4); break;
+            default: MUONBP_DMAP(192, 192, 2, 2); break;
           }
 #undef MUONBP_DMAP
           break;
