@@ -83,10 +83,11 @@ typedef struct {
                                11/12/13 = 128x128 / 256x128 / 256x256 /
                                192x256 / 256x192 / 192x192 tiles with the
                                LDS-DMA loop interleaved with the MFMAs (same
-                               conditions as 4-6); 14 = 256x256 interleaved
-                               tiles over 8 waves (two per SIMD).
+                               conditions as 4-6); 14/15/16 = 256x256 /
+                               192x256 / 256x192 interleaved tiles over 8
+                               waves (two per SIMD).
                                Symmetric products use square tiles (128x128
-                               for 2, 5, 9; 192x192 for 11, 12). */
+                               for 2, 5, 9; 192x192 for 11, 12, 15, 16). */
   int32_t k_split;          /* interleaved DMA kernels only: 1..8 = each
                                tile's K loop shared by that many workgroups
                                (fp32 partial sums added by the last one to

@@ -77,15 +77,15 @@ enum GemmVariant : int32_t {
   kGemm128x128Split2 = 6,
   kGemmDmaP128x128 = 7, kGemmDmaP256x128 = 8, kGemmDmaP256x256 = 9,
   kGemmDmaP192x256 = 10, kGemmDmaP256x192 = 11, kGemmDmaP192x192 = 12,
-  kGemmDmaP256x256W8 = 13,
-  kNumGemmVariants = 14
+  kGemmDmaP256x256W8 = 13, kGemmDmaP192x256W8 = 14, kGemmDmaP256x192W8 = 15,
+  kNumGemmVariants = 16
 };
-constexpr int kGemmTileRows[kNumGemmVariants] = {128, 256, 256, 128, 256, 256, 128,
-                                                 128, 256, 256, 192, 256, 192, 256};
-constexpr int kGemmTileCols[kNumGemmVariants] = {128, 128, 256, 128, 128, 256, 128,
-                                                 128, 128, 256, 256, 192, 192, 256};
-constexpr bool kGemmIsDma[kNumGemmVariants] = {false, false, false, true, true, true, false,
-                                               true,  true,  true,  true, true, true, true};
+constexpr int kGemmTileRows[kNumGemmVariants] = {128, 256, 256, 128, 256, 256, 128, 128,
+                                                 256, 256, 192, 256, 192, 256, 192, 256};
+constexpr int kGemmTileCols[kNumGemmVariants] = {128, 128, 256, 128, 128, 256, 128, 128,
+                                                 128, 256, 256, 192, 192, 256, 256, 192};
+constexpr bool kGemmIsDma[kNumGemmVariants] = {false, false, false, true, true, true, false, true,
+                                               true,  true,  true,  true, true, true, true,  true};
 // Interleaved DMA kernels (k_ns_gemm_dmap).
 constexpr bool gemm_is_dmap(int v) { return v >= kGemmDmaP128x128; }
 

@@ -960,11 +960,16 @@ __global__ __launch_bounds__(64 * WM * WN) void k_ns_gemm_dmap(const GemmDesc* _
   using G = DmaShape<BM, BN, NS>;
   using T = bf16;
   // WM x WN waves, each owning a (BM / WM) x (BN / WN) sub-tile of TM x TN
-  // MFMA tiles; every wave issues LPW of the 16-row copies of a slice.
+  // MFMA tiles.  A slice is RG copies of 1 KB (16 rows of X or Y, or two NN
+  // k-rows); wave w issues copies w, w + W, ...  When W does not divide RG,
+  // a wave past the last copy repeats its previous one (same bytes to the
+  // same LDS place), so that every wave has LPW copies per slice in flight
+  // and the waits stay constant counts.
   constexpr int W = WM * WN;
   constexpr int TM = BM / (32 * WM), TN = BN / (32 * WN), ES = 2, NF = TM + TN;
-  constexpr int LPW = (BM + BN) / (16 * W);
-  static_assert(TM * 32 * WM == BM && TN * 32 * WN == BN && LPW * 16 * W == BM + BN, "wave layout");
+  constexpr int RG = (BM + BN) / 16;
+  constexpr int LPW = (RG + W - 1) / W;
+  static_assert(TM * 32 * WM == BM && TN * 32 * WN == BN && RG * 16 == BM + BN, "wave layout");
   constexpr int NM = TM * TN;  // MFMAs per K step
   // LDS read instructions per K step: one per X fragment; one per Y
   // fragment (NT) or two (NN).
@@ -972,7 +977,7 @@ __global__ __launch_bounds__(64 * WM * WN) void k_ns_gemm_dmap(const GemmDesc* _
   constexpr int RPM = (NR + NM - 1) / NM;  // reads issued after each MFMA of a step
   constexpr int CPR = BN / 8;  // NN: 16-byte chunks per staged k-row
   static_assert(!NN || (BN % 128 == 0 ? CPR % 16 == 0 : CPR % 8 == 0), "NN chunk swizzle range");
-  static_assert(BM % (16 * W) == 0, "copy jj holds X rows iff jj < BM / (16 W)");
+  static_assert(BM % 16 == 0, "copies hold X rows or Y rows, not both");
   // MFMAs of the second step issued before the barrier: one keeps the
   // matrix pipeline busy while the barrier resolves, and leaves the rest of
   // the step to hide the next slice's reads (measured: 2-4% faster than
@@ -993,12 +998,31 @@ __global__ __launch_bounds__(64 * WM * WN) void k_ns_gemm_dmap(const GemmDesc* _
   const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(d.X), 0, xbytes, kBufferWord3);
   const __amdgpu_buffer_rsrc_t yr = __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(d.Y), 0, ybytes, kBufferWord3);
 
+  // cu[jj]: which of the slice's RG copies copy jj is (wave-uniform);
   // chunk[jj]: K chunk of an X (or NT Y) row; NN Y: the k-row in the slice.
-  int voff[LPW], chunk[LPW];
+  // holds_x(jj): copy jj holds X rows.  With 4 waves (every copy index
+  // jj is all X or all Y) the tests are the ones the kernel has always
+  // used; with 8 the W copies of one index may straddle the X / Y boundary,
+  // and the test is then made per wave.
+  constexpr int XG = BM / 16;  // copies of X rows per slice
+  constexpr bool EVEN = RG % W == 0;
+  static_assert(W == 8 || (W == 4 && EVEN && BM % (16 * W) == 0), "4-wave copy layout");
+  int voff[LPW], chunk[LPW], cu[LPW];
+  auto holds_x = [&](int jj) {
+    if constexpr (W == 4) {
+      return NN ? jj < BM / 64 : wave + 4 * jj < BM / 16;
+    } else {
+      const int lo = (!EVEN && jj == LPW - 1) ? W * (jj - 1) : W * jj;  // lowest copy index
+      if (W * jj + W <= XG) return true;
+      if (lo >= XG) return false;
+      return cu[jj] < XG;
+    }
+  };
 #pragma unroll
   for (int jj = 0; jj < LPW; ++jj) {
-    const int u = wave + W * jj;
-    if (NN && jj >= BM / (16 * W)) {  // Y slice copy (u >= BM / 16)
+    const int u = (EVEN || wave + W * jj < RG) ? wave + W * jj : wave + W * (jj - 1);
+    cu[jj] = u;
+    if (NN && !holds_x(jj)) {  // Y slice copy
       const int q = 64 * (u - BM / 16) + lane, kr = q / CPR;
       const int cn = (q - kr * CPR) ^ nn_swz<BN>(kr);
       chunk[jj] = kr;
@@ -1017,9 +1041,9 @@ __global__ __launch_bounds__(64 * WM * WN) void k_ns_gemm_dmap(const GemmDesc* _
   auto copy = [&](int kt, int jj) {
     unsigned char* base = lds + (kt % NS) * G::STAGE;
     const int k0 = kt * 32;
-    lds_void_t* dst = (lds_void_t*)(base + (wave + W * jj) * 1024);
+    lds_void_t* dst = (lds_void_t*)(base + (W == 4 ? wave + 4 * jj : cu[jj]) * 1024);
     if constexpr (NN) {
-      if (jj < BM / (16 * W)) {  // X rows (wave + W jj < BM / 16 for every wave)
+      if (holds_x(jj)) {  // uniform: X rows
         const bool kin = kt < ke && k0 + 8 * chunk[jj] < d.K;
         dma16(xr, dst, kin ? voff[jj] : xbytes, k0 * ES);
       } else {
@@ -1028,7 +1052,7 @@ __global__ __launch_bounds__(64 * WM * WN) void k_ns_gemm_dmap(const GemmDesc* _
       }
     } else {
       const bool kin = kt < ke && k0 + 8 * chunk[jj] < d.K;
-      if (wave + W * jj < BM / 16)  // uniform: X rows
+      if (holds_x(jj))  // uniform: X rows
         dma16(xr, dst, kin ? voff[jj] : xbytes, k0 * ES);
       else
         dma16(yr, dst, kin ? voff[jj] : ybytes, k0 * ES);
@@ -1481,6 +1505,8 @@ hipError_t launch_ns_gemm(DType ns_t, int variant, bool nn, int n_tiles, const G
       case kGemmDmaP256x192:
       case kGemmDmaP192x192:
       case kGemmDmaP256x256W8:
+      case kGemmDmaP192x256W8:
+      case kGemmDmaP256x192W8:
         if constexpr (std::is_same<TN, bf16>::value) {
 #define MUONBP_DMAP(BM_, BN_, WM_, WN_)                                                        \
   if (nn)                                                                                      \
@@ -1496,6 +1522,8 @@ hipError_t launch_ns_gemm(DType ns_t, int variant, bool nn, int n_tiles, const G
             case kGemmDmaP192x256: MUONBP_DMAP(192, 256, 2, 2); break;
             case kGemmDmaP256x192: MUONBP_DMAP(256, 192, 2, 2); break;
             case kGemmDmaP256x256W8: MUONBP_DMAP(256, 256, 2, 4); break;
+            case kGemmDmaP192x256W8: MUONBP_DMAP(192, 256, 2, 4); break;
+            case kGemmDmaP256x192W8: MUONBP_DMAP(256, 192, 4, 2); break;
             default: MUONBP_DMAP(192, 192, 2, 2); break;
           }
 #undef MUONBP_DMAP

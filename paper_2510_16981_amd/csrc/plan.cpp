@@ -186,11 +186,13 @@ int32_t choose_variant(const std::vector<Problem>& probs, GemmKind kind, int til
     // Symmetric products take square tiles; without the DMA path, the
     // register K loop on the same (or, for 192-wide tiles, the nearest) shape.
     if (sym && kGemmTileRows[v] != kGemmTileCols[v]) {
-      static const int32_t square[kNumGemmVariants] = {0, 0, 2, 3, 3, 5, 6, 7, 7, 9, 12, 12, 12, 13};
+      static const int32_t square[kNumGemmVariants] = {0, 0, 2, 3, 3, 5, 6, 7, 7, 9, 12, 12, 12, 13,
+                                                        12, 12};
       v = square[v];
     }
     if (kGemmIsDma[v] && !dma) {
-      static const int32_t twin[kNumGemmVariants] = {0, 1, 2, 0, 1, 2, 6, 0, 1, 2, 2, 2, 0, 2};
+      static const int32_t twin[kNumGemmVariants] = {0, 1, 2, 0, 1, 2, 6, 0, 1, 2, 2, 2, 0, 2,
+                                                      2, 2};
       v = twin[v];
     }
     return v;
@@ -204,6 +206,10 @@ int32_t choose_variant(const std::vector<Problem>& probs, GemmKind kind, int til
   if (dma) {
     // 256 x 256 tiles run on the 8-wave kernel (two waves per SIMD): 4-19%
     // faster than the 4-wave one on every measured launch, never slower.
+    // The 8-wave 192 x 256 / 256 x 192 kernels (tile policies only) are
+    // 5-6% faster per launch, but on the 2048 x 6144 benchmark the Gram and
+    // A.A launches that follow them ran 3-7% slower, and the step did not
+    // gain.
     static const int32_t sym_cands[] = {kGemmDmaP128x128, kGemmDmaP192x192, kGemmDmaP256x256W8};
     static const int32_t gen_cands[] = {kGemmDmaP128x128, kGemmDmaP256x128, kGemmDmaP192x256,
                                         kGemmDmaP256x192, kGemmDmaP256x256W8};

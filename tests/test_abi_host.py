@@ -90,7 +90,7 @@ def test_create_rejects_bad_arguments_before_gpu(lib):
     bad = mb.options_default(coeffs=[(2.0, -1.5, 0.5)])
     bad.coeff_table[1] = float("nan")
     assert _create(lib, [(8, 8, 1, 1)], opt=bad)[0] == 1
-    assert _create(lib, [(8, 8, 1, 1)], opt=mb.options_default(tile_policy=15))[0] == 1
+    assert _create(lib, [(8, 8, 1, 1)], opt=mb.options_default(tile_policy=17))[0] == 1
     assert _create(lib, [(8, 8, 1, 1)], opt=mb.options_default(stream_hint=3))[0] == 1
     assert _create(lib, [(8, 8, 1, 1)], opt=mb.options_default(stream_hint=-1))[0] == 1
     assert _create(lib, [(8, 8, 1, 1)], opt=mb.options_default(apply_mode=2))[0] == 1
@@ -156,7 +156,7 @@ def test_describe_plan_qkv_numbers(lib):
     (1, (128, 128), 128), (2, (256, 128), 128), (3, (256, 256), 256), (4, (128, 128), 128),
     (5, (256, 128), 128), (6, (256, 256), 256), (7, (128, 128), 128), (8, (128, 128), 128),
     (9, (256, 128), 128), (10, (256, 256), 256), (11, (192, 256), 192), (12, (256, 192), 192),
-    (13, (192, 192), 192), (14, (256, 256), 256)])
+    (13, (192, 192), 192), (14, (256, 256), 256), (15, (192, 256), 192), (16, (256, 192), 192)])
 def test_tile_policy_forces_shape(lib, policy, shape, square):
     """A forced tile shape reaches the apply product; the symmetric products
     take the nearest square shape."""

@@ -93,11 +93,11 @@ def test_ragged_shapes_fp32(mats):
 BIG_RAGGED = [(520, 1000, 1, 2), (1000, 264, 2, 1), (300, 300, 1, 1)]
 
 
-@pytest.mark.parametrize("policy", [1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11, 12, 13, 14],
+@pytest.mark.parametrize("policy", [1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11, 12, 13, 14, 15, 16],
                          ids=["128x128", "256x128", "256x256", "dma128x128", "dma256x128",
                               "dma256x256", "128x128split2", "dmap128x128", "dmap256x128",
                               "dmap256x256", "dmap192x256", "dmap256x192", "dmap192x192",
-                              "dmap256x256w8"])
+                              "dmap256x256w8", "dmap192x256w8", "dmap256x192w8"])
 @pytest.mark.parametrize("ns", ["bf16", "f32"])
 def test_every_tile_shape(policy, ns):
     """Each NS GEMM kernel, forced, on units spanning several tiles with
@@ -117,9 +117,10 @@ ALIGNED = [(264, 1040, 1, 2), (1040, 264, 2, 1), (296, 296, 1, 1), (136, 2048, 1
 
 
 @pytest.mark.parametrize("ksplit", [0, 2, 3, 8])
-@pytest.mark.parametrize("policy", [8, 9, 10, 11, 12, 13, 14],
+@pytest.mark.parametrize("policy", [8, 9, 10, 11, 12, 13, 14, 15, 16],
                          ids=["dmap128x128", "dmap256x128", "dmap256x256", "dmap192x256",
-                              "dmap256x192", "dmap192x192", "dmap256x256w8"])
+                              "dmap256x192", "dmap192x192", "dmap256x256w8", "dmap192x256w8",
+                              "dmap256x192w8"])
 def test_dma_pipeline_and_k_split(policy, ksplit):
     """The interleaved DMA kernels, with each tile's K loop shared by 2..8
     workgroups (0 = not split).  With 8, the 136-row units' A.A and apply
@@ -129,9 +130,10 @@ def test_dma_pipeline_and_k_split(policy, ksplit):
     _check(res, BF16_TOL)
 
 
-@pytest.mark.parametrize("policy", [8, 9, 10, 11, 12, 13, 14],
+@pytest.mark.parametrize("policy", [8, 9, 10, 11, 12, 13, 14, 15, 16],
                          ids=["dmap128x128", "dmap256x128", "dmap256x256", "dmap192x256",
-                              "dmap256x192", "dmap192x192", "dmap256x256w8"])
+                              "dmap256x192", "dmap192x192", "dmap256x256w8", "dmap192x256w8",
+                              "dmap256x192w8"])
 def test_apply_with_transposed_copy(policy):
     """apply_mode 1: the interleaved DMA kernels read Z^T for the apply (the
     layout every other kernel uses) instead of Z through transpose reads."""
