@@ -140,7 +140,14 @@ muonbp_status muonbp_create(const muonbp_matrix* mats, int32_t n_mats,
  *  step    t >= 0.  Full step iff period > 0 and step % period == 0.
  * Enqueues: momentum (+ per-segment sum of squares), per-unit scale,
  * operand pack, K x (Gram, polynomial, apply) grouped MFMA launches, update.
- * Errors: E_INVALID (NULL ctx/arrays/pointers, step < 0), E_STATE, E_HIP. */
+ * The step may be captured into a HIP graph on the context's stream when
+ * profiling is off and the pointers equal those of the step before (their
+ * device table is then not re-uploaded); a replay repeats the captured step
+ * kind, learning rates and options, and reads the params and grads in
+ * place.
+ * Errors: E_INVALID (NULL ctx/arrays/pointers, step < 0), E_STATE (also:
+ * new pointers or profiling while the stream captures; nothing enqueued),
+ * E_HIP. */
 muonbp_status muonbp_step(muonbp_ctx* ctx, void* const* params,
                           const void* const* grads, int64_t step);
 

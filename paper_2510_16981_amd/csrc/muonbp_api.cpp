@@ -530,7 +530,16 @@ muonbp_status muonbp_step(muonbp_ctx* c, void* const* params, const void* const*
     aligned = aligned && reinterpret_cast<uintptr_t>(params[i]) % 16 == 0 &&
               reinterpret_cast<uintptr_t>(grads[i]) % 16 == 0;
   }
+  if (c->prof != 0) {  // the profiling events cannot be part of a graph
+    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(c->stream, &cap) == hipSuccess && cap != hipStreamCaptureStatusNone)
+      return fail(c, MUONBP_E_STATE, "profiling is enabled while the stream captures a graph");
+  }
   hipError_t e = c->ptrs.stage(params, grads, c->stream);
+  if (e == hipErrorStreamCaptureUnsupported)  // nothing enqueued: the context stays usable
+    return fail(c, MUONBP_E_STATE,
+                "param / grad pointers differ from the previous step's while the stream captures a "
+                "graph; run one step with these pointers before capturing");
   if (e != hipSuccess) return hip_fail(c, e, "pointer upload");
   const MatPtrs* mats = c->ptrs.current();
 

@@ -53,13 +53,19 @@ struct PtrRing {
   // change of stream.
   void invalidate() { valid = false; }
 
-  // Make the table of this step current on stream s.
+  // Make the table of this step current on stream s.  Refused while s is
+  // capturing a graph: the graph would record a copy from a pinned slot
+  // that later uploads rewrite (a captured step must reuse the table of the
+  // step before it).
   hipError_t stage(void* const* params, const void* const* grads, hipStream_t s) {
     bool same = valid;
     for (size_t i = 0; same && i < n; ++i) same = last[i].param == params[i] && last[i].grad == grads[i];
     if (same) return hipSuccess;
-    const int next = (slot + 1) % kSlots;
     hipError_t e;
+    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+    if ((e = hipStreamIsCapturing(s, &cap)) != hipSuccess) return e;
+    if (cap != hipStreamCaptureStatusNone) return hipErrorStreamCaptureUnsupported;
+    const int next = (slot + 1) % kSlots;
     if (ev_used[next] && (e = hipEventSynchronize(ev[next])) != hipSuccess) return e;
     for (size_t i = 0; i < n; ++i) host[next][i] = MatPtrs{params[i], grads[i]};
     if ((e = hipMemcpyAsync(dev[next], host[next], n * sizeof(MatPtrs), hipMemcpyHostToDevice, s)) !=

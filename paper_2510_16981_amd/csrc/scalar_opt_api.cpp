@@ -189,6 +189,9 @@ muonbp_status muonbp_adamw_step(muonbp_adamw_ctx* c, void* const* params, const 
     aligned = aligned && a % 16 == 0 && b % 16 == 0;
   }
   hipError_t e = c->ptrs.stage(params, grads, c->stream);
+  if (e == hipErrorStreamCaptureUnsupported)  // nothing enqueued: the context stays usable
+    return fail(c, MUONBP_E_STATE,
+                "param / grad pointers differ from the previous step's while the stream captures a graph");
   if (e != hipSuccess) return hip_fail(c, e, "pointer upload");
   const DType tp = c->opt.param_dtype == MUONBP_F32 ? DType::F32 : DType::BF16;
   const bool clipping = c->opt.max_grad_norm > 0.f;
