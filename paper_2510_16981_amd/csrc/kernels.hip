@@ -923,7 +923,10 @@ __global__ __launch_bounds__(kThreads) void k_ns_gemm_dma(const GemmDesc* __rest
 //
 // Slices past K are copied too (as zeros, through an out-of-range offset),
 // so the loop has no branches and every wait is a constant count.
-
+//
+// Waves: WM x WN, row-major; 2 x 2 (one wave per SIMD), or 8 waves as
+// 2 x 4 / 4 x 2 so that each SIMD holds two waves whose MFMAs cover each
+// other's waits (the sub-tile then needs half the accumulator registers).
 //
 // K split (nsplit > 1): the workgroups of one tile each run about 1/nsplit
 // of its K slices (share t.part), store their fp32 sums at
