@@ -91,7 +91,10 @@ typedef struct {
   int32_t k_split;          /* interleaved DMA kernels only: 1..8 = each
                                tile's K loop shared by that many workgroups
                                (fp32 partial sums added by the last one to
-                               finish); 0 = no split. */
+                               finish); 1 = no split; 0 = the planner's
+                               choice (3 for a launch with fewer tiles than
+                               0.6 x the CUs and at least 128 K slices in
+                               every product, else none). */
   int32_t coeff_count;      /* 0 = every NS iteration uses (a, b, c) above;
                                1..MUONBP_MAX_COEFFS = iteration k uses
                                coeff_table[min(k, coeff_count - 1)] (tuned or

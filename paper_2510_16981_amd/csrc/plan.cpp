@@ -239,11 +239,22 @@ int32_t choose_variant(const std::vector<Problem>& probs, GemmKind kind, int til
 // per-XCD caches, and on MI355X that traffic (a full fp32 tile per share)
 // cost more than the extra CUs gained on every launch measured (the 2048 x
 // 6144 shards' Gram: 35 us split 3 ways against 27 us unsplit).
+// With k_split = 0 the planner splits 3 ways only a launch that leaves
+// most CUs idle and has a long K loop everywhere (fewer tiles than 0.6 x
+// the CUs, at least 128 K slices per product): there the extra CUs win
+// over the partial-sum traffic (the whole 2048 x 6144 matrix's Gram, 136
+// tiles at K = 6144: 56 against 60 us a launch).
 int32_t choose_split(const std::vector<Problem>& probs, GemmKind kind, int32_t v, int k_split) {
-  (void)probs;
-  (void)kind;
   if (!gemm_is_dmap(v)) return 1;
-  return k_split > 0 ? k_split : 1;
+  if (k_split > 0) return k_split;
+  const int64_t tiles = count_tiles(probs, kind, v);
+  if (tiles == 0 || 10 * tiles > 6 * kNumCUs) return 1;
+  for (const Problem& p : probs) {
+    int64_t m, c, k;
+    gemm_dims(p, kind, &m, &c, &k);
+    if (ceil_div(k, 32) < 128) return 1;
+  }
+  return 3;
 }
 
 double ns_unit_flops(int64_t S, int64_t L, int K) {
