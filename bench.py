@@ -1,18 +1,21 @@
 """Benchmark of the MuonBP optimizer step on one MI355X.
 
-Default workload (the one the metric is quoted on): one fused attention QKV
-weight, 2048 x 6144 bf16 (params, grads, momentum and NS operands), cut into
-8 column shards of 2048 x 768 (the 8-way tensor-parallel shard shape),
-rank-128 synthetic gradients, K = 5 Newton-Schulz iterations, period P = 5
-(steps t = 0, 5, 10, ... are full).  Other workloads (--workload) are the
-larger shapes of the same method: a 16-layer d=2048 model, the 32-layer
-8B-shaped model (with a period sweep) and the 4096 x 14336 MLP matrices.
+Default workload: every 2D weight of a 32-layer model with the shapes of the
+paper's 8B Llama-style model (Table 5: d = 4096, ffn = 14336, GQA kv width
+1024), bf16 params, grads, momentum and NS operands, each matrix cut into
+the 8-way Megatron shard grid (column shards 1 x 8 for q, k, v, gate, up;
+row shards 8 x 1 for o, down), rank-128 synthetic gradients, K = 5
+Newton-Schulz iterations, period P = 5 (steps t = 0, 5, 10, ... are full).
+This is the largest configuration that fits one GPU (6.98 B parameters).
+Other workloads (--workload) are smaller shapes of the same method: one
+2048 x 6144 QKV weight in 8 column shards, a 16-layer d=2048 model and the
+4096 x 14336 MLP matrices.
 
 A step is one whole optimizer step: momentum, norms, NS (blockwise or full)
 and the weight update, all in the HIP library.  Inputs are resident in HBM
 before timing starts.  Printed: ONE JSON line.
 
-    python bench.py [--gpus 1] [--steps 100] [--warmup 5] [--workload NAME]
+    python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--workload NAME]
                     [--period P] [--no-cpu-baseline]
 
 Counter support (the roofline's `traffic` and MFMA utilisation):
@@ -35,7 +38,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
-DEFAULT_WORKLOAD = "qkv-2048x6144-bf16"
+DEFAULT_WORKLOAD = "llama-32L-d4096-bf16"
 METRIC = "optimizer steps/sec and NS TFLOP/s (% of bf16 MFMA peak), block vs full"
 BF16_PEAK_TFLOPS = 2500.0   # MI355X dense bf16 MFMA, published
 HBM_PEAK_GBS = 8000.0       # MI355X HBM3E, published
@@ -66,10 +69,14 @@ def plan_flops(mats, full, K):
     return tot
 
 
+def _oracle_threads():
+    from threadpoolctl import threadpool_info
+    return int(max([i.get("num_threads", 1) for i in threadpool_info()] or [1]))
+
+
 def cpu_baseline(workload, mats, period, rank, sample_steps):
     """The fp64 oracle on the host cores over `sample_steps` steps of the
     workload (from t = 0, so the sample holds full and block steps)."""
-    from threadpoolctl import threadpool_info
     from oracle import muonbp_oracle as O
     from paper_2510_16981_amd import workload as W
 
@@ -85,12 +92,73 @@ def cpu_baseline(workload, mats, period, rank, sample_steps):
     for t in range(sample_steps):
         X = orc.step(X, Gs[t], t)
     dt = time.perf_counter() - t0
-    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     nf = sum(1 for t in range(sample_steps) if period and t % period == 0)
-    return {"value": sample_steps / dt, "unit": "steps/s", "cores": int(threads),
+    return {"value": sample_steps / dt, "unit": "steps/s", "cores": _oracle_threads(),
             "kind": "oracle",
             "sample": f"{sample_steps} consecutive steps (t=0..{sample_steps - 1}: {nf} full, "
                       f"{sample_steps - nf} blockwise) of {workload}, numpy float64, {dt:.1f} s",
+            "host_cpus": len(os.sched_getaffinity(0)), "cpu": platform.processor() or platform.machine()}
+
+
+def _time_oracle_step(O, W, spec, t, period, rank, lr_block, min_s=0.5):
+    """Seconds of one MuonBPOracle.step (momentum, NS, update) on one
+    matrix, repeated until min_s has passed (small units), averaged."""
+    orc = O.MuonBPOracle([spec], O.OracleConfig(period=period, lr_block=lr_block,
+                                                lr_full=LR_FULL, momentum=MU, weight_decay=WD))
+    X = [W.quantize(W.init_param(spec.rows, spec.cols, 0, 0), "bf16").double().numpy()]
+    G = [W.quantize(W.lowrank_grad(spec.rows, spec.cols, rank, 0, 0, t), "bf16").double().numpy()]
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        orc.step(X, G, t)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= min_s:
+            return el / reps
+
+
+def cpu_baseline_sampled(workload, mats, period, rank):
+    """The fp64 oracle on a bounded sample of a workload too large to run
+    whole on the host (a full step of the 8B-shaped model is about 666
+    TFLOP), scaled to the whole step.  Sample: for every distinct block
+    shape, one block run through MuonBPOracle.step as a matrix of its own on
+    a block step; for every distinct NS problem of the full plan (S x L,
+    S = the smaller side; a tall matrix shares the problem of its transpose),
+    one whole matrix through MuonBPOracle.step on a full step.  Each timing
+    covers the oracle's momentum, NS and update of that unit.  Block step =
+    sum over blocks, full step = sum over matrices; steps/s is averaged over
+    the period as P / (t_full + (P - 1) t_block).  Labelled extrapolated."""
+    from oracle import muonbp_oracle as O
+    from paper_2510_16981_amd import workload as W
+
+    gr0, gc0 = mats[0][2], mats[0][3]
+    lr_block = LR_FULL / (gr0 * gc0) ** 0.5
+    t_all = time.perf_counter()
+    block_t, full_t = {}, {}
+    for r, c, gr, gc in mats:
+        b = (r // gr, c // gc)
+        if b not in block_t:
+            block_t[b] = _time_oracle_step(O, W, O.MatrixSpec(b[0], b[1], 1, 1), 1, 0, rank, lr_block)
+        f = (min(r, c), max(r, c))
+        if f not in full_t:
+            # one run of a large matrix is long enough on its own
+            full_t[f] = _time_oracle_step(O, W, O.MatrixSpec(r, c, gr, gc), 0, 1, rank, lr_block,
+                                          min_s=0.0)
+    sample_s = time.perf_counter() - t_all
+    t_block = sum(block_t[(r // gr, c // gc)] * gr * gc for r, c, gr, gc in mats)
+    t_full = sum(full_t[(min(r, c), max(r, c))] for r, c, _, _ in mats)
+    P = max(period, 1)
+    value = P / (t_full + (P - 1) * t_block) if period else 1.0 / t_block
+    blocks = ", ".join(f"{a}x{b}" for a, b in block_t)
+    fulls = ", ".join(f"{a}x{b}" for a, b in full_t)
+    return {"value": value, "unit": "steps/s", "cores": _oracle_threads(), "kind": "oracle",
+            "extrapolated": True,
+            "sample": f"{workload}: one block of each distinct block shape ({blocks}) on a block "
+                      f"step and one whole matrix of each distinct full-step NS problem S x L "
+                      f"({fulls}) on a full step, each through MuonBPOracle.step (numpy float64), "
+                      f"{sample_s:.1f} s in all; scaled by the workload's block and matrix counts "
+                      f"to t_block {t_block:.1f} s and t_full {t_full:.1f} s per step, then "
+                      f"P / (t_full + (P - 1) t_block) at P = {period} (extrapolated)",
+            "t_block_step_s": t_block, "t_full_step_s": t_full,
             "host_cpus": len(os.sched_getaffinity(0)), "cpu": platform.processor() or platform.machine()}
 
 
@@ -652,8 +720,8 @@ def main():
     mats = W.workload_matrices(name)
     n_el = sum(r * c for r, c, _, _ in mats)
     large = n_el > HOST_INPUT_LIMIT
-    steps = args.steps if args.steps is not None else (5 if large else 100)
-    warmup = args.warmup if args.warmup is not None else (2 if large else 5)
+    steps = args.steps if args.steps is not None else (20 if large else 100)
+    warmup = args.warmup if args.warmup is not None else 5
     period = args.period if args.period is not None else wl["period"]
     rank = wl["rank"]
     gr, gc = mats[0][2], mats[0][3]
@@ -806,9 +874,12 @@ def main():
     if not args.no_scalar:
         log("scalar optimizer (AdamW) pass")
         out["scalar_optimizer"] = scalar_optimizer_bench()
-    if not args.no_cpu_baseline and not large:
+    if not args.no_cpu_baseline:
         log("cpu baseline (oracle)")
-        out["cpu_baseline"] = cpu_baseline(name, mats, period, rank, 3 * max(period, 1))
+        if large:
+            out["cpu_baseline"] = cpu_baseline_sampled(name, mats, period, rank)
+        else:
+            out["cpu_baseline"] = cpu_baseline(name, mats, period, rank, 3 * max(period, 1))
     print(json.dumps(out), flush=True)
 
 

@@ -39,7 +39,9 @@ typedef enum {
   MUONBP_E_DTYPE = 3,   /* unsupported dtype or dtype combination             */
   MUONBP_E_NOMEM = 4,   /* device or host allocation failed                   */
   MUONBP_E_HIP = 5,     /* a HIP runtime call or kernel launch failed         */
-  MUONBP_E_STATE = 6    /* context poisoned by an earlier MUONBP_E_HIP        */
+  MUONBP_E_STATE = 6,   /* context poisoned by an earlier MUONBP_E_HIP        */
+  MUONBP_E_NONFINITE = 7 /* muonbp_options.check_finite found NaN / Inf in an
+                            orthogonalization input (context stays usable)    */
 } muonbp_status;
 
 typedef enum { MUONBP_F32 = 0, MUONBP_BF16 = 1 } muonbp_dtype;
@@ -112,6 +114,16 @@ typedef struct {
                                transpose reads wherever the interleaved DMA
                                kernel runs it (no Z^T kept between
                                iterations); 1 = keeps Z^T and reads it. */
+  int32_t check_finite;     /* debug check, off by default (0).  1: after the
+                               momentum update, muonbp_step waits for the
+                               stream and returns MUONBP_E_NONFINITE when the
+                               NS input of some unit (M, or G + mu M with
+                               Nesterov) holds a NaN or an Inf, or its sum of
+                               squares overflows fp32; nothing after the
+                               momentum is enqueued then (params and U keep
+                               their values, M holds this step's update).
+                               Off: NaN / Inf propagate silently into U and
+                               the params of their unit. */
 } muonbp_options;
 
 /* Fill *opt with the defaults above.  NULL is ignored. */
@@ -128,7 +140,12 @@ void muonbp_options_default(muonbp_options* opt);
  *  hip_stream  hipStream_t to enqueue on (NULL = the null stream).
  *  out         receives the context; *out is NULL on error.
  * Allocates the momentum buffers (zeroed, Algorithm 1's M_{-1} = 0), the NS
- * workspace and the plan tables on the current device; enqueues no compute.
+ * workspace and the plan tables on the current device; the zeroing and the
+ * table uploads run on hip_stream, which the call waits for (no device-wide
+ * synchronisation).
+ * E_SHAPE also when an orthogonalization unit of either plan (a block, or a
+ * whole matrix) needs an NS operand of 2^31 bytes or more (e.g. a 40000 x
+ * 40000 bf16 matrix): the kernels address operands with 32-bit offsets.
  * Errors: E_INVALID, E_SHAPE, E_DTYPE (before any HIP call), E_NOMEM, E_HIP. */
 muonbp_status muonbp_create(const muonbp_matrix* mats, int32_t n_mats,
                             int64_t period, float lr_block, float lr_full,
@@ -148,9 +165,13 @@ muonbp_status muonbp_create(const muonbp_matrix* mats, int32_t n_mats,
  * device table is then not re-uploaded); a replay repeats the captured step
  * kind, learning rates and options, and reads the params and grads in
  * place.
+ * A step captured into a graph keeps using the device copy of its pointer
+ * table: later eager steps with other pointers upload theirs elsewhere, so
+ * a replay still reads and updates the captured step's tensors.
  * Errors: E_INVALID (NULL ctx/arrays/pointers, step < 0), E_STATE (also:
- * new pointers or profiling while the stream captures; nothing enqueued),
- * E_HIP. */
+ * new pointers, profiling or check_finite while the stream captures;
+ * nothing enqueued), E_NONFINITE (check_finite only: momentum updated,
+ * nothing else enqueued; the context stays usable), E_HIP. */
 muonbp_status muonbp_step(muonbp_ctx* ctx, void* const* params,
                           const void* const* grads, int64_t step);
 

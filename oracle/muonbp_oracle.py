@@ -76,10 +76,16 @@ def orthogonalize_via_ns(G, K: int = 5, eps: float = NS_EPS,
                          transpose_tall: bool = True) -> np.ndarray:
     """Algorithm 2 (Orthogonalize-via-NS), in fp64.
 
-    X <- G / (||G||_F + eps); K times: A <- X X^T, B <- b A + c A^2,
-    X <- a X + B X, with iteration k's (a, b, c) from ``ns_coefficients``.
-    With ``transpose_tall`` the iteration runs on G^T when G has more rows
-    than columns and the result is transposed back.
+    The input is scaled to unit Frobenius norm (plus eps), which puts every
+    singular value in [0, 1].  Each of the K iterations then maps every
+    singular value x to the odd quintic p_k(x) = a_k x + b_k x^3 + c_k x^5
+    and keeps the singular vectors.  As a matrix function on the left Gram
+    matrix, whose eigenvalues are the squared singular values, that is
+    X <- q_k(X X^T) X with q_k(lam) = a_k + b_k lam + c_k lam^2, evaluated
+    here in Horner form.  Iteration k's (a_k, b_k, c_k) come from
+    ``ns_coefficients``.  With ``transpose_tall`` the iteration runs on G^T
+    when G has more rows than columns and the result is transposed back
+    (the same matrix function, on the smaller Gram matrix).
     """
     table = ns_coefficients(coeffs, K)
     G = np.asarray(G, dtype=np.float64)
@@ -89,10 +95,11 @@ def orthogonalize_via_ns(G, K: int = 5, eps: float = NS_EPS,
     if transposed:
         G = G.T
     X = G / (np.linalg.norm(G, "fro") + eps)
+    eye = np.eye(X.shape[0])
     for a, b, c in table:
-        A = X @ X.T
-        B = b * A + c * (A @ A)
-        X = a * X + B @ X
+        gram = X @ X.T
+        q = a * eye + gram @ (b * eye + c * gram)  # q_k(X X^T)
+        X = q @ X
     return X.T.copy() if transposed else X
 
 

@@ -16,6 +16,10 @@ hipError_t launch_momentum(DType grad_t, DType mom_t, bool vec, bool nt, int n_s
                            const MatPtrs* mats, void* mom, float mu,
                            int nesterov, float* partials, hipStream_t s);
 
+// flag[0] = 1 if any of partials[0 .. n) is NaN or Inf, else 0 (one
+// workgroup; the debug check of muonbp_options.check_finite).
+hipError_t launch_check_finite(int n, const float* partials, int* flag, hipStream_t s);
+
 // scales[p] = 1 / (sqrt(sum of its partials) + eps)  (Algorithm 2, first line).
 hipError_t launch_scale(int n_probs, const ScaleDesc* sd, const float* partials,
                         float* scales, float eps, hipStream_t s);

@@ -204,6 +204,26 @@ __global__ __launch_bounds__(kThreads) void k_momentum(
   if (threadIdx.x == 0) partials[blockIdx.x] = acc;
 }
 
+// ---------------------------------------------------------------- finite check
+
+// flag[0] = 1 when some partial sum is NaN or Inf (a NaN or Inf anywhere in a
+// segment's NS input makes its sum of squares non-finite).  One workgroup,
+// so the flag is written once, by thread 0, with no atomics.
+__global__ __launch_bounds__(kThreads) void k_check_finite(const float* __restrict__ partials, int n,
+                                                           int* __restrict__ flag) {
+  __shared__ int any[kThreads / 64];
+  int bad = 0;
+  for (int i = threadIdx.x; i < n; i += kThreads) bad |= !isfinite(partials[i]);
+  bad = __any(bad) ? 1 : 0;
+  if ((threadIdx.x & 63) == 0) any[threadIdx.x >> 6] = bad;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int f = 0;
+    for (int w = 0; w < kThreads / 64; ++w) f |= any[w];
+    flag[0] = f;
+  }
+}
+
 // ---------------------------------------------------------------- scale
 
 __global__ __launch_bounds__(64) void k_scale(const ScaleDesc* __restrict__ sd,
@@ -1441,6 +1461,11 @@ hipError_t launch_momentum(DType grad_t, DType mom_t, bool vec, bool nt, int n_s
       return hipGetLastError();
     });
   });
+}
+
+hipError_t launch_check_finite(int n, const float* partials, int* flag, hipStream_t s) {
+  hipLaunchKernelGGL(k_check_finite, dim3(1), dim3(kThreads), 0, s, partials, n, flag);
+  return hipGetLastError();
 }
 
 hipError_t launch_scale(int n_probs, const ScaleDesc* sd, const float* partials, float* scales,

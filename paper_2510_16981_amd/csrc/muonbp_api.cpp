@@ -60,6 +60,8 @@ struct muonbp_ctx {
   float* scales = nullptr;
   float* ksum = nullptr;   // fp32 partial sums of K-split NS GEMM launches
   int* kcount = nullptr;   // one arrival counter per tile of such a launch (kept zeroed)
+  int* finite_flag = nullptr;       // check_finite: 1 when a partial sum is not finite
+  int* finite_host = nullptr;       // pinned copy of it
   SegDesc* segs = nullptr;
   BlockDesc* blocks = nullptr;
   PlanDev pd[2];
@@ -124,11 +126,15 @@ std::string validate_opts(const muonbp_options& o) {
   if (o.coeff_count < 0 || o.coeff_count > MUONBP_MAX_COEFFS) return "coeff_count out of range";
   if (o.stream_hint < 0 || o.stream_hint > 2) return "stream_hint out of range";
   if (o.apply_mode < 0 || o.apply_mode > 1) return "apply_mode out of range";
+  if (o.check_finite != 0 && o.check_finite != 1) return "check_finite must be 0 or 1";
   for (int i = 0; i < 3 * o.coeff_count; ++i)
     if (!std::isfinite(o.coeff_table[i])) return "coefficients must be finite";
   return "";
 }
 
+// Copies a host table into new device memory on the context's stream and
+// waits for that stream only (no device-wide synchronisation, which would
+// also wait for, or break a graph capture on, the caller's other streams).
 template <typename T>
 hipError_t upload(muonbp_ctx* c, T** dst, const std::vector<T>& src) {
   *dst = nullptr;
@@ -138,7 +144,9 @@ hipError_t upload(muonbp_ctx* c, T** dst, const std::vector<T>& src) {
   if (e != hipSuccess) return e;
   c->allocs.push_back(p);
   *dst = static_cast<T*>(p);
-  return hipMemcpy(p, src.data(), src.size() * sizeof(T), hipMemcpyHostToDevice);
+  e = hipMemcpyAsync(p, src.data(), src.size() * sizeof(T), hipMemcpyHostToDevice, c->stream);
+  if (e != hipSuccess) return e;
+  return hipStreamSynchronize(c->stream);
 }
 
 hipError_t dev_alloc(muonbp_ctx* c, void** p, size_t bytes) {
@@ -181,17 +189,20 @@ hipError_t build_plan_tables(muonbp_ctx* c, int full) {
     d.seg_begin = p.seg_begin;
     d.seg_end = p.seg_end;
     // Z = Y (S = rows) or Y^T (S = cols); Z^T the other way round, needed
-    // by the NT apply, or as U when there are no iterations.
-    const bool want_zt = !plan.nn_apply || o.ns_steps == 0;
+    // by the NT apply.  The apply that reads Z row-major needs Z only, and
+    // with no iterations the straight copy is U itself (in the matrix's
+    // orientation, where the update reads it).
+    const bool z_only = plan.nn_apply && o.ns_steps > 0;
+    const bool u_only = plan.nn_apply && o.ns_steps == 0;
     if (!p.trans) {
       d.dst_s = at(p.off_z[0]);
       d.ld_s = p.Lp;
-      d.dst_t = want_zt ? at(p.off_zt[0]) : nullptr;
+      d.dst_t = (z_only || u_only) ? nullptr : at(p.off_zt[0]);
       d.ld_t = p.Sp;
     } else {
-      d.dst_s = want_zt ? at(p.off_zt[0]) : nullptr;
+      d.dst_s = z_only ? nullptr : at(p.off_zt[0]);
       d.ld_s = p.Sp;
-      d.dst_t = at(p.off_z[0]);
+      d.dst_t = u_only ? nullptr : at(p.off_z[0]);
       d.ld_t = p.Lp;
     }
     pk.push_back(d);
@@ -260,6 +271,7 @@ void free_ctx(muonbp_ctx* c) {
     if (r.stop) (void)hipEventDestroy(r.stop);
   }
   for (hipEvent_t e : c->ev_pool) (void)hipEventDestroy(e);
+  if (c->finite_host) (void)hipHostFree(c->finite_host);
   delete c;
 }
 
@@ -353,6 +365,7 @@ const char* muonbp_status_string(muonbp_status s) {
     case MUONBP_E_NOMEM: return "out of memory";
     case MUONBP_E_HIP: return "HIP error";
     case MUONBP_E_STATE: return "context unusable after an earlier HIP error";
+    case MUONBP_E_NONFINITE: return "non-finite orthogonalization input";
   }
   return "unknown status";
 }
@@ -489,7 +502,8 @@ muonbp_status muonbp_create(const muonbp_matrix* mats, int32_t n_mats, int64_t p
     c->ksum = static_cast<float*>(p);
     if ((e = dev_alloc(c, &p, size_t(split_slots) * sizeof(int))) != hipSuccess) return bail(e, "split counters");
     c->kcount = static_cast<int*>(p);
-    if ((e = hipMemset(c->kcount, 0, size_t(split_slots) * sizeof(int))) != hipSuccess)
+    if ((e = hipMemsetAsync(c->kcount, 0, size_t(split_slots) * sizeof(int), c->stream)) !=
+        hipSuccess)
       return bail(e, "split counters");
   }
   if ((e = upload(c, &c->segs, c->lay.segs)) != hipSuccess) return bail(e, "segments");
@@ -508,9 +522,16 @@ muonbp_status muonbp_create(const muonbp_matrix* mats, int32_t n_mats, int64_t p
   for (int full = 0; full < 2; ++full)
     if ((e = build_plan_tables(c, full)) != hipSuccess) return bail(e, "plan tables");
   if ((e = c->ptrs.init(shapes.size())) != hipSuccess) return bail(e, "pointer tables");
+  if (o.check_finite) {
+    if ((e = dev_alloc(c, &p, sizeof(int))) != hipSuccess) return bail(e, "finite flag");
+    c->finite_flag = static_cast<int*>(p);
+    if ((e = hipHostMalloc(&p, sizeof(int), 0)) != hipSuccess) return bail(e, "finite flag");
+    c->finite_host = static_cast<int*>(p);
+  }
   // Algorithm 1: M_{-1} = 0.
-  if ((e = hipMemset(c->mom, 0, size_t(c->lay.total_elems) * sb)) != hipSuccess) return bail(e, "memset");
-  if ((e = hipDeviceSynchronize()) != hipSuccess) return bail(e, "sync");
+  if ((e = hipMemsetAsync(c->mom, 0, size_t(c->lay.total_elems) * sb, c->stream)) != hipSuccess)
+    return bail(e, "memset");
+  if ((e = hipStreamSynchronize(c->stream)) != hipSuccess) return bail(e, "sync");
   *out = c;
   return MUONBP_OK;
 }
@@ -530,10 +551,12 @@ muonbp_status muonbp_step(muonbp_ctx* c, void* const* params, const void* const*
     aligned = aligned && reinterpret_cast<uintptr_t>(params[i]) % 16 == 0 &&
               reinterpret_cast<uintptr_t>(grads[i]) % 16 == 0;
   }
-  if (c->prof != 0) {  // the profiling events cannot be part of a graph
+  if (c->prof != 0 || c->opt.check_finite) {
+    // Profiling events and the finite check's wait cannot be part of a graph.
     hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
     if (hipStreamIsCapturing(c->stream, &cap) == hipSuccess && cap != hipStreamCaptureStatusNone)
-      return fail(c, MUONBP_E_STATE, "profiling is enabled while the stream captures a graph");
+      return fail(c, MUONBP_E_STATE,
+                  "profiling or check_finite is enabled while the stream captures a graph");
   }
   hipError_t e = c->ptrs.stage(params, grads, c->stream);
   if (e == hipErrorStreamCaptureUnsupported)  // nothing enqueued: the context stays usable
@@ -558,6 +581,18 @@ muonbp_status muonbp_step(muonbp_ctx* c, void* const* params, const void* const*
                            c->mu, o.nesterov, c->partials, s);
   });
   if (e != hipSuccess) return hip_fail(c, e, "momentum");
+  if (o.check_finite) {
+    // Debug check: any non-finite per-segment sum of squares of the NS input.
+    if ((e = launch_check_finite(nsegs, c->partials, c->finite_flag, s)) != hipSuccess ||
+        (e = hipMemcpyAsync(c->finite_host, c->finite_flag, sizeof(int), hipMemcpyDeviceToHost, s)) !=
+            hipSuccess ||
+        (e = hipStreamSynchronize(s)) != hipSuccess)
+      return hip_fail(c, e, "finite check");
+    if (*c->finite_host != 0)
+      return fail(c, MUONBP_E_NONFINITE,
+                  "NaN or Inf in the orthogonalization input (momentum of this step) of some unit; "
+                  "params not updated");
+  }
   if (!pd.fuse_scale) {
     e = timed(c, 1, [&] {
       return launch_scale(int(plan.probs.size()), pd.scale, c->partials, c->scales, o.eps, s);

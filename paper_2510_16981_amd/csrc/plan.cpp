@@ -16,21 +16,42 @@ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 constexpr int64_t kMaxDim = int64_t(1) << 30;    // int32 leading dims stay valid
 constexpr int64_t kMaxTiles = int64_t(1) << 16;  // tile index packs in 16 bits
 
+// Byte offsets inside one NS operand are 32-bit in the GEMM kernels (buffer
+// descriptors and per-lane offsets), so no operand may reach 2^31 bytes.
+constexpr int64_t kMaxOperandBytes = int64_t(1) << 31;
+
 // Appends the workspace buffers of one problem; returns false on overflow.
-bool place_problem(Problem* p, int64_t* cursor, int64_t align_elems) {
+// nn (the apply reads Z row-major, so no Z^T is kept between iterations):
+// Z[0], Z[1], A, B, with each Z buffer large enough for either layout (S x
+// Lp or L x Sp); U of a transposed unit is written as Z^T into the buffer
+// the last apply would otherwise fill (off_zt aliases off_z).  Otherwise
+// (the transposed-copy apply, or the register-loop kernels): Z[2], Z^T[2],
+// A, B.
+bool place_problem(Problem* p, int64_t* cursor, int64_t align_elems, bool nn) {
   auto take = [&](int64_t n) {
     int64_t at = *cursor;
     *cursor = round_up(at + n, align_elems);
     return at;
   };
   const int64_t zs = p->S * p->Lp, zts = p->L * p->Sp, as = p->S * p->Sp;
-  p->off_z[0] = take(zs);
-  p->off_z[1] = take(zs);
-  p->off_zt[0] = take(zts);
-  p->off_zt[1] = take(zts);
+  if (nn) {
+    const int64_t both = std::max(zs, zts);
+    p->off_z[0] = p->off_zt[0] = take(both);
+    p->off_z[1] = p->off_zt[1] = take(both);
+  } else {
+    p->off_z[0] = take(zs);
+    p->off_z[1] = take(zs);
+    p->off_zt[0] = take(zts);
+    p->off_zt[1] = take(zts);
+  }
   p->off_a = take(as);
   p->off_b = take(as);
   return *cursor > 0 && *cursor < (int64_t(1) << 46);
+}
+
+// Largest operand of a problem in bytes (Z in either layout, A, B).
+int64_t max_operand_bytes(const Problem& p, int es) {
+  return std::max(std::max(p.S * p.Lp, p.L * p.Sp), p.S * p.Sp) * int64_t(es);
 }
 
 void add_pack_tiles(Plan* plan, int32_t prob) {
@@ -324,13 +345,13 @@ std::string build_layout(const MatrixShape* mats, int32_t n_mats,
   for (int full = 0; full < 2; ++full) {
     Plan& plan = L.plan[full];
     plan.full = full != 0;
-    int64_t cursor = 0;
     int32_t bi = 0;
+    // The units: every block (block plan) or every matrix (full plan).
     for (int32_t k = 0; k < n_mats; ++k) {
       const MatrixShape& m = mats[k];
       const int32_t nb = m.grid_rows * m.grid_cols;
-      auto add = [&](int64_t r0, int64_t c0, int64_t rows, int64_t cols,
-                     int32_t first_block, int32_t n_blocks) -> bool {
+      auto add = [&](int64_t r0, int64_t c0, int64_t rows, int64_t cols, int32_t first_block,
+                     int32_t n_blocks) {
         Problem p{};
         p.mat = k;
         p.row0 = r0;
@@ -346,25 +367,26 @@ std::string build_layout(const MatrixShape* mats, int32_t n_mats,
         p.n_blocks = n_blocks;
         p.seg_begin = L.blocks[first_block].seg_begin;
         p.seg_end = L.blocks[first_block + n_blocks - 1].seg_end;
-        if (!place_problem(&p, &cursor, align_elems)) return false;
         plan.probs.push_back(p);
-        add_pack_tiles(&plan, int32_t(plan.probs.size() - 1));
-        plan.ns_flops += ns_unit_flops(p.S, p.L, ns_steps);
-        plan.ns_dense_flops += ns_unit_dense_flops(p.S, p.L, ns_steps);
-        return true;
       };
       if (full) {
-        if (!add(0, 0, m.rows, m.cols, bi, nb)) return "workspace too large";
+        add(0, 0, m.rows, m.cols, bi, nb);
       } else {
         for (int32_t b = 0; b < nb; ++b) {
           const BlockPlan& bp = L.blocks[bi + b];
-          if (!add(bp.row0, bp.col0, bp.rows, bp.cols, bi + b, 1))
-            return "workspace too large";
+          add(bp.row0, bp.col0, bp.rows, bp.cols, bi + b, 1);
         }
       }
       bi += nb;
     }
-    plan.ws_elems = cursor;
+    for (const Problem& p : plan.probs)
+      if (max_operand_bytes(p, ns_elem_bytes) >= kMaxOperandBytes) {
+        *shape_error = true;
+        return "matrix " + std::to_string(p.mat) + (full ? "" : " (one block)") + ": a " +
+               std::to_string(p.S) + " x " + std::to_string(p.L) +
+               " orthogonalization operand reaches 2^31 bytes, beyond the 32-bit byte offsets "
+               "of the NS kernels";
+      }
     for (int kind = 0; kind < 3; ++kind) {
       plan.variant[kind] = choose_variant(plan.probs, GemmKind(kind), tile_policy, ns_elem_bytes);
       plan.nsplit[kind] = choose_split(plan.probs, GemmKind(kind), plan.variant[kind], k_split);
@@ -373,6 +395,15 @@ std::string build_layout(const MatrixShape* mats, int32_t n_mats,
         return "too many tiles";
     }
     plan.nn_apply = apply_mode == 0 && gemm_is_dmap(plan.variant[kApply]);
+    int64_t cursor = 0;
+    for (int32_t pi = 0; pi < int32_t(plan.probs.size()); ++pi) {
+      Problem& p = plan.probs[pi];
+      if (!place_problem(&p, &cursor, align_elems, plan.nn_apply)) return "workspace too large";
+      add_pack_tiles(&plan, pi);
+      plan.ns_flops += ns_unit_flops(p.S, p.L, ns_steps);
+      plan.ns_dense_flops += ns_unit_dense_flops(p.S, p.L, ns_steps);
+    }
+    plan.ws_elems = cursor;
     build_phases(&plan, ns_steps, poly_slots, kSlotPoly0 + poly_slots);
     if (plan.pack_tiles.size() > size_t(std::numeric_limits<int32_t>::max() / 2))
       return "too many tiles";

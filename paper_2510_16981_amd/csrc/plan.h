@@ -41,7 +41,9 @@ struct Problem {
   int64_t Sp, Lp;  // leading dimensions (multiples of 8 elements)
   // Element offsets inside the NS workspace arena.
   int64_t off_z[2];   // Z (S x Lp), ping-pong
-  int64_t off_zt[2];  // Z^T (L x Sp), ping-pong
+  int64_t off_zt[2];  // Z^T (L x Sp), ping-pong; the same buffers as off_z
+                      // when the plan's apply reads Z row-major (Plan::nn_apply):
+                      // then only U of a transposed unit is stored this way
   int64_t off_a;      // A = Z Z^T (S x Sp)
   int64_t off_b;      // B = b A + c A^2 (S x Sp)
   int32_t seg_begin, seg_end;

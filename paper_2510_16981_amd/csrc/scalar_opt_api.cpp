@@ -162,13 +162,14 @@ muonbp_status muonbp_adamw_create(const int64_t* sizes, int32_t n, const muonbp_
   if ((e = dev_alloc(c, &p, 2 * sizeof(float))) != hipSuccess) return bail(e);
   c->clip = static_cast<float*>(p);
   if ((e = c->ptrs.init(size_t(n))) != hipSuccess) return bail(e);
-  if ((e = hipMemcpy(c->segs, segs.data(), segs.size() * sizeof(ScalarSeg), hipMemcpyHostToDevice)) !=
-      hipSuccess)
+  // Table upload and m_0 = v_0 = 0 on the context's stream; the call waits
+  // for that stream only (not for the device's other streams).
+  if ((e = hipMemcpyAsync(c->segs, segs.data(), segs.size() * sizeof(ScalarSeg),
+                          hipMemcpyHostToDevice, c->stream)) != hipSuccess)
     return bail(e);
-  // m_0 = v_0 = 0.
-  if ((e = hipMemset(c->m, 0, size_t(c->state_elems) * 4)) != hipSuccess) return bail(e);
-  if ((e = hipMemset(c->v, 0, size_t(c->state_elems) * 4)) != hipSuccess) return bail(e);
-  if ((e = hipDeviceSynchronize()) != hipSuccess) return bail(e);
+  if ((e = hipMemsetAsync(c->m, 0, size_t(c->state_elems) * 4, c->stream)) != hipSuccess) return bail(e);
+  if ((e = hipMemsetAsync(c->v, 0, size_t(c->state_elems) * 4, c->stream)) != hipSuccess) return bail(e);
+  if ((e = hipStreamSynchronize(c->stream)) != hipSuccess) return bail(e);
   *out = c;
   return MUONBP_OK;
 }

@@ -20,7 +20,7 @@ NS_KINDS = ("gram", "poly", "apply")
 
 STATUS = {0: "MUONBP_OK", 1: "MUONBP_E_INVALID", 2: "MUONBP_E_SHAPE",
           3: "MUONBP_E_DTYPE", 4: "MUONBP_E_NOMEM", 5: "MUONBP_E_HIP",
-          6: "MUONBP_E_STATE"}
+          6: "MUONBP_E_STATE", 7: "MUONBP_E_NONFINITE"}
 
 
 class MuonBPError(RuntimeError):
@@ -43,7 +43,7 @@ class Options(ctypes.Structure):
                 ("ns_dtype", ctypes.c_int), ("tile_policy", ctypes.c_int32),
                 ("k_split", ctypes.c_int32), ("coeff_count", ctypes.c_int32),
                 ("coeff_table", ctypes.c_float * (3 * 16)), ("stream_hint", ctypes.c_int32),
-                ("apply_mode", ctypes.c_int32)]
+                ("apply_mode", ctypes.c_int32), ("check_finite", ctypes.c_int32)]
 
 
 class PlanInfo(ctypes.Structure):

@@ -1,6 +1,28 @@
 """Shared driver of the GPU parity tests: runs the HIP library and the CPU
-oracle in lockstep on the same seeded inputs and reports relative Frobenius
-errors.  Imported by the GPU tests only."""
+oracle in lockstep on the same seeded inputs and reports errors.  Imported
+by the GPU tests only.
+
+What is compared, per checked step and matrix:
+
+* U, teacher-forced: the oracle orthogonalizes the GPU's own momentum (so
+  the NS error is isolated), as a relative Frobenius error of the whole
+  matrix, of every orthogonalized unit (each block on a block step, the
+  matrix on a full step) and of every 64 x 64 tile of a unit (relative to the
+  tile's own norm, floored at the unit's average tile norm so that a tile of
+  near-zero entries does not divide by nothing).  A wrong or skipped tile
+  shows up in the tile maximum even when the matrix total hides it.
+* M, element by element: the GPU's M_t against mu M_{t-1} + G_t computed
+  from the GPU's own M_{t-1} (eq. NTR) and rounded to the state dtype; at
+  most one unit in the last place apart (the kernel rounds its fp32 fma to
+  the state dtype, the check rounds the exact value).
+* X, element by element: the GPU's X_{t+1} against (1 - eta lambda) X_t -
+  eta s U_t from the GPU's own X_t and U_t (Alg. 1's update with the
+  decoupled decay), with the kernel's fp32 constants, rounded to the param
+  dtype; at most one ulp apart.  A skipped or misplaced segment of the
+  update is caught here however small it is.
+* M, X, and X - X_0 against the free-running fp64 oracle (relative
+  Frobenius), and U against the free-running oracle's U.
+"""
 
 from __future__ import annotations
 
@@ -14,6 +36,8 @@ from oracle import muonbp_oracle as O
 from paper_2510_16981_amd import workload as W
 
 DT = {"f32": 0, "bf16": 1}
+MANTISSA_BITS = {"f32": 23, "bf16": 7}
+TILE = 64
 
 
 def rel(a: np.ndarray, b: np.ndarray) -> float:
@@ -26,6 +50,77 @@ def rel(a: np.ndarray, b: np.ndarray) -> float:
 def announce(msg: str) -> None:
     print(f"[gpu-case] {msg}", flush=True)
     sys.stdout.flush()
+
+
+def round_to(x: np.ndarray, dtype: str) -> np.ndarray:
+    """float64 values rounded (to nearest even) to the storage dtype."""
+    return W.quantize(x, dtype).double().numpy()
+
+
+def ulp(x: np.ndarray, dtype: str) -> np.ndarray:
+    """Spacing of the storage dtype at |x| (its smallest normal spacing
+    near zero)."""
+    p = MANTISSA_BITS[dtype]
+    a = np.maximum(np.abs(x), np.finfo(np.float32).tiny)
+    return np.exp2(np.floor(np.log2(a)) - p)
+
+
+def ulp_distance(got: np.ndarray, want: np.ndarray, dtype: str) -> float:
+    """Largest |got - want| over the coarser of the two values' spacings."""
+    if got.size == 0:
+        return 0.0
+    d = np.abs(got - want) / np.maximum(ulp(got, dtype), ulp(want, dtype))
+    return float(np.max(d))
+
+
+def tile_errors(u: np.ndarray, ref: np.ndarray, tile: int = TILE) -> float:
+    """Worst relative error over tile x tile tiles of one unit (ragged edge
+    tiles included): ||du_tile|| / max(||ref_tile||, ||ref|| sqrt(n_tile / n))."""
+    n_all = np.linalg.norm(ref)
+    worst = 0.0
+    m, n = ref.shape
+    for i in range(0, m, tile):
+        for j in range(0, n, tile):
+            r = ref[i:i + tile, j:j + tile]
+            d = np.linalg.norm(u[i:i + tile, j:j + tile] - r)
+            floor = n_all * np.sqrt(r.size / ref.size)
+            den = max(np.linalg.norm(r), floor)
+            worst = max(worst, d / den if den > 0 else d)
+    return float(worst)
+
+
+def unit_errors(u: np.ndarray, ref: np.ndarray, units) -> tuple:
+    """(worst per-unit relative error, worst per-tile error) over the units
+    (row and column slices) of one matrix."""
+    wu = wt = 0.0
+    for rs, cs in units:
+        wu = max(wu, rel(u[rs, cs], ref[rs, cs]))
+        wt = max(wt, tile_errors(u[rs, cs], ref[rs, cs]))
+    return wu, wt
+
+
+def matrix_units(shape, grid, full):
+    r, c = shape
+    return [(slice(0, r), slice(0, c))] if full else O.block_ranges(r, c, *grid)
+
+
+def momentum_reference(m_prev: np.ndarray, g: np.ndarray, mu: float, state: str) -> np.ndarray:
+    """mu M_{t-1} + G_t with the kernel's fp32 mu, rounded to the state dtype."""
+    return round_to(float(np.float32(mu)) * m_prev + g, state)
+
+
+def update_reference(x_prev: np.ndarray, u: np.ndarray, eta: float, lam: float, s: float,
+                     param: str) -> np.ndarray:
+    """X <- (1 - eta lambda) X - eta s U as the update kernel computes it: the
+    decay and step constants in fp32, the product step * U rounded to fp32,
+    one fused multiply-add (exact here, then rounded to fp32), then the
+    param dtype."""
+    f32 = np.float32
+    decay = float(f32(1.0) - f32(eta) * f32(lam))
+    step = f32(eta) * f32(s)
+    prod = (-step * u.astype(np.float32)).astype(np.float64)
+    fma = (decay * x_prev + prod).astype(np.float32).astype(np.float64)
+    return round_to(fma, param) if param != "f32" else fma
 
 
 @dataclass
@@ -58,11 +153,15 @@ class Case:
 
 @dataclass
 class Result:
-    u_err: List[float] = field(default_factory=list)      # teacher-forced U
+    u_err: List[float] = field(default_factory=list)       # teacher-forced U, whole matrix
+    u_unit_err: List[float] = field(default_factory=list)  # worst unit (block / matrix)
+    u_tile_err: List[float] = field(default_factory=list)  # worst 64 x 64 tile of a unit
     u_free_err: List[float] = field(default_factory=list)  # U vs free-running oracle
     m_err: List[float] = field(default_factory=list)
     x_err: List[float] = field(default_factory=list)
     dx_err: List[float] = field(default_factory=list)  # X_t - X_0 against the oracle's
+    m_ulp: List[float] = field(default_factory=list)   # teacher-forced M, elementwise
+    x_ulp: List[float] = field(default_factory=list)   # teacher-forced X, elementwise
     fulls: List[bool] = field(default_factory=list)
     final_params: List[np.ndarray] = field(default_factory=list)
     final_mom: List[np.ndarray] = field(default_factory=list)
@@ -70,8 +169,9 @@ class Result:
 
     def worst(self) -> Dict[str, float]:
         f = lambda v: max(v) if v else 0.0
-        return dict(u=f(self.u_err), u_free=f(self.u_free_err), m=f(self.m_err), x=f(self.x_err),
-                    dx=f(self.dx_err))
+        return dict(u=f(self.u_err), u_unit=f(self.u_unit_err), u_tile=f(self.u_tile_err),
+                    u_free=f(self.u_free_err), m=f(self.m_err), x=f(self.x_err),
+                    dx=f(self.dx_err), m_ulp=f(self.m_ulp), x_ulp=f(self.x_ulp))
 
 
 def make_inputs(case: Case):
@@ -117,25 +217,37 @@ def run_case(case: Case, keep_updates: bool = False) -> Result:
     params = [p.cuda() for p in params_h]
     x_ref = [p.double().numpy() for p in params_h]
     x_init = [x.copy() for x in x_ref]
+    m_gpu_prev = [np.zeros((r, c)) for r, c, _, _ in case.mats]  # M_{-1} = 0
     res = Result()
     for t in range(case.steps):
         if case.period_schedule and t in case.period_schedule:
             opt.set_period(case.period_schedule[t])
             orc.cfg.period = case.period_schedule[t]
+        check = case.check_steps is None or t in case.check_steps or t == case.steps - 1
+        prev_checked = case.check_steps is None or t == 0 or (t - 1) in case.check_steps
+        if check and not prev_checked:
+            # The GPU's own M_{t-1} for the elementwise momentum check.
+            torch.cuda.synchronize()
+            m_gpu_prev = [opt.get_momentum(k).double().cpu().numpy() for k in range(len(case.mats))]
+        x_prev = [p.double().cpu().numpy() for p in params] if check else None
         g_dev = [g.cuda() for g in grads_h[t]]
         opt.step(params, g_dev, t)
         full = opt.is_full(t)
         res.fulls.append(full)
         g64 = [g.double().numpy() for g in grads_h[t]]
         x_ref, rec = orc.step(x_ref, g64, t, record=True)
-        check = case.check_steps is None or t in case.check_steps
-        if not check and t != case.steps - 1:
+        if not check:
             continue
         torch.cuda.synchronize()
+        eta = case.lr_full if full else case.lr_block
         for k, (r, c, gr, gc) in enumerate(case.mats):
             m_gpu = opt.get_momentum(k).double().cpu().numpy()
             torch.cuda.synchronize()
             res.m_err.append(rel(m_gpu, rec.M[k]))
+            res.m_ulp.append(ulp_distance(
+                m_gpu, momentum_reference(m_gpu_prev[k], g64[k], case.momentum, case.state),
+                case.state))
+            m_gpu_prev[k] = m_gpu
             x_gpu = params[k].double().cpu().numpy()
             res.x_err.append(rel(x_gpu, x_ref[k]))
             res.dx_err.append(rel(x_gpu - x_init[k], x_ref[k] - x_init[k]))
@@ -149,9 +261,19 @@ def run_case(case: Case, keep_updates: bool = False) -> Result:
             u_tf = O.orthogonalize_via_ns(y, **ns) if full else \
                 O.orthogonalize_blockwise(y, (gr, gc), **ns)
             res.u_err.append(rel(u_gpu, u_tf))
+            wu, wt = unit_errors(u_gpu, u_tf, matrix_units((r, c), (gr, gc), full))
+            res.u_unit_err.append(wu)
+            res.u_tile_err.append(wt)
+            # The update from the GPU's own X_t and U_t (RMS scale of the unit).
+            p, q = (r, c) if full else (r // gr, c // gc)
+            s = 1.0
+            if case.scale_mode == 1:
+                s = float(np.float32(case.rms_beta) * np.sqrt(np.float32(max(p, q))))
+            res.x_ulp.append(ulp_distance(
+                x_gpu, update_reference(x_prev[k], u_gpu, eta, case.weight_decay, s, case.param),
+                case.param))
             u_free = rec.U[k]
             if case.scale_mode == 1:
-                p, q = (r, c) if full else (r // gr, c // gc)
                 u_free = u_free / O.rms_scale(p, q, case.rms_beta)
             res.u_free_err.append(rel(u_gpu, u_free))
             if keep_updates:

@@ -58,7 +58,7 @@ def test_options_default(lib):
 
 
 def test_status_strings(lib):
-    for code in range(7):
+    for code in range(8):
         assert lib.muonbp_status_string(code)
     assert lib.muonbp_last_error(None) == b"no context"
     lib.muonbp_destroy(None)  # NULL-safe
@@ -94,6 +94,38 @@ def test_create_rejects_bad_arguments_before_gpu(lib):
     assert _create(lib, [(8, 8, 1, 1)], opt=mb.options_default(stream_hint=3))[0] == 1
     assert _create(lib, [(8, 8, 1, 1)], opt=mb.options_default(stream_hint=-1))[0] == 1
     assert _create(lib, [(8, 8, 1, 1)], opt=mb.options_default(apply_mode=2))[0] == 1
+    assert _create(lib, [(8, 8, 1, 1)], opt=mb.options_default(check_finite=2))[0] == 1
+
+
+def _describe_status(lib, mats, opt=None, full=0):
+    info = mb.PlanInfo()
+    return lib.muonbp_describe_plan(mb._mats(mats), len(mats), ctypes.byref(opt) if opt else None,
+                                    full, ctypes.byref(info))
+
+
+@pytest.mark.parametrize("mats,ns_dtype", [
+    ([(4096, 600000, 1, 1)], mb.BF16),      # 4.9 GB operand (full plan and its one block)
+    ([(40000, 40000, 1, 1)], mb.BF16),      # 3.2 GB
+    ([(40000, 40000, 8, 8)], mb.BF16),      # blocks are small, the full matrix is not
+    ([(16384, 32768, 1, 1)], mb.F32),       # exactly 2^31 bytes in fp32
+    ([(64, 64, 1, 1), (4096, 600000, 1, 8)], mb.BF16),
+])
+def test_units_with_operands_of_2_31_bytes_are_rejected(lib, mats, ns_dtype):
+    """The NS kernels address an operand with 32-bit byte offsets: any unit of
+    either plan whose Z, Z^T, A or B reaches 2^31 bytes is refused with
+    E_SHAPE (no HIP call is made by describe_plan or before it in create)."""
+    opt = mb.options_default(ns_dtype=ns_dtype, param_dtype=ns_dtype, state_dtype=ns_dtype)
+    for full in (0, 1):
+        assert _describe_status(lib, mats, opt, full) == 2
+    st, ctx = _create(lib, mats, opt=opt)
+    assert st == 2 and not ctx.value
+
+
+def test_largest_accepted_units_stay_below_2_31_bytes(lib):
+    # A 32768 x 32768 bf16 Z is exactly 2^31 bytes; one 8-element padding
+    # step smaller is accepted.
+    assert _describe_status(lib, [(32760, 32760, 1, 1)]) == 0
+    assert _describe_status(lib, [(32768, 32768, 1, 1)]) == 2
 
 
 def test_null_context_calls(lib):
@@ -139,6 +171,16 @@ def test_describe_plan_counts_and_flops(lib, name):
         assert info.gemm_tiles[0] == gram and info.gemm_tiles[1] == poly
         assert info.gemm_tiles[2] == apply
         assert info.workspace_bytes > 0
+        # The apply reads Z row-major on every bf16 workload: per unit two Z
+        # buffers (either layout) plus A and B, nothing else.
+        if info.apply_nn:
+            ws = 0
+            for p, q in units:
+                S, L = min(p, q), max(p, q)
+                Sp, Lp = -(-S // 8) * 8, -(-L // 8) * 8
+                for n_el in (max(S * Lp, L * Sp),) * 2 + (S * Sp,) * 2:
+                    ws = -(-(ws + n_el) // 128) * 128  # 256-byte aligned bf16 buffers
+            assert info.workspace_bytes == 2 * ws
 
 
 def test_describe_plan_qkv_numbers(lib):

@@ -104,3 +104,45 @@ def test_capture_with_new_pointers_is_refused():
     _same_state(A, pA, B, pB)
     A.close()
     B.close()
+
+
+def test_replay_after_many_eager_steps_with_other_pointers():
+    """The captured step's pointer table is never overwritten: after more
+    eager steps with other pointers than the table has slots (alternating
+    between two other sets of tensors), a replay still updates the captured
+    tensors with the captured gradients.  Context B runs the same sequence
+    eagerly (the replay's place taken by an eager step with the captured
+    tensors); every tensor and the momentum agree bit for bit."""
+    import torch
+    ((A, sA, pA), (B, _, pB)), g = _setup()
+    rng = np.random.default_rng(11)
+    others = []
+    for _ in range(2):
+        po = [torch.from_numpy(0.02 * rng.standard_normal((r, c))).to(torch.bfloat16).cuda()
+              for r, c, _, _ in MATS]
+        go = [torch.from_numpy(0.01 * rng.standard_normal((r, c))).to(torch.bfloat16).cuda()
+              for r, c, _, _ in MATS]
+        others.append(([p.clone() for p in po], [p.clone() for p in po], go))
+    for t in (0, 1):
+        A.step(pA, g, t)
+        B.step(pB, g, t)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=sA):
+        A.step(pA, g, 2)
+    torch.cuda.synchronize()
+    for r in range(2):
+        for i in range(9):  # more pointer changes than the initial slot count
+            pa_o, pb_o, go = others[i % 2]
+            A.step(pa_o, go, 3 + i)
+            B.step(pb_o, go, 3 + i)
+        torch.cuda.synchronize()
+        announce(f"replay after 9 eager steps with other pointers, round {r}")
+        graph.replay()
+        B.step(pB, g, 2)
+        _same_state(A, pA, B, pB)
+        for pa_o, pb_o, _ in others:
+            for x, y in zip(pa_o, pb_o):
+                assert torch.equal(x, y)
+    A.close()
+    B.close()
