@@ -40,8 +40,10 @@ typedef enum {
   MUONBP_E_NOMEM = 4,   /* device or host allocation failed                   */
   MUONBP_E_HIP = 5,     /* a HIP runtime call or kernel launch failed         */
   MUONBP_E_STATE = 6,   /* context poisoned by an earlier MUONBP_E_HIP        */
-  MUONBP_E_NONFINITE = 7 /* muonbp_options.check_finite found NaN / Inf in an
-                            orthogonalization input (context stays usable)    */
+  MUONBP_E_NONFINITE = 7, /* muonbp_options.check_finite found NaN / Inf in
+                             an orthogonalization input (context stays usable) */
+  MUONBP_E_TOO_LARGE = 8  /* muonbp_step_static: the step needs more scratch
+                             than MUONBP_STATIC_SCRATCH_BYTES                  */
 } muonbp_status;
 
 typedef enum { MUONBP_F32 = 0, MUONBP_BF16 = 1 } muonbp_dtype;
@@ -216,6 +218,9 @@ typedef struct {
   int64_t workspace_bytes; /* NS workspace this plan needs                  */
   int32_t gemm_split[3];   /* workgroups sharing one tile's K loop (1 = none) */
   int32_t apply_nn;        /* 1: the apply products read Z row-major (no Z^T) */
+  int64_t static_scratch_bytes; /* scratch muonbp_step_static needs for a step
+                              of this plan (MUONBP_E_TOO_LARGE above
+                              MUONBP_STATIC_SCRATCH_BYTES)                    */
 } muonbp_plan_info;
 
 /* Plan description for a set of matrices without creating a context
@@ -256,6 +261,41 @@ const char* muonbp_last_error(const muonbp_ctx* ctx);
 /* Free everything the context owns (waits for its stream first).
  * NULL is a no-op. */
 void muonbp_destroy(muonbp_ctx* ctx);
+
+/* ------------------------------------------------------------------------
+ * Allocation-free step, for callers that cannot allocate device memory
+ * (tight serving loops, harnesses that forbid hipMalloc).  One iteration
+ * t = step of Algorithm 1, the same kernels and plans as muonbp_create +
+ * muonbp_step with the same arguments, but nothing is allocated and no
+ * context is kept:
+ *  - the momentum is the caller's: `momentum` is one device buffer of
+ *    sum_i rows_i * cols_i elements of opt->state_dtype, the matrices back
+ *    to back in the order of `mats`, each row-major; updated in place
+ *    (all zeros before the first step: Algorithm 1's M_{-1} = 0);
+ *  - params / grads as for muonbp_step (host arrays of device pointers);
+ *  - full step iff period > 0 and step % period == 0;
+ *  - every other buffer of the step (NS workspace, partial sums, scales,
+ *    split-K sums and counters, plan and pointer tables) lives in one
+ *    static device array of MUONBP_STATIC_SCRATCH_BYTES per GPU, which the
+ *    library holds from its first use on that GPU until the process ends.
+ *    A step that needs more (muonbp_plan_info.static_scratch_bytes) is
+ *    refused with MUONBP_E_TOO_LARGE before any HIP call; e.g. every step
+ *    of one 2048 x 6144 bf16 matrix in 2048 x 768 shards fits.
+ * The tables are built on the host (host heap only) and copied into the
+ * scratch array on hip_stream; the call returns after the step has run to
+ * completion on hip_stream (it waits for that stream), so it cannot be
+ * captured into a graph.  Calls on one GPU share its scratch array, which
+ * keeps the last call's contents (what must start at zero is cleared by
+ * each call): calls that overlap on one GPU (from several host threads or
+ * streams) race and must be serialized by the caller.
+ * Errors: E_INVALID (NULL or bad arguments, bad options), E_SHAPE, E_DTYPE,
+ * E_TOO_LARGE (before any HIP call), E_HIP; check_finite as in muonbp_step
+ * (E_NONFINITE: momentum updated, nothing else run). */
+#define MUONBP_STATIC_SCRATCH_BYTES ((int64_t)128 << 20)
+muonbp_status muonbp_step_static(const muonbp_matrix* mats, int32_t n_mats, void* const* params,
+                                 const void* const* grads, void* momentum, int64_t step,
+                                 int64_t period, float lr_block, float lr_full, float momentum_mu,
+                                 float weight_decay, const muonbp_options* opt, void* hip_stream);
 
 /* ------------------------------------------------------------------------
  * Scalar optimizer for the parameters MuonBP does not orthogonalize.

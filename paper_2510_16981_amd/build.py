@@ -17,7 +17,8 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(os.path.dirname(HERE), "include")
 LIB_NAME = "libmuonbp.so"
 LIB_PATH = os.path.join(HERE, LIB_NAME)
-SOURCES = ["kernels.hip", "muonbp_api.cpp", "plan.cpp", "scalar_opt_api.cpp"]
+SOURCES = ["kernels.hip", "muonbp_api.cpp", "plan.cpp", "scalar_opt_api.cpp", "step_core.cpp",
+           "static_step.hip"]
 
 
 def hipcc() -> str:

@@ -16,15 +16,11 @@
 #include "kernels.h"
 #include "plan.h"
 #include "ptr_ring.h"
+#include "step_core.h"
 
 using namespace muonbp;
 
 namespace {
-
-
-size_t dtype_size(muonbp_dtype d) { return d == MUONBP_F32 ? 4 : 2; }
-DType dt(muonbp_dtype d) { return d == MUONBP_F32 ? DType::F32 : DType::BF16; }
-bool dtype_ok(muonbp_dtype d) { return d == MUONBP_F32 || d == MUONBP_BF16; }
 
 struct PlanDev {
   ScaleDesc* scale = nullptr;
@@ -35,6 +31,18 @@ struct PlanDev {
   UpdDesc* upd = nullptr;
   std::vector<UpdDesc> upd_host;  // for muonbp_get_update
   bool fuse_scale = false;        // the pack computes the scales (no k_scale launch)
+
+  PlanView view() const {
+    PlanView v;
+    v.scale = scale;
+    v.pack = pack;
+    v.pack_tiles = pack_tiles;
+    v.descs = descs;
+    v.phase_tiles = phase_tiles.data();
+    v.upd = upd;
+    v.fuse_scale = fuse_scale;
+    return v;
+  }
 };
 
 struct ProfRec {
@@ -96,42 +104,6 @@ muonbp_status hip_fail(muonbp_ctx* c, hipError_t e, const char* what) {
   return MUONBP_E_HIP;
 }
 
-// Polynomial descriptors per problem: one for the constant quintic, else
-// one per table entry that some iteration uses.
-int poly_slots(const muonbp_options& o) {
-  if (o.coeff_count <= 0) return 1;
-  return std::max(1, std::min(o.coeff_count, o.ns_steps));
-}
-
-// Iteration k's (a, b, c) (Alg. 2; a table's last entry repeats).
-void ns_coeffs(const muonbp_options& o, int k, float* a, float* b, float* c) {
-  if (o.coeff_count <= 0) {
-    *a = o.a, *b = o.b, *c = o.c;
-    return;
-  }
-  const int e = std::min(k, o.coeff_count - 1);
-  *a = o.coeff_table[3 * e], *b = o.coeff_table[3 * e + 1], *c = o.coeff_table[3 * e + 2];
-}
-
-std::string validate_opts(const muonbp_options& o) {
-  if (o.ns_steps < 0 || o.ns_steps > 1000) return "ns_steps must be in [0, 1000]";
-  if (!(o.eps >= 0.f) || !std::isfinite(o.eps)) return "eps must be finite and >= 0";
-  if (!std::isfinite(o.a) || !std::isfinite(o.b) || !std::isfinite(o.c))
-    return "NS coefficients must be finite";
-  if (o.nesterov != 0 && o.nesterov != 1) return "nesterov must be 0 or 1";
-  if (o.scale_mode != 0 && o.scale_mode != 1) return "scale_mode must be 0 or 1";
-  if (!std::isfinite(o.rms_beta)) return "rms_beta must be finite";
-  if (o.tile_policy < 0 || o.tile_policy > kNumGemmVariants) return "tile_policy out of range";
-  if (o.k_split < 0 || o.k_split > kMaxKSplit) return "k_split out of range";
-  if (o.coeff_count < 0 || o.coeff_count > MUONBP_MAX_COEFFS) return "coeff_count out of range";
-  if (o.stream_hint < 0 || o.stream_hint > 2) return "stream_hint out of range";
-  if (o.apply_mode < 0 || o.apply_mode > 1) return "apply_mode out of range";
-  if (o.check_finite != 0 && o.check_finite != 1) return "check_finite must be 0 or 1";
-  for (int i = 0; i < 3 * o.coeff_count; ++i)
-    if (!std::isfinite(o.coeff_table[i])) return "coefficients must be finite";
-  return "";
-}
-
 // Copies a host table into new device memory on the context's stream and
 // waits for that stream only (no device-wide synchronisation, which would
 // also wait for, or break a graph capture on, the caller's other streams).
@@ -161,95 +133,13 @@ hipError_t dev_alloc(muonbp_ctx* c, void** p, size_t bytes) {
 hipError_t build_plan_tables(muonbp_ctx* c, int full) {
   const Plan& plan = c->lay.plan[full];
   PlanDev& pd = c->pd[full];
-  const size_t es = dtype_size(c->opt.ns_dtype);
-  char* ws = static_cast<char*>(c->ws);
-  auto at = [&](int64_t off) { return static_cast<void*>(ws + off * int64_t(es)); };
-  const muonbp_options& o = c->opt;
-
-  std::vector<ScaleDesc> sd;
-  std::vector<PackDesc> pk;
-  std::vector<GemmDesc> descs;
-  std::vector<int64_t> pack_tiles_of(plan.probs.size(), 0);
-  for (const TileRef& t : plan.pack_tiles) ++pack_tiles_of[size_t(t.prob)];
-  int64_t fused_reads = 0;
-  for (size_t i = 0; i < plan.probs.size(); ++i)
-    fused_reads += pack_tiles_of[i] * (plan.probs[i].seg_end - plan.probs[i].seg_begin);
-  pd.fuse_scale = fused_reads <= kFuseScaleMaxReads;
-  for (const Problem& p : plan.probs) {
-    sd.push_back(ScaleDesc{p.seg_begin, p.seg_end});
-    const MatrixShape& m = c->lay.mats[p.mat];
-    PackDesc d{};
-    d.in_mat_off = p.row0 * m.cols + p.col0;
-    d.mom_off = c->lay.mat_off[p.mat] + d.in_mat_off;
-    d.ld = m.cols;
-    d.mat = p.mat;
-    d.rows = int32_t(p.rows);
-    d.cols = int32_t(p.cols);
-    d.tiles_c = int32_t((p.cols + kPackTile - 1) / kPackTile);
-    d.seg_begin = p.seg_begin;
-    d.seg_end = p.seg_end;
-    // Z = Y (S = rows) or Y^T (S = cols); Z^T the other way round, needed
-    // by the NT apply.  The apply that reads Z row-major needs Z only, and
-    // with no iterations the straight copy is U itself (in the matrix's
-    // orientation, where the update reads it).
-    const bool z_only = plan.nn_apply && o.ns_steps > 0;
-    const bool u_only = plan.nn_apply && o.ns_steps == 0;
-    if (!p.trans) {
-      d.dst_s = at(p.off_z[0]);
-      d.ld_s = p.Lp;
-      d.dst_t = (z_only || u_only) ? nullptr : at(p.off_zt[0]);
-      d.ld_t = p.Sp;
-    } else {
-      d.dst_s = z_only ? nullptr : at(p.off_zt[0]);
-      d.ld_s = p.Sp;
-      d.dst_t = u_only ? nullptr : at(p.off_z[0]);
-      d.ld_t = p.Lp;
-    }
-    pk.push_back(d);
-    const int32_t S = int32_t(p.S), Lr = int32_t(p.L), Sp = int32_t(p.Sp), Lp = int32_t(p.Lp);
-    // Slots in DescSlot order.  Gram: A = Z_q Z_q^T (symmetric).
-    for (int q = 0; q < 2; ++q)
-      descs.push_back(GemmDesc{at(p.off_z[q]), at(p.off_z[q]), nullptr, at(p.off_a), at(p.off_a),
-                               S, S, Lr, Lp, Lp, 0, Sp, Sp, 1.f, 0.f, 0.f, 1});
-    // Apply: Z_{1-q} = (a I + B) Z_q (= a Z_q + B Z_q).  NT: Y = Z_q^T and
-    // Z_{1-q} also stored transposed.  NN: Y = Z_q itself, and only the last
-    // apply of a transposed unit writes Z^T (as U, where the update reads it).
-    auto apply_desc = [&](int q, bool last) {
-      if (!plan.nn_apply)
-        return GemmDesc{at(p.off_b), at(p.off_zt[q]), nullptr, at(p.off_z[1 - q]), at(p.off_zt[1 - q]),
-                        S, Lr, S, Sp, Sp, 0, Lp, Sp, 1.f, 0.f, 0.f, 0};
-      const bool t_only = last && p.trans;
-      return GemmDesc{at(p.off_b), at(p.off_z[q]), nullptr, t_only ? nullptr : at(p.off_z[1 - q]),
-                      t_only ? at(p.off_zt[1 - q]) : nullptr, S, Lr, S, Sp, Lp, 0, Lp, Sp,
-                      1.f, 0.f, 0.f, 0};
-    };
-    for (int q = 0; q < 2; ++q) descs.push_back(apply_desc(q, false));
-    descs.push_back(apply_desc((o.ns_steps + 1) & 1, true));  // iteration K - 1 reads Z_{(K-1) mod 2}
-    // Polynomial of iteration k: B = c_k A A^T + b_k A + a_k I (A symmetric;
-    // the a I term carries Algorithm 2's a X into the apply).
-    for (int k = 0; k < c->lay.poly_slots; ++k) {
-      float a, b, cc;
-      ns_coeffs(o, k, &a, &b, &cc);
-      descs.push_back(GemmDesc{at(p.off_a), at(p.off_a), at(p.off_a), at(p.off_b), at(p.off_b), S,
-                               S, S, Sp, Sp, Sp, Sp, Sp, cc, b, a, 1});
-    }
-  }
-  // Update table: U of every block after K iterations (buffer K mod 2).
-  const int fin = o.ns_steps & 1;
-  pd.upd_host.clear();
-  for (const Problem& p : plan.probs) {
-    const MatrixShape& m = c->lay.mats[p.mat];
-    float s = 1.f;
-    if (o.scale_mode == 1) s = o.rms_beta * std::sqrt(float(std::max(p.rows, p.cols)));
-    const int64_t base = p.trans ? p.off_zt[fin] : p.off_z[fin];
-    const int64_t ldu = p.trans ? p.Sp : p.Lp;
-    (void)m;
-    for (int32_t b = p.first_block; b < p.first_block + p.n_blocks; ++b) {
-      const BlockPlan& bp = c->lay.blocks[b];
-      const int64_t off = base + (bp.row0 - p.row0) * ldu + (bp.col0 - p.col0);
-      pd.upd_host.push_back(UpdDesc{at(off), ldu, s, 0});
-    }
-  }
+  PlanHostTables h;
+  build_plan_host_tables(c->lay, c->opt, full, c->ws, &h);
+  pd.fuse_scale = h.fuse_scale;
+  pd.upd_host = h.upd;
+  const std::vector<ScaleDesc>& sd = h.scale;
+  const std::vector<PackDesc>& pk = h.pack;
+  const std::vector<GemmDesc>& descs = h.descs;
   hipError_t e;
   if ((e = upload(c, &pd.scale, sd)) != hipSuccess) return e;
   if ((e = upload(c, &pd.pack, pk)) != hipSuccess) return e;
@@ -273,15 +163,6 @@ void free_ctx(muonbp_ctx* c) {
   for (hipEvent_t e : c->ev_pool) (void)hipEventDestroy(e);
   if (c->finite_host) (void)hipHostFree(c->finite_host);
   delete c;
-}
-
-std::string check_mats(const muonbp_matrix* mats, int32_t n_mats, std::vector<MatrixShape>* out) {
-  if (!mats) return "mats is NULL";
-  if (n_mats <= 0) return "n_mats must be > 0";
-  out->clear();
-  for (int32_t i = 0; i < n_mats; ++i)
-    out->push_back(MatrixShape{mats[i].rows, mats[i].cols, mats[i].grid_rows, mats[i].grid_cols});
-  return "";
 }
 
 // Profiling helpers: bracket a launch with events when enabled.
@@ -390,9 +271,7 @@ muonbp_status muonbp_describe_plan(const muonbp_matrix* mats, int32_t n_mats,
   Layout lay;
   bool shape_err = false;
   try {
-    if (!build_layout(shapes.data(), n_mats, int(dtype_size(o.ns_dtype)), o.ns_steps,
-                      poly_slots(o), o.tile_policy, o.k_split, o.apply_mode, &lay, &shape_err)
-             .empty())
+    if (!layout_for(shapes, o, &lay, &shape_err).empty())
       return shape_err ? MUONBP_E_SHAPE : MUONBP_E_INVALID;
   } catch (const std::bad_alloc&) {
     return MUONBP_E_NOMEM;
@@ -416,6 +295,7 @@ muonbp_status muonbp_describe_plan(const muonbp_matrix* mats, int32_t n_mats,
   // momentum: read G, M, write M; update: read X, U, write X.
   out->elementwise_bytes = double(lay.total_elems) * ((pb + 2 * sb) + (2 * pb + nb));
   out->workspace_bytes = p.ws_elems * int64_t(nb);
+  out->static_scratch_bytes = scratch_plan(lay, full, o).total;
   return MUONBP_OK;
 }
 
@@ -441,9 +321,7 @@ muonbp_status muonbp_create(const muonbp_matrix* mats, int32_t n_mats, int64_t p
   if (!c) return MUONBP_E_NOMEM;
   try {
     bool shape_err = false;
-    std::string msg = build_layout(shapes.data(), n_mats, int(dtype_size(o.ns_dtype)), o.ns_steps,
-                                   poly_slots(o), o.tile_policy, o.k_split, o.apply_mode, &c->lay,
-                                   &shape_err);
+    std::string msg = layout_for(shapes, o, &c->lay, &shape_err);
     if (!msg.empty()) {
       free_ctx(c);
       return shape_err ? MUONBP_E_SHAPE : MUONBP_E_INVALID;
@@ -461,17 +339,8 @@ muonbp_status muonbp_create(const muonbp_matrix* mats, int32_t n_mats, int64_t p
   c->stream = static_cast<hipStream_t>(hip_stream);
 
   // 16-byte vector paths need 8-element aligned windows and strides.
-  bool vec = true;
-  for (const BlockPlan& b : c->lay.blocks) {
-    const MatrixShape& m = c->lay.mats[b.mat];
-    vec = vec && b.cols % 8 == 0 && b.col0 % 8 == 0 && m.cols % 8 == 0 && c->lay.mat_off[b.mat] % 8 == 0;
-  }
-  c->vec_layout = vec;
-  // Nontemporal streaming once a step's momentum and update data cannot stay
-  // in the last-level cache anyway.
-  const int64_t streamed = c->lay.total_elems * int64_t(2 * dtype_size(o.param_dtype) +
-                                                       dtype_size(o.state_dtype));
-  c->stream_nt = o.stream_hint == 2 || (o.stream_hint == 0 && streamed > kStreamNtBytes);
+  c->vec_layout = layout_vectorizable(c->lay);
+  c->stream_nt = stream_nontemporal(c->lay, o);
 
   hipError_t e = hipGetDevice(&c->device);
   if (e != hipSuccess) {
@@ -507,18 +376,7 @@ muonbp_status muonbp_create(const muonbp_matrix* mats, int32_t n_mats, int64_t p
       return bail(e, "split counters");
   }
   if ((e = upload(c, &c->segs, c->lay.segs)) != hipSuccess) return bail(e, "segments");
-  std::vector<BlockDesc> bd;
-  for (const BlockPlan& b : c->lay.blocks) {
-    const MatrixShape& m = c->lay.mats[b.mat];
-    BlockDesc d{};
-    d.in_mat_off = b.row0 * m.cols + b.col0;
-    d.mom_off = c->lay.mat_off[b.mat] + d.in_mat_off;
-    d.ld = m.cols;
-    d.mat = b.mat;
-    d.cols = int32_t(b.cols);
-    bd.push_back(d);
-  }
-  if ((e = upload(c, &c->blocks, bd)) != hipSuccess) return bail(e, "blocks");
+  if ((e = upload(c, &c->blocks, block_descs(c->lay))) != hipSuccess) return bail(e, "blocks");
   for (int full = 0; full < 2; ++full)
     if ((e = build_plan_tables(c, full)) != hipSuccess) return bail(e, "plan tables");
   if ((e = c->ptrs.init(shapes.size())) != hipSuccess) return bail(e, "pointer tables");
@@ -568,22 +426,30 @@ muonbp_status muonbp_step(muonbp_ctx* c, void* const* params, const void* const*
 
   // Algorithm 1: full orthogonalization iff t mod P = 0 (P = 0 means infinity).
   const int full = (c->period > 0 && step % c->period == 0) ? 1 : 0;
-  const Plan& plan = c->lay.plan[full];
-  const PlanDev& pd = c->pd[full];
   const muonbp_options& o = c->opt;
-  const DType tp = dt(o.param_dtype), tm = dt(o.state_dtype), tn = dt(o.ns_dtype);
-  const int nsegs = int(c->lay.segs.size());
   const hipStream_t s = c->stream;
   c->prof_full = full;
-
-  e = timed(c, 0, [&] {
-    return launch_momentum(tp, tm, aligned, c->stream_nt, nsegs, c->segs, c->blocks, mats, c->mom,
-                           c->mu, o.nesterov, c->partials, s);
-  });
-  if (e != hipSuccess) return hip_fail(c, e, "momentum");
+  StepBuffers b;
+  b.mom = c->mom;
+  b.partials = c->partials;
+  b.scales = c->scales;
+  b.ksum = c->ksum;
+  b.kcount = c->kcount;
+  b.segs = c->segs;
+  b.blocks = c->blocks;
+  b.mats = mats;
+  b.n_segs = int(c->lay.segs.size());
+  StepScalars sc;
+  sc.mu = c->mu;
+  sc.eta = full ? c->lr_full : c->lr_block;
+  sc.wd = c->wd;
+  sc.vec = aligned;
+  sc.nt = c->stream_nt;
+  auto wrap = [&](int kind, auto&& launch) { return timed(c, kind, launch); };
+  if ((e = enqueue_momentum(o, b, sc, s, wrap)) != hipSuccess) return hip_fail(c, e, "momentum");
   if (o.check_finite) {
     // Debug check: any non-finite per-segment sum of squares of the NS input.
-    if ((e = launch_check_finite(nsegs, c->partials, c->finite_flag, s)) != hipSuccess ||
+    if ((e = launch_check_finite(b.n_segs, c->partials, c->finite_flag, s)) != hipSuccess ||
         (e = hipMemcpyAsync(c->finite_host, c->finite_flag, sizeof(int), hipMemcpyDeviceToHost, s)) !=
             hipSuccess ||
         (e = hipStreamSynchronize(s)) != hipSuccess)
@@ -593,35 +459,11 @@ muonbp_status muonbp_step(muonbp_ctx* c, void* const* params, const void* const*
                   "NaN or Inf in the orthogonalization input (momentum of this step) of some unit; "
                   "params not updated");
   }
-  if (!pd.fuse_scale) {
-    e = timed(c, 1, [&] {
-      return launch_scale(int(plan.probs.size()), pd.scale, c->partials, c->scales, o.eps, s);
-    });
-    if (e != hipSuccess) return hip_fail(c, e, "scale");
-  }
-  e = timed(c, 2, [&] {
-    return launch_pack(tm, tp, tn, aligned, int(plan.pack_tiles.size()), pd.pack_tiles, pd.pack, mats,
-                       c->mom, c->scales, c->partials, o.eps, pd.fuse_scale, c->mu, o.nesterov, s);
-  });
-  if (e != hipSuccess) return hip_fail(c, e, "pack");
-  const int nphases = int(plan.phases.size());
-  if ((e = span_mark(c, true, nphases)) != hipSuccess) return hip_fail(c, e, "profiling event");
-  for (int ph = 0; ph < nphases; ++ph) {
-    const GemmPhase& P = plan.phases[ph];
-    e = timed(c, 3 + P.kind, [&] {
-      return launch_ns_gemm(tn, P.variant, P.nn, int(P.tiles.size()), pd.descs, pd.phase_tiles[ph],
-                            P.nsplit, c->ksum, c->kcount, s);
-    });
-    if (e != hipSuccess) return hip_fail(c, e, "NS GEMM");
-  }
-  if ((e = span_mark(c, false, nphases)) != hipSuccess) return hip_fail(c, e, "profiling event");
-  const float eta = full ? c->lr_full : c->lr_block;
-  bool upd_vec = aligned;
-  e = timed(c, 6, [&] {
-    return launch_update(tp, tn, upd_vec, c->stream_nt, nsegs, c->segs, c->blocks, mats, pd.upd, eta,
-                         c->wd, s);
-  });
-  if (e != hipSuccess) return hip_fail(c, e, "update");
+  const char* what = "";
+  e = enqueue_after_momentum(o, c->lay.plan[full], c->pd[full].view(), b, sc, s, wrap,
+                             [&](bool begin, int n_launches) { return span_mark(c, begin, n_launches); },
+                             &what);
+  if (e != hipSuccess) return hip_fail(c, e, what);
   c->last_plan = full;
   return MUONBP_OK;
 }

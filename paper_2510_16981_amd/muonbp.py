@@ -20,7 +20,8 @@ NS_KINDS = ("gram", "poly", "apply")
 
 STATUS = {0: "MUONBP_OK", 1: "MUONBP_E_INVALID", 2: "MUONBP_E_SHAPE",
           3: "MUONBP_E_DTYPE", 4: "MUONBP_E_NOMEM", 5: "MUONBP_E_HIP",
-          6: "MUONBP_E_STATE", 7: "MUONBP_E_NONFINITE"}
+          6: "MUONBP_E_STATE", 7: "MUONBP_E_NONFINITE", 8: "MUONBP_E_TOO_LARGE"}
+STATIC_SCRATCH_BYTES = 128 << 20
 
 
 class MuonBPError(RuntimeError):
@@ -54,7 +55,8 @@ class PlanInfo(ctypes.Structure):
                 ("ns_dense_flops", ctypes.c_double),
                 ("elementwise_bytes", ctypes.c_double),
                 ("workspace_bytes", ctypes.c_int64),
-                ("gemm_split", ctypes.c_int32 * 3), ("apply_nn", ctypes.c_int32)]
+                ("gemm_split", ctypes.c_int32 * 3), ("apply_nn", ctypes.c_int32),
+                ("static_scratch_bytes", ctypes.c_int64)]
 
 
 class AdamwOptions(ctypes.Structure):
@@ -113,6 +115,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "muonbp_adamw_synchronize": (ctypes.c_int, [P]),
         "muonbp_adamw_last_error": (ctypes.c_char_p, [P]),
         "muonbp_adamw_destroy": (None, [P]),
+        "muonbp_step_static": (ctypes.c_int, [ctypes.POINTER(Matrix), I32, ctypes.POINTER(P),
+                                              ctypes.POINTER(P), P, I64, I64, F, F, F, F,
+                                              ctypes.POINTER(Options), P]),
         "muonbp_lr_cosine": (ctypes.c_double, [I64, I64, ctypes.c_double, ctypes.c_double, I64]),
         "muonbp_lr_wsd": (ctypes.c_double, [I64, I64, ctypes.c_double, ctypes.c_double, I64, I64]),
     }
@@ -164,6 +169,43 @@ def describe_plan(mats, full: bool, options: Optional[Options] = None) -> PlanIn
     if st:
         raise MuonBPError(st, "describe_plan")
     return info
+
+
+def step_static(mats, params: List, grads: List, momentum, step: int, period: int,
+                lr_block: float, lr_full: float, mu: float, weight_decay: float = 0.0,
+                options: Optional[Options] = None, stream=None) -> None:
+    """One allocation-free step (muonbp_step_static): the momentum is the
+    caller's ``momentum`` tensor (all matrices back to back, state dtype),
+    everything else lives in the library's static scratch array.  Returns
+    after the step has completed on ``stream``."""
+    import torch
+    lib = load_library()
+    mats = [tuple(int(v) for v in m) for m in mats]
+    n = len(mats)
+    if len(params) != n or len(grads) != n:
+        raise ValueError("one param and one grad per matrix")
+    opts = options if options is not None else options_default()
+    total = sum(r * c for r, c, _, _ in mats)
+    if not (momentum.is_cuda and momentum.is_contiguous() and momentum.numel() == total
+            and momentum.dtype == _torch_dtype(opts.state_dtype)):
+        raise ValueError(f"momentum: need a contiguous {_torch_dtype(opts.state_dtype)} CUDA "
+                         f"tensor of {total} elements")
+    for i, (r, c, _, _) in enumerate(mats):
+        for t in (params[i], grads[i]):
+            if not (t.is_cuda and t.is_contiguous() and t.dtype == _torch_dtype(opts.param_dtype)
+                    and tuple(t.shape) == (r, c)):
+                raise ValueError(f"matrix {i}: need contiguous {_torch_dtype(opts.param_dtype)} "
+                                 f"CUDA tensors of shape {(r, c)}")
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    pp = (ctypes.c_void_p * n)(*[p.data_ptr() for p in params])
+    gp = (ctypes.c_void_p * n)(*[g.data_ptr() for g in grads])
+    st = lib.muonbp_step_static(_mats(mats), n, pp, gp, ctypes.c_void_p(momentum.data_ptr()),
+                                int(step), int(period), float(lr_block), float(lr_full), float(mu),
+                                float(weight_decay), ctypes.byref(opts),
+                                ctypes.c_void_p(stream.cuda_stream))
+    if st:
+        raise MuonBPError(st, "muonbp_step_static")
 
 
 def _torch_dtype(code: int):

@@ -58,7 +58,7 @@ def test_options_default(lib):
 
 
 def test_status_strings(lib):
-    for code in range(8):
+    for code in range(9):
         assert lib.muonbp_status_string(code)
     assert lib.muonbp_last_error(None) == b"no context"
     lib.muonbp_destroy(None)  # NULL-safe
@@ -329,3 +329,31 @@ def test_adamw_create_rejects_bad_arguments_before_gpu(lib):
     assert lib.muonbp_adamw_grad_norm(None, None) == 1
     assert lib.muonbp_adamw_synchronize(None) == 1
     lib.muonbp_adamw_destroy(None)
+
+
+def test_static_step_refuses_on_the_host(lib):
+    """muonbp_step_static checks its arguments and the scratch its plan needs
+    before any HIP call (no GPU here): NULL arrays are E_INVALID, a step
+    larger than the static scratch array is E_TOO_LARGE.  The pointers are
+    never dereferenced on these paths."""
+    fake = (ctypes.c_void_p * 1)(256)
+    mats = mb._mats([(4096, 8192, 1, 1)])
+    args = (0, 1, 0.01, 0.02, 0.9, 0.0, None, None)
+    assert lib.muonbp_step_static(None, 1, fake, fake, ctypes.c_void_p(256), *args) == 1
+    assert lib.muonbp_step_static(mats, 1, None, fake, ctypes.c_void_p(256), *args) == 1
+    assert lib.muonbp_step_static(mats, 1, fake, fake, None, *args) == 1
+    assert lib.muonbp_step_static(mats, 1, fake, fake, ctypes.c_void_p(256), -1, 1, 0.01, 0.02,
+                                  0.9, 0.0, None, None) == 1
+    assert lib.muonbp_step_static(mats, 1, fake, fake, ctypes.c_void_p(256), *args) == 8
+    assert mb.describe_plan([(4096, 8192, 1, 1)], True).static_scratch_bytes > mb.STATIC_SCRATCH_BYTES
+    bad = (ctypes.c_void_p * 1)(257)  # not element-aligned
+    assert lib.muonbp_step_static(mats, 1, bad, fake, ctypes.c_void_p(256), *args) == 1
+
+
+def test_static_scratch_fits_the_qkv_workload(lib):
+    """The static scratch array is sized for one 2048 x 6144 matrix in
+    2048 x 768 shards, in both plans."""
+    mats = W.workload_matrices("qkv-2048x6144-bf16")
+    for full in (False, True):
+        info = mb.describe_plan(mats, full)
+        assert info.workspace_bytes < info.static_scratch_bytes <= mb.STATIC_SCRATCH_BYTES
