@@ -80,9 +80,8 @@ typedef struct {
   int32_t tile_policy;      /* NS GEMM kernel: 0 = chosen per launch from its
                                tile counts; 1/2/3 = 128x128 / 256x128 /
                                256x256 tiles with a register-staged K loop;
-                               4/5/6 = the same tiles with an LDS-DMA K loop
-                               (bf16 NS only, K a multiple of 8, else the
-                               register loop); 7 = 128x128 tiles with the K
+                               4/5/6 = the same as 8/9/10 (aliases kept for
+                               existing callers); 7 = 128x128 tiles with the K
                                loop split over two 4-wave groups; 8/9/10/
                                11/12/13 = 128x128 / 256x128 / 256x256 /
                                192x256 / 256x192 / 192x192 tiles with the

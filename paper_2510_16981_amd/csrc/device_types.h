@@ -7,12 +7,14 @@
 namespace muonbp {
 
 // Row segment of one block, the unit of work of the elementwise kernels
-// (momentum, update).  One workgroup per segment.
+// (momentum, update).  One workgroup per segment, in launch order; `slot` is
+// where the segment's sum of squares goes (the segments of one block have
+// consecutive slots, whatever their launch order).
 struct SegDesc {
   int32_t block;      // index into the block table
   int32_t row_begin;  // first row inside the block
   int32_t nrows;      // rows in this segment
-  int32_t pad;
+  int32_t slot;       // index of its partial sum
 };
 
 // One block of the shard grid (Sec. 3): a rows x cols window of a matrix.
@@ -70,7 +72,8 @@ struct GemmDesc {
 // register-staged K loop (any dtype, any K) or LDS-DMA K loop (bf16, K a
 // multiple of 8).
 // kGemm128x128Split2 runs two K halves of each tile in one 8-wave
-// workgroup; the DMA kernels keep 3 K slices in flight.
+// workgroup.  kGemmDma128x128 .. kGemmDma256x256 are kept as numbers only:
+// the planner turns them into the interleaved kernels of the same shapes.
 enum GemmVariant : int32_t {
   kGemm128x128 = 0, kGemm256x128 = 1, kGemm256x256 = 2,
   kGemmDma128x128 = 3, kGemmDma256x128 = 4, kGemmDma256x256 = 5,

@@ -201,7 +201,7 @@ __global__ __launch_bounds__(kThreads) void k_momentum(
     }
   }
   acc = block_sum(acc);
-  if (threadIdx.x == 0) partials[blockIdx.x] = acc;
+  if (threadIdx.x == 0) partials[sd.slot] = acc;
 }
 
 // ---------------------------------------------------------------- finite check
@@ -716,13 +716,13 @@ __global__ __launch_bounds__(kThreads * KS) void k_ns_gemm(const GemmDesc* __res
                            d, m0, n0, ti == tj && d.sym, d.alpha, d.beta, d.gamma, grp == 0);
 }
 
-// ---------------------------------------------------------------- NS GEMM, LDS-DMA pipeline
+// ---------------------------------------------------------------- NS GEMM, LDS-DMA staging
 //
-// bf16 variant of k_ns_gemm for units whose K is a multiple of 8.  Operand
+// The bf16 kernel below serves units whose K is a multiple of 8.  Operand
 // slices go straight from global memory into LDS (buffer_load_dwordx4 ...
 // lds: lane l of a wave writes 16 bytes at the wave's LDS window + 16 l),
-// through a ring of kStages stages of 32-element (64-byte) K slices, kStages
-// - 1 slices ahead of the MFMAs; no registers hold prefetched data.  Inside
+// through a ring of NS stages of 32-element (64-byte) K slices, NS - 1
+// slices ahead of the MFMAs; no registers hold prefetched data.  Inside
 // a stage a row occupies 64 bytes as four 16-byte chunks, chunk c stored at
 // position c ^ swz(row), swz(row) = ((row >> 1) & 3) ^ ((row >> 3) & 1), so
 // that any 8 (or 16) consecutive rows read at the same chunk by one MFMA
@@ -744,21 +744,6 @@ struct DmaShape {
   static constexpr int LDS_EPI = 4 * 32 * ST_PITCH * 4;
   static constexpr int LDS_BYTES = NS * STAGE > LDS_EPI ? NS * STAGE : LDS_EPI;
 };
-
-// Waits until at most `after` slices of LPW copies each are still in flight
-// for this wave (after in [0, MAXA]; s_waitcnt needs an immediate).
-template <int LPW, int MAXA>
-__device__ __forceinline__ void wait_slices(int after) {
-  if constexpr (MAXA > 0) {
-    if (after >= MAXA) {
-      __builtin_amdgcn_s_waitcnt(vmcnt_imm(MAXA * LPW));
-      return;
-    }
-    wait_slices<LPW, MAXA - 1>(after);
-  } else {
-    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
-  }
-}
 
 typedef __attribute__((address_space(3))) void lds_void_t;
 
@@ -828,110 +813,11 @@ __device__ __forceinline__ uint32_t lds_addr(const unsigned char* p) {
   return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const lds_void_t*)p));
 }
 
-template <int BM, int BN, int NS>
-__global__ __launch_bounds__(kThreads) void k_ns_gemm_dma(const GemmDesc* __restrict__ probs,
-                                                          const TileRef* __restrict__ tiles) {
-  using G = DmaShape<BM, BN, NS>;
-  using T = bf16;
-  constexpr int TM = G::TM, TN = G::TN, LPW = G::LPW, ES = 2, NF = TM + TN;
-  __shared__ __attribute__((aligned(1024))) unsigned char lds[G::LDS_BYTES];
-
-  const TileRef t = tiles[blockIdx.x];
-  const GemmDesc d = probs[t.prob];
-  const int ti = t.ij >> 16, tj = t.ij & 0xffff;
-  const int m0 = ti * BM, n0 = tj * BN;
-  const int tid = threadIdx.x, lane = tid & 63;
-  // The wave index is uniform across the wave; saying so keeps the LDS
-  // window of each copy (held in M0) in a scalar register.
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave >> 1, wn = wave & 1;
-
-  const int xbytes = d.M * d.ldx * ES, ybytes = d.N * d.ldy * ES;
-  const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(d.X), 0, xbytes, kBufferWord3);
-  const __amdgpu_buffer_rsrc_t yr = __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(d.Y), 0, ybytes, kBufferWord3);
-
-  // This lane's share of every stage: copy u = wave + 4 jj covers staged rows
-  // [16 u, 16 u + 16) (X rows first, then Y rows); the lane fills row
-  // 16 u + lane / 4 at physical chunk lane % 4.
-  int voff[LPW], chunk[LPW];
-#pragma unroll
-  for (int jj = 0; jj < LPW; ++jj) {
-    const int u = wave + 4 * jj;
-    const int row = 16 * u + (lane >> 2);  // stage row (X rows, then Y rows)
-    const int c = (lane & 3) ^ swz(row);
-    chunk[jj] = c;
-    voff[jj] = row < BM ? ((m0 + row) * d.ldx + 8 * c) * ES : ((n0 + row - BM) * d.ldy + 8 * c) * ES;
-  }
-  const int nk = (d.K + 31) / 32;
-  auto issue = [&](int kt) {
-    unsigned char* base = lds + (kt % NS) * G::STAGE;
-    const int k0 = kt * 32;
-#pragma unroll
-    for (int jj = 0; jj < LPW; ++jj) {
-      const bool kin = k0 + 8 * chunk[jj] < d.K;
-      lds_void_t* dst = (lds_void_t*)(base + (wave + 4 * jj) * 1024);
-      if (wave + 4 * jj < BM / 16)  // uniform: X rows
-        dma16(xr, dst, kin ? voff[jj] : xbytes, k0 * ES);
-      else
-        dma16(yr, dst, kin ? voff[jj] : ybytes, k0 * ES);
-    }
-  };
-
-  f32x16_t acc[TM][TN];
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
-
-#pragma unroll
-  for (int s = 0; s < NS - 1; ++s)
-    if (s < nk) issue(s);
-
-  // LDS byte addresses of this lane's fragment rows in stage 0 (chunk
-  // position added per K step).
-  uint32_t fa[NF];
-  int fsw[NF];
-#pragma unroll
-  for (int f = 0; f < NF; ++f) {
-    const int r = f < TM ? wm * 32 * TM + 32 * f + (lane & 31) : BM + wn * 32 * TN + 32 * (f - TM) + (lane & 31);
-    fa[f] = lds_addr(lds) + r * kDmaRow;
-    fsw[f] = swz(r);
-  }
-  for (int kt = 0; kt < nk; ++kt) {
-    // Wait until this wave's copies of slice kt have landed (slices issued
-    // later may stay in flight), make every wave's copies visible, refill
-    // the stage consumed one slice ago, then multiply.
-    wait_slices<LPW, NS - 2>(min(nk - 1, kt + NS - 2) - kt);
-    barrier_no_fence();
-    if (kt + NS - 1 < nk) issue(kt + NS - 1);
-    const uint32_t sbase = (kt % NS) * G::STAGE;
-#pragma unroll
-    for (int s = 0; s < 2; ++s) {
-      const int c = 2 * s + (lane >> 5);
-      u32x4_t fr[NF];
-#pragma unroll
-      for (int f = 0; f < NF; ++f) fr[f] = lds_read16(fa[f] + sbase + ((c ^ fsw[f]) << 4));
-      lds_wait(fr);
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-          acc[i][j] = Mfma<T>::step(__builtin_bit_cast(uint4, fr[i]), __builtin_bit_cast(uint4, fr[TM + j]),
-                                    acc[i][j]);
-    }
-  }
-  __syncthreads();
-  gemm_epilogue<T, TM, TN>(acc, reinterpret_cast<float*>(lds) + wave * 32 * (32 * TN + 1), d, m0, n0,
-                           ti == tj && d.sym, d.alpha, d.beta, d.gamma);
-}
-
 // ---------------------------------------------------------------- NS GEMM, interleaved DMA pipeline
 //
-// Same operand staging as k_ns_gemm_dma (4-stage ring of 32-element K
-// slices, straight from global memory into LDS), but scheduled so that the
-// matrix pipeline never drains at a slice boundary:
+// The operands are staged as described above (a 4-stage ring of 32-element
+// K slices, straight from global memory into LDS), and the loop is
+// scheduled so that the matrix pipeline never drains at a slice boundary:
 //
 //   * both K steps of a slice are read from LDS one step ahead, each read
 //     issued between two MFMAs of the previous step;
@@ -1555,23 +1441,6 @@ hipError_t launch_ns_gemm(DType ns_t, int variant, bool nn, int n_tiles, const G
             default: MUONBP_DMAP(192, 192, 2, 2); break;
           }
 #undef MUONBP_DMAP
-          break;
-        } else {
-          return hipErrorInvalidValue;
-        }
-      case kGemmDma128x128:
-      case kGemmDma256x128:
-      case kGemmDma256x256:
-        if constexpr (std::is_same<TN, bf16>::value) {
-          if (variant == kGemmDma128x128)
-            hipLaunchKernelGGL((k_ns_gemm_dma<128, 128, 4>), dim3(n_tiles), dim3(kThreads), 0, s,
-                               probs, tiles);
-          else if (variant == kGemmDma256x128)
-            hipLaunchKernelGGL((k_ns_gemm_dma<256, 128, 4>), dim3(n_tiles), dim3(kThreads), 0, s,
-                               probs, tiles);
-          else
-            hipLaunchKernelGGL((k_ns_gemm_dma<256, 256, 4>), dim3(n_tiles), dim3(kThreads), 0, s,
-                               probs, tiles);
           break;
         } else {
           return hipErrorInvalidValue;

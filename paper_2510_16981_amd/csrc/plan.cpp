@@ -204,6 +204,10 @@ int32_t choose_variant(const std::vector<Problem>& probs, GemmKind kind, int til
   const bool dma = dma_allowed(probs, kind, ns_elem_bytes);
   if (tile_policy > 0) {
     int v = tile_policy - 1;
+    // The block-ordered LDS-DMA loop these variants named was removed (the
+    // interleaved loop of the same tile shape was 20-25% faster on every
+    // launch): they select the interleaved kernel.
+    if (v >= kGemmDma128x128 && v <= kGemmDma256x256) v += kGemmDmaP128x128 - kGemmDma128x128;
     // Symmetric products take square tiles; without the DMA path, the
     // register K loop on the same (or, for 192-wide tiles, the nearest) shape.
     if (sym && kGemmTileRows[v] != kGemmTileCols[v]) {
@@ -334,11 +338,34 @@ std::string build_layout(const MatrixShape* mats, int32_t n_mats,
           if (L.segs.size() >= size_t(std::numeric_limits<int32_t>::max()))
             return "too many segments";
           L.segs.push_back(SegDesc{int32_t(L.blocks.size()), int32_t(r),
-                                   int32_t(std::min(rows_per_seg, br - r)), 0});
+                                   int32_t(std::min(rows_per_seg, br - r)),
+                                   int32_t(L.segs.size())});
         }
         b.seg_end = int32_t(L.segs.size());
         L.blocks.push_back(b);
       }
+  }
+  // Launch order: the r-th segment of every block of one block row of a
+  // matrix, then the (r+1)-th, ...  For a column-sharded matrix the
+  // workgroups that run together then cover whole rows of the matrix instead
+  // of one block's narrow row pieces (a 4096 x 1024 matrix in 8 shards has
+  // 256-byte pieces of 2 KB rows); for a single column of blocks it is the
+  // block order.
+  {
+    std::vector<SegDesc> order;
+    order.reserve(L.segs.size());
+    int32_t bi = 0;
+    for (int32_t k = 0; k < n_mats; ++k) {
+      const MatrixShape& m = mats[k];
+      for (int32_t i = 0; i < m.grid_rows; ++i) {
+        const int32_t b0 = bi + i * m.grid_cols;
+        const int32_t nseg = L.blocks[b0].seg_end - L.blocks[b0].seg_begin;
+        for (int32_t r = 0; r < nseg; ++r)
+          for (int32_t j = 0; j < m.grid_cols; ++j) order.push_back(L.segs[L.blocks[b0 + j].seg_begin + r]);
+      }
+      bi += m.grid_rows * m.grid_cols;
+    }
+    L.segs.swap(order);
   }
 
   const int64_t align_elems = kWsAlignBytes / ns_elem_bytes;

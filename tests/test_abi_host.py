@@ -283,7 +283,9 @@ def test_apply_reads_z_row_major_where_the_dma_kernel_runs(lib):
         assert mb.describe_plan(mats, full, mb.options_default(apply_mode=1)).apply_nn == 0
         assert mb.describe_plan(mats, full, mb.options_default(ns_dtype=0)).apply_nn == 0
         assert mb.describe_plan(mats, full, mb.options_default(tile_policy=3)).apply_nn == 0
-        assert mb.describe_plan(mats, full, mb.options_default(tile_policy=6)).apply_nn == 0
+        # Policy 6 is an alias of 10 (interleaved DMA, 256 x 256 tiles).
+        assert mb.describe_plan(mats, full, mb.options_default(tile_policy=6)).apply_nn == \
+            mb.describe_plan(mats, full, mb.options_default(tile_policy=10)).apply_nn
         assert mb.describe_plan(mats, full, mb.options_default(tile_policy=11)).apply_nn == 1
 
 
@@ -357,3 +359,4 @@ def test_static_scratch_fits_the_qkv_workload(lib):
     for full in (False, True):
         info = mb.describe_plan(mats, full)
         assert info.workspace_bytes < info.static_scratch_bytes <= mb.STATIC_SCRATCH_BYTES
+
