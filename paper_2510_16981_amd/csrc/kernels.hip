@@ -123,7 +123,7 @@ template <bool NT> __device__ __forceinline__ void store8r(float* p, const float
 
 // Chunks of 8 elements each thread of an elementwise kernel loads before it
 // does any arithmetic (memory-level parallelism of the streaming loops).
-constexpr int kStreamUnroll = 4;
+constexpr int kStreamUnroll = 8;
 
 // Deterministic workgroup sum (fixed butterfly inside each wave, fixed
 // wave order across the workgroup).

@@ -247,6 +247,7 @@ const char* muonbp_status_string(muonbp_status s) {
     case MUONBP_E_HIP: return "HIP error";
     case MUONBP_E_STATE: return "context unusable after an earlier HIP error";
     case MUONBP_E_NONFINITE: return "non-finite orthogonalization input";
+    case MUONBP_E_TOO_LARGE: return "step needs more than the static scratch array";
   }
   return "unknown status";
 }

@@ -75,13 +75,19 @@ _lib = None
 
 
 def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
-    """Load the HIP library (raises when it has not been built)."""
+    """Load the HIP library (raises when it has not been built).
+
+    torch is imported first: its wheel ships its own HIP runtime under the
+    same soname as the system one, and the library must bind to the runtime
+    that owns torch's memory and streams (loaded the other way round, the
+    process would end up with two runtimes)."""
     global _lib
     if _lib is not None:
         return _lib
     if not os.path.exists(path):
         raise RuntimeError(
             f"{path} is missing: build it with `python -m paper_2510_16981_amd.build`")
+    import torch  # noqa: F401  (see above)
     lib = ctypes.CDLL(path)
     P, I32, I64, F = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float
     sig = {

@@ -58,8 +58,9 @@ def test_options_default(lib):
 
 
 def test_status_strings(lib):
-    for code in range(9):
-        assert lib.muonbp_status_string(code)
+    texts = [lib.muonbp_status_string(code) for code in range(9)]
+    assert all(texts) and b"unknown status" not in texts and len(set(texts)) == 9
+    assert lib.muonbp_status_string(99) == b"unknown status"
     assert lib.muonbp_last_error(None) == b"no context"
     lib.muonbp_destroy(None)  # NULL-safe
 
