@@ -307,6 +307,12 @@ muonbp_status muonbp_step_static(const muonbp_matrix* mats, int32_t n_mats, void
  *   m <- beta1 m + (1 - beta1) g,   v <- beta2 v + (1 - beta2) g^2
  *   p <- p (1 - lr wd) - lr (m / (1 - beta1^t)) / (sqrt(v / (1 - beta2^t)) + eps)
  * with t = step + 1.  The moments are fp32 and owned by the context.
+ * The same context runs Lion instead (algorithm = 1), the scalar optimizer
+ * of the paper's 160M comparison (Sec. 4), as Chen et al. (2023) define it:
+ *   c <- beta1 m + (1 - beta1) g,   p <- p (1 - lr wd) - lr sign(c),
+ *   m <- beta2 m + (1 - beta2) g
+ * (after the same clipping; sign(0) = 0; eps and v are not used; the
+ * defaults below are AdamW's, Lion is usually run with betas (0.9, 0.99)).
  * The conventions of the MuonBP functions above apply (status codes,
  * asynchrony on the context's stream, pointer alignment, thread safety).
  * ---------------------------------------------------------------------- */
@@ -320,6 +326,7 @@ typedef struct {
   muonbp_dtype param_dtype; /* dtype of params and grads                       */
   int32_t stream_hint;      /* cache policy of the streamed accesses, as
                                muonbp_options.stream_hint (0 = by size)        */
+  int32_t algorithm;        /* 0 = AdamW, 1 = Lion                             */
 } muonbp_adamw_options;
 
 /* Defaults: beta1 0.9, beta2 0.95, eps 1e-8, weight decay 0.1, clipping at

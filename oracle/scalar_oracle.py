@@ -22,6 +22,14 @@ and the input embedding) with AdamW, clips their gradients to a global norm of
                           p <- p - lr m_hat / (sqrt(v_hat) + eps),
                       m_hat = m / (1 - b1^t), v_hat = v / (1 - b2^t), t = the
                       number of updates so far including this one.
+* ``lion_step``    -- one Lion iteration, the scalar optimizer of the paper's
+                      160M comparison (Sec. 4, "Lion as the scalar optimizer in
+                      line with the codebase"); the paper does not print it, so
+                      it follows its definition by Chen et al. (2023), with
+                      decoupled weight decay and the same clipping:
+                          c = b1 m + (1 - b1) g,
+                          p <- p (1 - lr wd) - lr sign(c),
+                          m <- b2 m + (1 - b2) g.
 * ``lr_cosine``, ``lr_wsd`` -- the two schedules.
 
 Readings taken where the paper is silent (listed in the design notes):
@@ -76,6 +84,23 @@ def adamw_step(params: List[np.ndarray], grads: Sequence[np.ndarray], m: List[np
         out_m.append(mi)
         out_v.append(vi)
     return out_p, out_m, out_v
+
+
+def lion_step(params: List[np.ndarray], grads: Sequence[np.ndarray], m: List[np.ndarray], lr: float,
+              beta1: float = 0.9, beta2: float = 0.99, weight_decay: float = 0.1,
+              max_norm: float = 1.0):
+    """One Lion update of every tensor.  Returns (params, m) as new float64
+    arrays.  sign(0) = 0 (numpy's sign; a NaN stays NaN)."""
+    c_clip = clip_factor(grads, max_norm)
+    out_p, out_m = [], []
+    for p, g, mi in zip(params, grads, m):
+        p = np.asarray(p, dtype=np.float64)
+        g = c_clip * np.asarray(g, dtype=np.float64)
+        mi = np.asarray(mi, dtype=np.float64)
+        direction = np.sign(beta1 * mi + (1.0 - beta1) * g)
+        out_p.append(p * (1.0 - lr * weight_decay) - lr * direction)
+        out_m.append(beta2 * mi + (1.0 - beta2) * g)
+    return out_p, out_m
 
 
 def lr_cosine(t: int, total: int, lr_max: float, lr_min: float = 0.0, warmup: int = 0) -> float:

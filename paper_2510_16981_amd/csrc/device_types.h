@@ -118,12 +118,13 @@ struct ScalarSeg {
   int64_t state;   // arena offset of element `begin`
 };
 
-// Per-step scalars of the AdamW kernel (computed on the host in double).
+// Per-step scalars of the AdamW and Lion kernels (computed on the host in
+// double).
 struct AdamwArgs {
   float beta1, beta2, eps;
   float decay;         // 1 - lr * weight_decay
-  float step;          // lr / (1 - beta1^t)
-  float inv_sqrt_bc2;  // 1 / sqrt(1 - beta2^t)
+  float step;          // AdamW: lr / (1 - beta1^t); Lion: lr
+  float inv_sqrt_bc2;  // AdamW: 1 / sqrt(1 - beta2^t)
 };
 
 }  // namespace muonbp

@@ -74,10 +74,11 @@ hipError_t launch_adamw_sumsq(DType param_t, bool vec, bool nt, int n_segs, cons
 // clip[1] = ||g||, from the n partial sums of the norm pass.
 hipError_t launch_adamw_clip(const float* partials, int n, float max_norm, float* clip,
                              hipStream_t s);
-// The AdamW update of params and of the fp32 moments m and v; gradients are
-// scaled by clip[0] when clip is not NULL.
+// The AdamW update of params and of the fp32 moments m and v, or (lion) the
+// Lion update of params and m; gradients are scaled by clip[0] when clip is
+// not NULL.
 hipError_t launch_adamw(DType param_t, bool vec, bool nt, int n_segs, const ScalarSeg* segs,
                         const MatPtrs* ptrs, float* m, float* v, const float* clip,
-                        const AdamwArgs& a, hipStream_t s);
+                        const AdamwArgs& a, bool lion, hipStream_t s);
 
 }  // namespace muonbp

@@ -1263,9 +1263,19 @@ __device__ __forceinline__ void adamw_elem(float& p, float g, float& m, float& v
   p = fmaf(p, a.decay, -a.step * (m / fmaf(sqrtf(v), a.inv_sqrt_bc2, a.eps)));
 }
 
+// Lion (Chen et al., 2023): c = b1 m + (1 - b1) g; p <- p (1 - lr wd) -
+// lr sign(c); m <- b2 m + (1 - b2) g.  sign(0) = 0, and a NaN in c stays NaN.
+__device__ __forceinline__ void lion_elem(float& p, float g, float& m, const AdamwArgs& a) {
+  const float c = fmaf(a.beta1, m, (1.f - a.beta1) * g);
+  const float sg = c > 0.f ? 1.f : (c < 0.f ? -1.f : c * 0.f);
+  p = fmaf(p, a.decay, -a.step * sg);
+  m = fmaf(a.beta2, m, (1.f - a.beta2) * g);
+}
+
 constexpr int kAdamwUnroll = 4;  // chunks of 8 elements in flight per thread
 
-template <typename TP, bool VEC, bool NT>
+// LION: the Lion update (v is neither read nor written).
+template <typename TP, bool VEC, bool NT, bool LION>
 __global__ __launch_bounds__(kThreads) void k_adamw(const ScalarSeg* __restrict__ segs,
                                                     const MatPtrs* __restrict__ ptrs,
                                                     float* __restrict__ m, float* __restrict__ v,
@@ -1287,7 +1297,7 @@ __global__ __launch_bounds__(kThreads) void k_adamw(const ScalarSeg* __restrict_
         pr[u] = load8r<NT>(p + 8 * k);
         gr[u] = load8r<NT>(g + 8 * k);
         mr[u] = load8r<NT>(ms + 8 * k);
-        vr[u] = load8r<NT>(vs + 8 * k);
+        if (!LION) vr[u] = load8r<NT>(vs + 8 * k);
       }
     }
 #pragma unroll
@@ -1298,21 +1308,31 @@ __global__ __launch_bounds__(kThreads) void k_adamw(const ScalarSeg* __restrict_
         unpack8(pr[u], pf);
         unpack8(gr[u], gf);
         unpack8(mr[u], mf);
-        unpack8(vr[u], vf);
+        if (LION) {
 #pragma unroll
-        for (int i = 0; i < 8; ++i) adamw_elem(pf[i], c * gf[i], mf[i], vf[i], a);
+          for (int i = 0; i < 8; ++i) lion_elem(pf[i], c * gf[i], mf[i], a);
+        } else {
+          unpack8(vr[u], vf);
+#pragma unroll
+          for (int i = 0; i < 8; ++i) adamw_elem(pf[i], c * gf[i], mf[i], vf[i], a);
+        }
         store8r<NT>(p + 8 * k, pf);
         store8r<NT>(ms + 8 * k, mf);
-        store8r<NT>(vs + 8 * k, vf);
+        if (!LION) store8r<NT>(vs + 8 * k, vf);
       }
     }
   }
   for (int e = 8 * nv + threadIdx.x; e < n; e += kThreads) {
-    float pf = to_f<TP>(p[e]), mf = ms[e], vf = vs[e];
-    adamw_elem(pf, c * to_f<TP>(g[e]), mf, vf, a);
+    float pf = to_f<TP>(p[e]), mf = ms[e];
+    if (LION) {
+      lion_elem(pf, c * to_f<TP>(g[e]), mf, a);
+    } else {
+      float vf = vs[e];
+      adamw_elem(pf, c * to_f<TP>(g[e]), mf, vf, a);
+      vs[e] = vf;
+    }
     p[e] = from_f<TP>(pf);
     ms[e] = mf;
-    vs[e] = vf;
   }
 }
 
@@ -1504,20 +1524,24 @@ hipError_t launch_adamw_clip(const float* partials, int n, float max_norm, float
 
 hipError_t launch_adamw(DType param_t, bool vec, bool nt, int n_segs, const ScalarSeg* segs,
                         const MatPtrs* ptrs, float* m, float* v, const float* clip,
-                        const AdamwArgs& a, hipStream_t s) {
+                        const AdamwArgs& a, bool lion, hipStream_t s) {
   if (n_segs <= 0) return hipSuccess;
   return dispatch1(param_t, [&](auto p) {
     using TP = decltype(p);
-    if (vec && nt)
-      hipLaunchKernelGGL((k_adamw<TP, true, true>), dim3(n_segs), dim3(kThreads), 0, s, segs, ptrs,
-                         m, v, clip, a);
-    else if (vec)
-      hipLaunchKernelGGL((k_adamw<TP, true, false>), dim3(n_segs), dim3(kThreads), 0, s, segs, ptrs,
-                         m, v, clip, a);
-    else
-      hipLaunchKernelGGL((k_adamw<TP, false, false>), dim3(n_segs), dim3(kThreads), 0, s, segs,
-                         ptrs, m, v, clip, a);
-    return hipGetLastError();
+    auto go = [&](auto lion_tag) {
+      constexpr bool L = decltype(lion_tag)::value;
+      if (vec && nt)
+        hipLaunchKernelGGL((k_adamw<TP, true, true, L>), dim3(n_segs), dim3(kThreads), 0, s, segs, ptrs,
+                           m, v, clip, a);
+      else if (vec)
+        hipLaunchKernelGGL((k_adamw<TP, true, false, L>), dim3(n_segs), dim3(kThreads), 0, s, segs,
+                           ptrs, m, v, clip, a);
+      else
+        hipLaunchKernelGGL((k_adamw<TP, false, false, L>), dim3(n_segs), dim3(kThreads), 0, s, segs,
+                           ptrs, m, v, clip, a);
+      return hipGetLastError();
+    };
+    return lion ? go(std::true_type{}) : go(std::false_type{});
   });
 }
 

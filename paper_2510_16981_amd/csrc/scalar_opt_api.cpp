@@ -1,6 +1,7 @@
 // C ABI of the scalar optimizer (AdamW with global-norm clipping) that the
 // paper's training setup applies to the parameters MuonBP does not
-// orthogonalize (Appendix B), and of the learning-rate schedules of its runs.
+// orthogonalize (Appendix B), or Lion (the scalar optimizer of its 160M
+// comparison, Sec. 4), and of the learning-rate schedules of its runs.
 #include <hip/hip_runtime_api.h>
 
 #include <algorithm>
@@ -76,6 +77,7 @@ std::string validate(const muonbp_adamw_options& o) {
   if (o.eps < 0.f) return "eps must be >= 0";
   if (o.max_grad_norm < 0.f) return "max_grad_norm must be >= 0";
   if (o.stream_hint < 0 || o.stream_hint > 2) return "stream_hint out of range";
+  if (o.algorithm != 0 && o.algorithm != 1) return "algorithm must be 0 (AdamW) or 1 (Lion)";
   return "";
 }
 
@@ -139,8 +141,9 @@ muonbp_status muonbp_adamw_create(const int64_t* sizes, int32_t n, const muonbp_
   }
   c->n_segs = int32_t(segs.size());
   // Nontemporal accesses once a step streams more than the last-level cache
-  // holds: params, grads, m and v read, params, m and v written.
-  const int64_t streamed = c->state_elems * int64_t(2 * elem_size(o.param_dtype) + 16);
+  // holds: params, grads, m and v read, params, m and v written (Lion: no v).
+  const int64_t streamed =
+      c->state_elems * int64_t(2 * elem_size(o.param_dtype) + (o.algorithm == 1 ? 8 : 16));
   c->stream_nt = o.stream_hint == 2 || (o.stream_hint == 0 && streamed > kStreamNtBytes);
 
   hipError_t e;
@@ -205,7 +208,8 @@ muonbp_status muonbp_adamw_step(muonbp_adamw_ctx* c, void* const* params, const 
         hipSuccess)
       return hip_fail(c, e, "clipping factor");
   }
-  // Bias corrections of step t = step + 1, in double on the host.
+  // Bias corrections of step t = step + 1 (AdamW), in double on the host.
+  const bool lion = c->opt.algorithm == 1;
   const double t = double(step) + 1.0;
   const double bc1 = 1.0 - std::pow(double(c->opt.beta1), t);
   const double bc2 = 1.0 - std::pow(double(c->opt.beta2), t);
@@ -214,11 +218,11 @@ muonbp_status muonbp_adamw_step(muonbp_adamw_ctx* c, void* const* params, const 
   a.beta2 = c->opt.beta2;
   a.eps = c->opt.eps;
   a.decay = float(1.0 - double(lr) * double(c->opt.weight_decay));
-  a.step = float(double(lr) / bc1);
+  a.step = lion ? lr : float(double(lr) / bc1);
   a.inv_sqrt_bc2 = float(1.0 / std::sqrt(bc2));
   if ((e = launch_adamw(tp, aligned, c->stream_nt, c->n_segs, c->segs, c->ptrs.current(), c->m, c->v,
-                        clipping ? c->clip : nullptr, a, c->stream)) != hipSuccess)
-    return hip_fail(c, e, "AdamW update");
+                        clipping ? c->clip : nullptr, a, lion, c->stream)) != hipSuccess)
+    return hip_fail(c, e, lion ? "Lion update" : "AdamW update");
   c->norm_valid = clipping;
   return MUONBP_OK;
 }

@@ -62,7 +62,8 @@ class PlanInfo(ctypes.Structure):
 class AdamwOptions(ctypes.Structure):
     _fields_ = [("beta1", ctypes.c_float), ("beta2", ctypes.c_float), ("eps", ctypes.c_float),
                 ("weight_decay", ctypes.c_float), ("max_grad_norm", ctypes.c_float),
-                ("param_dtype", ctypes.c_int), ("stream_hint", ctypes.c_int32)]
+                ("param_dtype", ctypes.c_int), ("stream_hint", ctypes.c_int32),
+                ("algorithm", ctypes.c_int32)]
 
 
 class Profile(ctypes.Structure):

@@ -307,6 +307,7 @@ def test_adamw_options_default(lib):
     assert (o.beta1, o.beta2) == pytest.approx((0.9, 0.95))
     assert o.eps == pytest.approx(1e-8) and o.weight_decay == pytest.approx(0.1)
     assert o.max_grad_norm == 1.0 and o.param_dtype == mb.BF16 and o.stream_hint == 0
+    assert o.algorithm == 0
 
 
 def test_adamw_create_rejects_bad_arguments_before_gpu(lib):
@@ -326,6 +327,8 @@ def test_adamw_create_rejects_bad_arguments_before_gpu(lib):
     assert create([10], max_grad_norm=-1.0)[0] == 1
     assert create([10], weight_decay=float("nan"))[0] == 1
     assert create([10], stream_hint=3)[0] == 1
+    assert create([10], algorithm=2)[0] == 1
+    assert create([10], algorithm=-1)[0] == 1
     assert create([10], param_dtype=7)[0] == 3
     assert lib.muonbp_adamw_create(None, 1, None, None, ctypes.byref(ctypes.c_void_p())) == 1
     assert lib.muonbp_adamw_step(None, None, None, 0, 0.1) == 1

@@ -20,6 +20,7 @@ STRUCTS = {
     "muonbp_options": mb.Options,
     "muonbp_plan_info": mb.PlanInfo,
     "muonbp_profile": mb.Profile,
+    "muonbp_adamw_options": mb.AdamwOptions,
 }
 
 

@@ -144,3 +144,82 @@ def test_adamw_deterministic_and_resumable():
     for o, _ in runs:
         o.close()
     opt2.close()
+
+
+# ---------------------------------------------------------------- Lion
+
+L_B1, L_B2 = 0.9, 0.99
+
+
+def _run_lion(sizes, dtype, max_norm, grad_scale, steps=4, offset=0):
+    """Teacher-forced Lion steps against the oracle.  sign(c) is an integer
+    decision taken from a float: where the oracle's fp64 c lies within fp32
+    rounding of zero either sign is a valid result, so those elements are
+    checked only for being p (1 - lr wd) - lr s with s in {-1, 0, 1}; every
+    other element is compared with the oracle directly."""
+    import torch
+    from paper_2510_16981_amd import muonbp as mb
+    code = {"f32": mb.F32, "bf16": mb.BF16}[dtype]
+    opt = mb.AdamW(sizes, mb.adamw_options_default(param_dtype=code, max_grad_norm=max_norm,
+                                                   algorithm=1, beta1=L_B1, beta2=L_B2))
+    params_h, grads_h = _inputs(sizes, 4, dtype, steps, grad_scale)
+    bufs = [torch.zeros(n + offset, dtype=p.dtype, device="cuda") for n, p in zip(sizes, params_h)]
+    params = [b[offset:] for b in bufs]
+    for p, h in zip(params, params_h):
+        p.copy_(h)
+    worst = {"p": 0.0, "m": 0.0, "v": 0.0, "undecided": 0}
+    lrs = [mb.lr_wsd(t, steps, 1e-2, 1e-3, 0, 2) for t in range(steps)]
+    for t in range(steps):
+        x0 = [p.double().cpu().numpy() for p in params]
+        m0 = [opt.get_state(i)[0].double().cpu().numpy() for i in range(len(sizes))]
+        g64 = [gg.double().numpy() for gg in grads_h[t]]
+        opt.step(params, [gg.cuda() for gg in grads_h[t]], t, lrs[t])
+        torch.cuda.synchronize()
+        xr, mr = S.lion_step(x0, g64, m0, lrs[t], L_B1, L_B2, WD, max_norm)
+        st = [opt.get_state(i) for i in range(len(sizes))]
+        x = np.concatenate([p.double().cpu().numpy() for p in params])
+        m = np.concatenate([a.double().cpu().numpy() for a, _ in st])
+        v = np.concatenate([b.double().cpu().numpy() for _, b in st])
+        worst["m"] = max(worst["m"], rel(m, np.concatenate(mr)))
+        worst["v"] = max(worst["v"], float(np.abs(v).max()))  # Lion never writes v
+        # Which elements have a sign fixed beyond fp32 rounding.
+        clip = S.clip_factor(g64, max_norm)
+        mc, gc = np.concatenate(m0), clip * np.concatenate(g64)
+        c = L_B1 * mc + (1 - L_B1) * gc
+        slack = 1e-6 * (np.abs(L_B1 * mc) + np.abs((1 - L_B1) * gc)) + 1e-30
+        decided = np.abs(c) > slack
+        xrc, x0c = np.concatenate(xr), np.concatenate(x0)
+        decayed = x0c * (1 - lrs[t] * WD)
+        if dtype == "f32":
+            err = np.abs(x - xrc)[decided]
+            bound = 4e-7 * (np.abs(xrc) + lrs[t])[decided]
+        else:
+            rounded = torch.from_numpy(xrc).to(torch.bfloat16).double().numpy()
+            err = np.abs(x - xrc)[decided]
+            bound = (2 * np.abs(rounded - xrc) + 1e-3 * lrs[t])[decided]
+        worst["p"] = max(worst["p"], float(np.max(err / bound)) if err.size else 0.0)
+        und = ~decided
+        worst["undecided"] += int(und.sum())
+        if und.any():
+            tol = 1e-2 * lrs[t] + (0 if dtype == "f32" else 8e-3 * np.abs(decayed[und]))
+            gap = np.min(np.abs(x[und][:, None] - (decayed[und][:, None] - lrs[t] * np.array([-1, 0, 1]))),
+                         axis=1)
+            assert np.all(gap <= tol), "an undecided element is not p (1 - lr wd) - lr s"
+    opt.close()
+    return worst
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("max_norm,grad_scale", [(0.0, 1.0), (1.0, 25.0)], ids=["no-clip", "clipped"])
+def test_lion_parity(dtype, max_norm, grad_scale):
+    announce(f"lion {dtype} clip {max_norm} scale {grad_scale}")
+    w = _run_lion(SIZES, dtype, max_norm, grad_scale)
+    announce(f"worst {w}")
+    assert w["m"] <= F32_TOL and w["v"] == 0.0
+    assert w["p"] <= 1.0
+
+
+def test_lion_unaligned_pointers():
+    announce("lion f32 offset pointers")
+    w = _run_lion(SIZES, "f32", 1.0, 25.0, steps=2, offset=1)
+    assert w["m"] <= F32_TOL and w["p"] <= 1.0

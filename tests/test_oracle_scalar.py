@@ -129,3 +129,81 @@ def test_wsd_schedule_boundaries():
     assert S.lr_wsd(T, T, hi, lo, 0, 0) == hi
     assert S.lr_wsd(3, T, hi, lo, warmup=4, decay=D) == hi
     assert S.lr_wsd(1, T, hi, lo, warmup=4, decay=D) == hi / 2
+
+
+# ---------------------------------------------------------------- Lion
+
+def test_lion_reduces_to_sign_descent_without_momentum():
+    """beta1 = beta2 = 0: c = g, so the step is p (1 - lr wd) - lr sign(g)
+    (clipping scales g and does not change its sign)."""
+    rng = np.random.default_rng(3)
+    p = [rng.standard_normal(37)]
+    g = [rng.standard_normal(37)]
+    g[0][5] = 0.0
+    out_p, out_m = S.lion_step(p, g, [np.zeros(37)], lr=0.03, beta1=0.0, beta2=0.0,
+                               weight_decay=0.1, max_norm=1.0)
+    want = p[0] * (1 - 0.03 * 0.1) - 0.03 * np.sign(g[0])
+    assert np.allclose(out_p[0], want, rtol=0, atol=1e-15)
+    assert out_p[0][5] == p[0][5] * (1 - 0.003)  # sign(0) = 0
+    assert np.allclose(out_m[0], S.clip_factor(g, 1.0) * g[0], rtol=0, atol=1e-15)
+
+
+def test_lion_constant_gradient_closed_form():
+    """With a constant gradient g from m = 0, m_t = (1 - b2^t) g, every c has
+    the sign of g, and p_T = d^T p_0 - lr sign(g) (1 - d^T) / (1 - d) with
+    d = 1 - lr wd."""
+    rng = np.random.default_rng(5)
+    p0 = rng.standard_normal(20)
+    g = rng.standard_normal(20)
+    lr, wd, b1, b2, T = 0.01, 0.1, 0.9, 0.99, 12
+    p, m = [p0], [np.zeros(20)]
+    for _ in range(T):
+        p, m = S.lion_step(p, [g], m, lr, b1, b2, wd, max_norm=0.0)
+    d = 1 - lr * wd
+    assert np.allclose(p[0], d ** T * p0 - lr * np.sign(g) * (1 - d ** T) / (1 - d), rtol=0, atol=1e-13)
+    assert np.allclose(m[0], (1 - b2 ** T) * g, rtol=0, atol=1e-14)
+
+
+def test_lion_zero_gradient_only_decays():
+    p0 = np.linspace(-1, 1, 11)
+    p, m = [p0], [np.zeros(11)]
+    for _ in range(7):
+        p, m = S.lion_step(p, [np.zeros(11)], m, lr=0.1, weight_decay=0.2)
+    assert np.array_equal(m[0], np.zeros(11))
+    assert np.allclose(p[0], (1 - 0.02) ** 7 * p0, rtol=0, atol=1e-15)
+
+
+def test_lion_momentum_sum_closed_form():
+    """m_T = sum_k (1 - b2) b2^(T-k) g_k over the (unclipped) gradients."""
+    rng = np.random.default_rng(9)
+    gs = [rng.standard_normal(8) for _ in range(6)]
+    b2 = 0.99
+    m = [np.zeros(8)]
+    p = [np.zeros(8)]
+    for g in gs:
+        p, m = S.lion_step(p, [g], m, lr=0.01, beta2=b2, max_norm=0.0)
+    T = len(gs)
+    want = sum((1 - b2) * b2 ** (T - 1 - k) * gs[k] for k in range(T))
+    assert np.allclose(m[0], want, rtol=0, atol=1e-15)
+
+
+def test_lion_hand_worked_steps():
+    """Three steps worked by hand (b1 = 0.9, b2 = 0.99, lr = 0.1, no decay,
+    no clipping): g = 1 gives c = 0.1 > 0; g = -0.5 gives c = 0.009 - 0.05 =
+    -0.041 < 0; g = -0.01 gives c = 0.9 * 0.0049 - 0.001 = 0.00341 > 0 (the
+    momentum outvotes a small opposite gradient).  m: 0.01, 0.0049, 0.004751."""
+    p, m = [np.array([1.0])], [np.array([0.0])]
+    seq_p, seq_m = [], []
+    for g in (1.0, -0.5, -0.01):
+        p, m = S.lion_step(p, [np.array([g])], m, lr=0.1, beta1=0.9, beta2=0.99, weight_decay=0.0,
+                           max_norm=0.0)
+        seq_p.append(float(p[0][0]))
+        seq_m.append(float(m[0][0]))
+    assert np.allclose(seq_p, [0.9, 1.0, 0.9], rtol=0, atol=1e-15)
+    assert np.allclose(seq_m, [0.01, 0.0049, 0.004751], rtol=0, atol=1e-15)
+
+
+def test_lion_nan_propagates():
+    p, m = S.lion_step([np.zeros(3)], [np.array([1.0, np.nan, -1.0])], [np.zeros(3)], lr=0.1,
+                       max_norm=0.0)
+    assert np.isnan(p[0][1]) and np.isfinite(p[0][[0, 2]]).all()
