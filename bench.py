@@ -69,6 +69,62 @@ def plan_flops(mats, full, K):
     return tot
 
 
+def kind_flops(mats, full, K):
+    """Algorithmic flops of each NS product kind per step (symmetric
+    products counted once per distinct entry, as ns_unit_flops)."""
+    out = {"gram": 0.0, "poly": 0.0, "apply": 0.0}
+    for r, c, gr, gc in mats:
+        units = [(r, c)] if full else [(r // gr, c // gc)] * (gr * gc)
+        for p, q in units:
+            S, L = float(min(p, q)), float(max(p, q))
+            out["gram"] += K * S * (S + 1) * L
+            out["poly"] += K * S * S * (S + 1)
+            out["apply"] += K * 2 * S * S * L
+    return out
+
+
+# Dominant product shapes of the 8B-shaped model: MLP shards 1792 x 4096 on
+# block steps (96 of the 224 matrices' 1792 units), whole 4096 x 14336 MLP
+# matrices on full steps.
+LIBRARY_SHAPES = {
+    "block_gram_96x(1792x4096)(4096x1792)": (96, 1792, 4096, 1792),
+    "block_poly_96x(1792x1792)^2": (96, 1792, 1792, 1792),
+    "block_apply_96x(1792x1792)(1792x4096)": (96, 1792, 1792, 4096),
+    "full_gram_(4096x14336)(14336x4096)": (1, 4096, 14336, 4096),
+    "full_poly_(4096x4096)^2": (1, 4096, 4096, 4096),
+    "full_apply_(4096x4096)(4096x14336)": (1, 4096, 4096, 14336),
+}
+
+
+def library_gemm_reference():
+    """The vendor library's bf16 GEMM (torch.matmul / bmm, hipBLASLt) on the
+    dominant NS product shapes, dense flops: what a tuned library product
+    reaches on this GPU, for comparison with the NS kernels.  Measurement
+    only; the optimizer never calls it."""
+    import torch
+    out = {}
+    for name, (b, m, k, n) in LIBRARY_SHAPES.items():
+        x = torch.randn(b, m, k, device="cuda", dtype=torch.bfloat16)
+        y = torch.randn(b, k, n, device="cuda", dtype=torch.bfloat16)
+        fn = (lambda: torch.bmm(x, y)) if b > 1 else (lambda: torch.matmul(x[0], y[0]))
+        for _ in range(3):
+            fn()
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        reps = 10
+        torch.cuda.synchronize()
+        s.record()
+        for _ in range(reps):
+            fn()
+        e.record()
+        torch.cuda.synchronize()
+        ms = s.elapsed_time(e) / reps
+        tf = 2.0 * b * m * k * n / (ms * 1e-3) / 1e12
+        out[name] = {"ms": ms, "tflops": tf, "frac_bf16_peak": tf / BF16_PEAK_TFLOPS}
+        del x, y
+    torch.cuda.empty_cache()
+    return out
+
+
 def _oracle_threads():
     from threadpoolctl import threadpool_info
     return int(max([i.get("num_threads", 1) for i in threadpool_info()] or [1]))
@@ -670,6 +726,10 @@ def main():
                     help="library option apply_mode (0: apply reads Z row-major, 1: keeps Z^T)")
     ap.add_argument("--k-split", type=int, default=0,
                     help="library option k_split (0: planner's choice)")
+    ap.add_argument("--no-library-reference", action="store_true",
+                    help="skip timing the vendor library's GEMM on the dominant shapes")
+    ap.add_argument("--tile-policy", type=int, default=0,
+                    help="library option tile_policy (0: planner's choice)")
     ap.add_argument("--copy-probe", type=int, metavar="MIB", default=None,
                     help="only run a plain copy of MIB MiB (counter calibration) and exit")
     ap.add_argument("--mfma-probe", action="store_true",
@@ -732,7 +792,7 @@ def main():
     params, grads, data = make_inputs(mats, rank)
     opt = mb.MuonBP(mats, period, lr_block, LR_FULL, MU, WD,
                     options=mb.options_default(ns_steps=K_NS, apply_mode=args.apply_mode,
-                                               k_split=args.k_split))
+                                               k_split=args.k_split, tile_policy=args.tile_policy))
     torch.cuda.synchronize()
 
     t = 0
@@ -811,6 +871,9 @@ def main():
             "detail_kernel_ms_per_step": {k: v[0] / reps for k, v in detail.items()
                                           if k != "ns_span"},
             "detail_launches": {k: v[1] for k, v in detail.items() if k != "ns_span"},
+            "detail_gemm_tflops": {k: f * reps / (detail[k][0] * 1e-3) / 1e12
+                                   for k, f in kind_flops(mats, full, K_NS).items()
+                                   if detail[k][0] > 0},
             "gemm_tiles": [f"{info.gemm_tile_rows[i]}x{info.gemm_tile_cols[i]}:{info.gemm_tiles[i]}"
                            for i in range(3)],
         }
@@ -871,6 +934,9 @@ def main():
     opt.close()
     del params, grads
     torch.cuda.empty_cache()
+    if name == DEFAULT_WORKLOAD and not args.no_library_reference:
+        log("library GEMM reference")
+        out["library_gemm_reference"] = library_gemm_reference()
     if not args.no_scalar:
         log("scalar optimizer (AdamW) pass")
         out["scalar_optimizer"] = scalar_optimizer_bench()

@@ -125,6 +125,15 @@ typedef struct {
                                their values, M holds this step's update).
                                Off: NaN / Inf propagate silently into U and
                                the params of their unit. */
+  int64_t device_memory_limit; /* > 0: muonbp_create allocates at most this
+                               many bytes of device memory (momentum, NS
+                               workspace, K-split sums, descriptor tables; the
+                               n_mats x 16-byte pointer tables aside) and
+                               returns MUONBP_E_NOMEM instead of going over,
+                               checking the momentum + workspace + split sums
+                               before any HIP call; 0 = no limit (default).
+                               muonbp_plan_info.device_bytes is the size of
+                               those three. */
 } muonbp_options;
 
 /* Fill *opt with the defaults above.  NULL is ignored. */
@@ -220,6 +229,8 @@ typedef struct {
   int64_t static_scratch_bytes; /* scratch muonbp_step_static needs for a step
                               of this plan (MUONBP_E_TOO_LARGE above
                               MUONBP_STATIC_SCRATCH_BYTES)                    */
+  int64_t device_bytes;    /* momentum + NS workspace + K-split sums of a
+                              context for these matrices (both plans)       */
 } muonbp_plan_info;
 
 /* Plan description for a set of matrices without creating a context

@@ -74,6 +74,7 @@ struct muonbp_ctx {
   BlockDesc* blocks = nullptr;
   PlanDev pd[2];
   std::vector<void*> allocs;
+  int64_t allocated = 0;  // bytes in allocs (device_memory_limit)
 
   PtrRing ptrs;  // caller's param / grad pointers of the current step
 
@@ -107,25 +108,33 @@ muonbp_status hip_fail(muonbp_ctx* c, hipError_t e, const char* what) {
 // Copies a host table into new device memory on the context's stream and
 // waits for that stream only (no device-wide synchronisation, which would
 // also wait for, or break a graph capture on, the caller's other streams).
+hipError_t dev_alloc(muonbp_ctx* c, void** p, size_t bytes);
+
 template <typename T>
 hipError_t upload(muonbp_ctx* c, T** dst, const std::vector<T>& src) {
   *dst = nullptr;
   if (src.empty()) return hipSuccess;
   void* p = nullptr;
-  hipError_t e = hipMalloc(&p, src.size() * sizeof(T));
+  hipError_t e = dev_alloc(c, &p, src.size() * sizeof(T));
   if (e != hipSuccess) return e;
-  c->allocs.push_back(p);
   *dst = static_cast<T*>(p);
   e = hipMemcpyAsync(p, src.data(), src.size() * sizeof(T), hipMemcpyHostToDevice, c->stream);
   if (e != hipSuccess) return e;
   return hipStreamSynchronize(c->stream);
 }
 
+// hipMalloc within the context's device_memory_limit (over it: out of
+// memory, without calling hipMalloc).
 hipError_t dev_alloc(muonbp_ctx* c, void** p, size_t bytes) {
   *p = nullptr;
   if (bytes == 0) bytes = 256;
+  const int64_t limit = c->opt.device_memory_limit;
+  if (limit > 0 && int64_t(bytes) > limit - c->allocated) return hipErrorOutOfMemory;
   hipError_t e = hipMalloc(p, bytes);
-  if (e == hipSuccess) c->allocs.push_back(*p);
+  if (e == hipSuccess) {
+    c->allocs.push_back(*p);
+    c->allocated += int64_t(bytes);
+  }
   return e;
 }
 
@@ -297,6 +306,7 @@ muonbp_status muonbp_describe_plan(const muonbp_matrix* mats, int32_t n_mats,
   out->elementwise_bytes = double(lay.total_elems) * ((pb + 2 * sb) + (2 * pb + nb));
   out->workspace_bytes = p.ws_elems * int64_t(nb);
   out->static_scratch_bytes = scratch_plan(lay, full, o).total;
+  out->device_bytes = context_bulk_bytes(lay, o);
   return MUONBP_OK;
 }
 
@@ -328,6 +338,10 @@ muonbp_status muonbp_create(const muonbp_matrix* mats, int32_t n_mats, int64_t p
       return shape_err ? MUONBP_E_SHAPE : MUONBP_E_INVALID;
     }
   } catch (const std::bad_alloc&) {
+    free_ctx(c);
+    return MUONBP_E_NOMEM;
+  }
+  if (o.device_memory_limit > 0 && context_bulk_bytes(c->lay, o) > o.device_memory_limit) {
     free_ctx(c);
     return MUONBP_E_NOMEM;
   }

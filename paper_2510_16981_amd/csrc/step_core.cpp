@@ -45,9 +45,17 @@ std::string validate_opts(const muonbp_options& o) {
   if (o.stream_hint < 0 || o.stream_hint > 2) return "stream_hint out of range";
   if (o.apply_mode < 0 || o.apply_mode > 1) return "apply_mode out of range";
   if (o.check_finite != 0 && o.check_finite != 1) return "check_finite must be 0 or 1";
+  if (o.device_memory_limit < 0) return "device_memory_limit must be >= 0";
   for (int i = 0; i < 3 * o.coeff_count; ++i)
     if (!std::isfinite(o.coeff_table[i])) return "coefficients must be finite";
   return "";
+}
+
+int64_t context_bulk_bytes(const Layout& lay, const muonbp_options& o) {
+  const int64_t ws = std::max(lay.plan[0].ws_elems, lay.plan[1].ws_elems);
+  const int64_t split = std::max(lay.plan[0].split_floats, lay.plan[1].split_floats);
+  return lay.total_elems * int64_t(dtype_size(o.state_dtype)) + ws * int64_t(dtype_size(o.ns_dtype)) +
+         split * int64_t(sizeof(float));
 }
 
 std::string check_mats(const muonbp_matrix* mats, int32_t n_mats, std::vector<MatrixShape>* out) {

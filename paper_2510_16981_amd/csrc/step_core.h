@@ -26,6 +26,10 @@ int poly_slots(const muonbp_options& o);
 // "" when the options are valid, else the reason.
 std::string validate_opts(const muonbp_options& o);
 
+// Device bytes of a context's momentum, NS workspace (the larger plan's)
+// and K-split partial sums.
+int64_t context_bulk_bytes(const Layout& lay, const muonbp_options& o);
+
 // Copies the shapes (E_INVALID text on a NULL array or a bad count).
 std::string check_mats(const muonbp_matrix* mats, int32_t n_mats, std::vector<MatrixShape>* out);
 

@@ -74,6 +74,21 @@ def _create(lib, mats, period=5, opt=None, out=True):
                              ctypes.byref(ctx) if out else None), ctx
 
 
+def test_device_memory_limit_refuses_before_gpu(lib):
+    """A budget below the momentum + workspace + split sums fails with
+    E_NOMEM before any HIP call (this container has no GPU, so reaching one
+    would give E_HIP); a negative budget is an invalid option."""
+    mats = W.workload_matrices("qkv-2048x6144-bf16")
+    info = mb.describe_plan(mats, True)
+    full_ws = info.workspace_bytes
+    assert info.device_bytes >= 2048 * 6144 * 2 + full_ws
+    assert mb.describe_plan(mats, False).device_bytes == info.device_bytes
+    for limit in (1, 2048 * 6144 * 2, info.device_bytes - 1):
+        st, ctx = _create(lib, mats, opt=mb.options_default(device_memory_limit=limit))
+        assert st == 4 and not ctx.value
+    assert _create(lib, mats, opt=mb.options_default(device_memory_limit=-1))[0] == 1
+
+
 def test_create_rejects_bad_arguments_before_gpu(lib):
     assert _create(lib, None)[0] == 1
     assert _create(lib, [])[0] == 1

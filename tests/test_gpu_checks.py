@@ -1,4 +1,5 @@
-"""The opt-in finite check of the step (muonbp_options.check_finite).
+"""The opt-in finite check of the step (muonbp_options.check_finite), and
+the device-memory budget of muonbp_create (muonbp_options.device_memory_limit).
 
 With the check on, a NaN or an Inf in a gradient (hence in the momentum that
 Alg. 2 normalises) makes muonbp_step return MUONBP_E_NONFINITE before any
@@ -105,3 +106,36 @@ def test_check_off_propagates_into_its_unit_only():
     assert torch.isfinite(p[0][:, :64].float()).all()
     assert torch.isfinite(p[1].float()).all()
     A.close()
+
+
+def test_device_memory_limit_out_of_memory_frees_everything():
+    """A budget just above the momentum + workspace + split sums passes the
+    up-front check and runs out on the descriptor tables: E_NOMEM, and every
+    allocation made so far is freed (the free device memory is the same
+    after 20 such failures).  A budget with room for the tables works."""
+    import torch
+    from paper_2510_16981_amd import muonbp as mb
+    mats = [(2048, 6144, 1, 8)]
+    bulk = mb.describe_plan(mats, True).device_bytes
+    announce(f"device_memory_limit around {bulk} bytes")
+    lib = mb.load_library()
+
+    def create(limit):
+        ctx = ctypes.c_void_p()
+        o = mb.options_default(device_memory_limit=limit)
+        st = lib.muonbp_create(mb._mats(mats), len(mats), 5, 0.01, 0.02, 0.95, 0.1, ctypes.byref(o),
+                               ctypes.c_void_p(torch.cuda.current_stream().cuda_stream),
+                               ctypes.byref(ctx))
+        return st, ctx
+
+    torch.cuda.synchronize()
+    st, ctx = create(bulk + 1024)
+    assert st == 4 and not ctx.value
+    free0 = torch.cuda.mem_get_info()[0]
+    for _ in range(20):
+        st, ctx = create(bulk + 1024)
+        assert st == 4 and not ctx.value
+    assert torch.cuda.mem_get_info()[0] == free0
+    st, ctx = create(bulk + (64 << 20))
+    assert st == 0 and ctx.value
+    lib.muonbp_destroy(ctx)
