@@ -401,14 +401,14 @@ rocprofv3 --pmc FETCH_SIZE -f csv -d $R/gpurun_out/prof/copy_fetch -o run -- pyt
 rocprofv3 --pmc WRITE_SIZE -f csv -d $R/gpurun_out/prof/copy_write -o run -- python3 $R/bench.py --copy-probe 1024
 rocprofv3 --pmc SQ_INSTS_VALU_MFMA_MOPS_BF16 MfmaUtil GRBM_GUI_ACTIVE -f csv -d $R/gpurun_out/prof/mfma_probe -o run -- python3 $R/bench.py --mfma-probe > $R/gpurun_out/prof/mfma_probe/mfma_probe.json
 # kind=block with P=0, kind=full with P=1; each run's JSON line saved as b.json in its folder
-rocprofv3 --pmc FETCH_SIZE -f csv -d $R/gpurun_out/prof/$W/${kind}_fetch -o run -- python3 $R/bench.py --workload $W --period $P --steps 10 --warmup 2 --no-cpu-baseline --no-scalar
-rocprofv3 --pmc WRITE_SIZE -f csv -d $R/gpurun_out/prof/$W/${kind}_write -o run -- python3 $R/bench.py --workload $W --period $P --steps 10 --warmup 2 --no-cpu-baseline --no-scalar
-rocprofv3 --pmc SQ_INSTS_VALU_MFMA_MOPS_BF16 MfmaUtil GRBM_GUI_ACTIVE -f csv -d $R/gpurun_out/prof/$W/${kind}_mfma -o run -- python3 $R/bench.py --workload $W --period $P --steps 10 --warmup 2 --no-cpu-baseline --no-scalar
+rocprofv3 --pmc FETCH_SIZE -f csv -d $R/gpurun_out/prof/$W/${kind}_fetch -o run -- python3 $R/bench.py --workload $W --period $P --steps 10 --warmup 2 --no-cpu-baseline --no-scalar --no-library-reference
+rocprofv3 --pmc WRITE_SIZE -f csv -d $R/gpurun_out/prof/$W/${kind}_write -o run -- python3 $R/bench.py --workload $W --period $P --steps 10 --warmup 2 --no-cpu-baseline --no-scalar --no-library-reference
+rocprofv3 --pmc SQ_INSTS_VALU_MFMA_MOPS_BF16 MfmaUtil GRBM_GUI_ACTIVE -f csv -d $R/gpurun_out/prof/$W/${kind}_mfma -o run -- python3 $R/bench.py --workload $W --period $P --steps 10 --warmup 2 --no-cpu-baseline --no-scalar --no-library-reference
 python3 bench.py --workload $W --ingest-counters gpurun_out/prof/{copy_fetch,copy_write,mfma_probe} gpurun_out/prof/$W/{block_fetch,block_write,block_mfma,full_fetch,full_write,full_mfma}
 """
 KERNEL_TRACE_COMMANDS = """\
 cd /tmp && export TMPDIR=/tmp   # R = repository root
-rocprofv3 --kernel-trace --stats -f csv -d $R/gpurun_out/prof/kt -o run -- python3 $R/bench.py --no-cpu-baseline > $R/gpurun_out/prof/kt/bench.json
+rocprofv3 --kernel-trace --stats -f csv -d $R/gpurun_out/prof/kt -o run -- python3 $R/bench.py --no-cpu-baseline --no-library-reference > $R/gpurun_out/prof/kt/bench.json
 python3 bench.py --ingest-kernel-trace gpurun_out/prof/kt
 """
 
