@@ -493,14 +493,17 @@ __device__ __forceinline__ void gemm_epilogue(f32x16_t (&acc)[TM][TN], float* st
   const int wr0 = m0 + wm * 32 * TM, wc0 = n0 + wn * 32 * TN;
   const __amdgpu_buffer_rsrc_t dr = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<void*>(has_d ? d.D : d.X), 0, has_d ? d.M * d.ldd * ES : 0, kBufferWord3);
+  // Rows past M take the out-of-range offset (no 32-bit product past 2^31).
   T* C = static_cast<T*>(d.C);
   T* Ct = static_cast<T*>(d.Ct);
   uint4 dv[2][CPL][VPC];
+  const int dbytes = has_d ? d.M * d.ldd * ES : 0;
   auto load_d = [&](int i, uint4 (&buf)[CPL][VPC]) {
 #pragma unroll
     for (int c = 0; c < CPL; ++c) {
       const int q = lane + 64 * c, r = q / NCH, ch = q - r * NCH;
-      const int o = ((wr0 + 32 * i + r) * d.ldd + wc0 + 8 * ch) * ES;
+      const int row = wr0 + 32 * i + r;
+      const int o = row < d.M ? (row * d.ldd + wc0 + 8 * ch) * ES : dbytes;
 #pragma unroll
       for (int h = 0; h < VPC; ++h) buf[c][h] = bld16(dr, o + 16 * h, 0);
     }
@@ -587,8 +590,10 @@ __global__ __launch_bounds__(kThreads * KS) void k_ns_gemm(const GemmDesc* __res
 
   // Operands are read with buffer loads: one 32-bit offset per 16-byte slice
   // (constant over the K loop) plus the K position as a uniform scalar
-  // offset.  Rows at or beyond M (N) lie past the descriptor's byte count and
-  // read as zero; columns at or beyond K are masked to zero in the last K
+  // offset.  Rows at or beyond M (N) take an offset past the descriptor's
+  // byte count (never a row product, which could pass 2^31 for the last
+  // tile of a unit just under the operand limit) and read as zero; columns
+  // at or beyond K are masked to zero in the last K
   // slice, which may straddle K (rows are padded to a multiple of 8 elements,
   // so the read stays inside the row).
   constexpr int ES = sizeof(T);
@@ -600,9 +605,15 @@ __global__ __launch_bounds__(kThreads * KS) void k_ns_gemm(const GemmDesc* __res
   const int kc = (tid & 7) * EPV;  // this thread's column inside a K slice
   int xo[QX], yo[QY];
 #pragma unroll
-  for (int q = 0; q < QX; ++q) xo[q] = ((m0 + (tid >> 3) + 32 * q) * d.ldx + kc) * ES;
+  for (int q = 0; q < QX; ++q) {
+    const int r = m0 + (tid >> 3) + 32 * q;
+    xo[q] = r < d.M ? (r * d.ldx + kc) * ES : xbytes;
+  }
 #pragma unroll
-  for (int q = 0; q < QY; ++q) yo[q] = ((n0 + (tid >> 3) + 32 * q) * d.ldy + kc) * ES;
+  for (int q = 0; q < QY; ++q) {
+    const int r = n0 + (tid >> 3) + 32 * q;
+    yo[q] = r < d.N ? (r * d.ldy + kc) * ES : ybytes;
+  }
   uint4 rx[QX], ry[QY];
   auto gload = [&](int k0) {
 #pragma unroll
@@ -935,12 +946,18 @@ __global__ __launch_bounds__(64 * WM * WN) void k_ns_gemm_dmap(const GemmDesc* _
       const int q = 64 * (u - BM / 16) + lane, kr = q / CPR;
       const int cn = (q - kr * CPR) ^ nn_swz<BN>(kr);
       chunk[jj] = kr;
-      voff[jj] = n0 + 8 * cn < d.N ? (kr * d.ldy + n0 + 8 * cn) * ES : ybytes;
+      // k-row kr of every slice: past K in all of them when kr >= K.
+      voff[jj] = n0 + 8 * cn < d.N && kr < d.K ? (kr * d.ldy + n0 + 8 * cn) * ES : ybytes;
     } else {
       const int row = 16 * u + (lane >> 2);
       const int c = (lane & 3) ^ swz(row);
       chunk[jj] = c;
-      voff[jj] = row < BM ? ((m0 + row) * d.ldx + 8 * c) * ES : ((n0 + row - BM) * d.ldy + 8 * c) * ES;
+      // Rows past M (N) take the out-of-range offset, not a row product
+      // (which could pass 2^31 in the last tile of a unit near the limit).
+      if (row < BM)
+        voff[jj] = m0 + row < d.M ? ((m0 + row) * d.ldx + 8 * c) * ES : xbytes;
+      else
+        voff[jj] = n0 + row - BM < d.N ? ((n0 + row - BM) * d.ldy + 8 * c) * ES : ybytes;
     }
   }
   const int nk_all = (d.K + 31) / 32;
@@ -957,7 +974,9 @@ __global__ __launch_bounds__(64 * WM * WN) void k_ns_gemm_dmap(const GemmDesc* _
         dma16(xr, dst, kin ? voff[jj] : xbytes, k0 * ES);
       } else {
         const bool kin = kt < ke && k0 + chunk[jj] < d.K;
-        dma16(yr, dst, kin ? voff[jj] : ybytes, k0 * d.ldy * ES);
+        // The slice's k-row offset only for slices that start inside K
+        // (k0 ldy < K ldy, so the product stays below the byte count).
+        dma16(yr, dst, kin ? voff[jj] : ybytes, (k0 < d.K ? k0 : 0) * d.ldy * ES);
       }
     } else {
       const bool kin = kt < ke && k0 + 8 * chunk[jj] < d.K;

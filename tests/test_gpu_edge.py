@@ -1,0 +1,105 @@
+"""GPU parity at the largest operand the library accepts.
+
+The NS kernels address an operand with 32-bit byte offsets, and the planner
+refuses any unit whose Z, A or B reaches 2^31 bytes.  This test runs a unit
+just under that limit: one 264 x 4065000 bf16 matrix (Z is 2.146e9 bytes;
+the column count is near the planner's tile-index limit of 65535 tiles of
+64).  264 rows is no multiple of any tile height, so the last tile row of
+every product holds rows past M, and the apply's K loop (K = S = 264) ends
+in a partial slice followed by slices past K: the offsets those take must
+not be row products past 2^31.
+
+One full step (P = 1) from zero momentum on seeded inputs (drawn on the GPU
+with a seeded generator): the momentum must equal the bf16 gradient bit for
+bit, U is compared with the fp64 oracle
+(Alg. 2 on the GPU's own momentum, teacher-forced) on the whole matrix and on
+every 64 x 64 tile, and the new weights with one step of Alg. 1's update
+from the GPU's U on sampled columns at the start and the end of the rows.
+"""
+
+import numpy as np
+import pytest
+
+from oracle import muonbp_oracle as O
+from tests.gpu_harness import announce, rel, ulp_distance, update_reference
+
+pytestmark = pytest.mark.gpu
+
+ROWS, COLS = 264, 4065000
+TOL = 2e-2
+LR, MU, WD = 0.02, 0.95, 0.1
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a ROCm device"
+    from paper_2510_16981_amd import muonbp as mb
+    mb.load_library()
+
+
+def _tile_errors(u, ref, tile=64, chunk=1 << 18):
+    """Worst relative error over tile x tile tiles (the harness's definition:
+    ||du_tile|| / max(||ref_tile||, ||ref|| sqrt(n_tile / n))), computed in
+    column chunks without a Python loop over tiles."""
+    m, n = ref.shape
+    rows = np.arange(0, m, tile)
+    d2_all, r2_all, sizes = [], [], []
+    for c0 in range(0, n, chunk):
+        c1 = min(n, c0 + chunk)
+        cols = np.arange(0, c1 - c0, tile)
+        d = (u[:, c0:c1] - ref[:, c0:c1]) ** 2
+        r = ref[:, c0:c1] ** 2
+        d2_all.append(np.add.reduceat(np.add.reduceat(d, rows, axis=0), cols, axis=1))
+        r2_all.append(np.add.reduceat(np.add.reduceat(r, rows, axis=0), cols, axis=1))
+        h = np.minimum(rows + tile, m) - rows
+        w = np.minimum(cols + tile, c1 - c0) - cols
+        sizes.append(np.outer(h, w))
+    d2, r2, sz = (np.concatenate(x, axis=1) for x in (d2_all, r2_all, sizes))
+    n_all = np.sqrt(r2.sum())
+    den = np.maximum(np.sqrt(r2), n_all * np.sqrt(sz / ref.size))
+    return float(np.max(np.sqrt(d2) / den))
+
+
+def test_largest_accepted_operand_against_oracle():
+    import torch
+    from paper_2510_16981_amd import muonbp as mb
+
+    mats = [(ROWS, COLS, 1, 1)]
+    info = mb.describe_plan(mats, True)
+    assert ROWS * COLS * 2 < 2 ** 31 <= ROWS * (COLS + 8 * 1024) * 2
+    announce(f"largest operand {ROWS} x {COLS} bf16: Z {ROWS * COLS * 2} bytes, tiles "
+             f"{[(info.gemm_tile_rows[k], info.gemm_tile_cols[k], info.gemm_tiles[k]) for k in range(3)]}")
+    # Seeded inputs drawn on the GPU (1.07 G elements each); the checks copy
+    # back what they compare.
+    gen = torch.Generator(device="cuda").manual_seed(2026)
+    g_dev = (torch.randn((ROWS, COLS), generator=gen, device="cuda") * 0.01).to(torch.bfloat16)
+    x_dev = (torch.randn((ROWS, COLS), generator=gen, device="cuda") * 0.02).to(torch.bfloat16)
+    cols = [slice(0, 100000), slice(COLS - 100000, COLS)]
+    x0 = [x_dev[:, cs].double().cpu().numpy() for cs in cols]
+    opt = mb.MuonBP(mats, 1, LR, LR, MU, WD)
+    opt.step([x_dev], [g_dev], 0)
+    m_dev = opt.get_momentum(0)
+    u_dev = opt.get_update(0)
+    torch.cuda.synchronize()
+    assert torch.equal(m_dev, g_dev), "momentum from zero must be the gradient itself"
+    y = m_dev.double().cpu().numpy()
+    u = u_dev.double().cpu().numpy()
+    x1 = [x_dev[:, cs].double().cpu().numpy() for cs in cols]
+    opt.close()
+    del g_dev, x_dev, m_dev, u_dev
+    torch.cuda.empty_cache()
+
+    ref = O.orthogonalize_via_ns(y, K=5)
+    del y
+    err = rel(u, ref)
+    tile_err = _tile_errors(u, ref)
+    announce(f"U relative error {err:.3e}, worst 64x64 tile {tile_err:.3e}")
+    assert err <= TOL and tile_err <= TOL
+    del ref
+
+    # Update on the first and last 100000 columns: one step of Alg. 1 from
+    # x0 with the GPU's U, at most one bf16 unit in the last place apart.
+    for cs, a, b in zip(cols, x0, x1):
+        want = update_reference(a, u[:, cs], LR, WD, 1.0, "bf16")
+        assert ulp_distance(b, want, "bf16") <= 1.0
