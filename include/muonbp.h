@@ -365,7 +365,8 @@ muonbp_status muonbp_adamw_step(muonbp_adamw_ctx* ctx, void* const* params,
 muonbp_status muonbp_adamw_grad_norm(muonbp_adamw_ctx* ctx, float* out);
 
 /* Copy tensor i's moments (fp32, sizes[i] elements) to / from device memory
- * (checkpoint and resume).  Asynchronous on the stream; NULL skips one. */
+ * (checkpoint and resume).  Asynchronous on the stream; NULL skips one.
+ * Lion keeps no v: get_state writes zeros to v_dst, set_state ignores v_src. */
 muonbp_status muonbp_adamw_get_state(muonbp_adamw_ctx* ctx, int32_t i, void* m_dst, void* v_dst);
 muonbp_status muonbp_adamw_set_state(muonbp_adamw_ctx* ctx, int32_t i, const void* m_src,
                                      const void* v_src);

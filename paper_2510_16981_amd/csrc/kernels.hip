@@ -1303,7 +1303,7 @@ __global__ __launch_bounds__(kThreads) void k_adamw(const ScalarSeg* __restrict_
   TP* p = static_cast<TP*>(ptrs[sg.tensor].param) + sg.begin;
   const TP* g = static_cast<const TP*>(ptrs[sg.tensor].grad) + sg.begin;
   float* ms = m + sg.state;
-  float* vs = v + sg.state;
+  float* vs = LION ? nullptr : v + sg.state;  // Lion: no v arena
   const float c = clip ? clip[0] : 1.f;
   const int n = sg.count, nv = VEC ? n >> 3 : 0;
   for (int c0 = threadIdx.x; c0 < nv; c0 += kThreads * kAdamwUnroll) {

@@ -156,8 +156,10 @@ muonbp_status muonbp_adamw_create(const int64_t* sizes, int32_t n, const muonbp_
   void* p = nullptr;
   if ((e = dev_alloc(c, &p, size_t(c->state_elems) * 4)) != hipSuccess) return bail(e);
   c->m = static_cast<float*>(p);
-  if ((e = dev_alloc(c, &p, size_t(c->state_elems) * 4)) != hipSuccess) return bail(e);
-  c->v = static_cast<float*>(p);
+  if (o.algorithm == 0) {  // Lion keeps no second moment
+    if ((e = dev_alloc(c, &p, size_t(c->state_elems) * 4)) != hipSuccess) return bail(e);
+    c->v = static_cast<float*>(p);
+  }
   if ((e = dev_alloc(c, &p, segs.size() * sizeof(ScalarSeg))) != hipSuccess) return bail(e);
   c->segs = static_cast<ScalarSeg*>(p);
   if ((e = dev_alloc(c, &p, segs.size() * sizeof(float))) != hipSuccess) return bail(e);
@@ -171,7 +173,8 @@ muonbp_status muonbp_adamw_create(const int64_t* sizes, int32_t n, const muonbp_
                           hipMemcpyHostToDevice, c->stream)) != hipSuccess)
     return bail(e);
   if ((e = hipMemsetAsync(c->m, 0, size_t(c->state_elems) * 4, c->stream)) != hipSuccess) return bail(e);
-  if ((e = hipMemsetAsync(c->v, 0, size_t(c->state_elems) * 4, c->stream)) != hipSuccess) return bail(e);
+  if (c->v && (e = hipMemsetAsync(c->v, 0, size_t(c->state_elems) * 4, c->stream)) != hipSuccess)
+    return bail(e);
   if ((e = hipStreamSynchronize(c->stream)) != hipSuccess) return bail(e);
   *out = c;
   return MUONBP_OK;
@@ -246,12 +249,14 @@ static muonbp_status state_copy(muonbp_adamw_ctx* c, int32_t i, void* m_dst, voi
   if (i < 0 || size_t(i) >= c->sizes.size()) return fail(c, MUONBP_E_INVALID, "tensor index out of range");
   const size_t bytes = size_t(c->sizes[size_t(i)]) * 4;
   float* m = c->m + c->state_off[size_t(i)];
-  float* v = c->v + c->state_off[size_t(i)];
+  float* v = c->v ? c->v + c->state_off[size_t(i)] : nullptr;  // no v under Lion
   hipError_t e = hipSuccess;
   if (m_dst) e = hipMemcpyAsync(m_dst, m, bytes, hipMemcpyDeviceToDevice, c->stream);
-  if (e == hipSuccess && v_dst) e = hipMemcpyAsync(v_dst, v, bytes, hipMemcpyDeviceToDevice, c->stream);
+  if (e == hipSuccess && v_dst)
+    e = v ? hipMemcpyAsync(v_dst, v, bytes, hipMemcpyDeviceToDevice, c->stream)
+          : hipMemsetAsync(v_dst, 0, bytes, c->stream);
   if (e == hipSuccess && m_src) e = hipMemcpyAsync(m, m_src, bytes, hipMemcpyDeviceToDevice, c->stream);
-  if (e == hipSuccess && v_src) e = hipMemcpyAsync(v, v_src, bytes, hipMemcpyDeviceToDevice, c->stream);
+  if (e == hipSuccess && v_src && v) e = hipMemcpyAsync(v, v_src, bytes, hipMemcpyDeviceToDevice, c->stream);
   if (e != hipSuccess) return hip_fail(c, e, "state copy");
   return MUONBP_OK;
 }

@@ -223,3 +223,31 @@ def test_lion_unaligned_pointers():
     announce("lion f32 offset pointers")
     w = _run_lion(SIZES, "f32", 1.0, 25.0, steps=2, offset=1)
     assert w["m"] <= F32_TOL and w["p"] <= 1.0
+
+
+def test_lion_state_has_no_second_moment():
+    """A Lion context keeps only m: get_state returns zeros for v, set_state
+    ignores it, and a context resumed from m alone continues identically."""
+    import torch
+    from paper_2510_16981_amd import muonbp as mb
+    sizes = [5, 20000, 33]
+    params_h, grads_h = _inputs(sizes, 6, "bf16", 2, 25.0)
+    o = mb.adamw_options_default(algorithm=1, beta1=L_B1, beta2=L_B2)
+    a = mb.AdamW(sizes, o)
+    pa = [h.cuda() for h in params_h]
+    a.step(pa, [g.cuda() for g in grads_h[0]], 0, 1e-2)
+    b = mb.AdamW(sizes, o)
+    for i in range(len(sizes)):
+        m, v = a.get_state(i)
+        torch.cuda.synchronize()
+        assert torch.count_nonzero(v) == 0 and torch.count_nonzero(m) > 0
+        b.set_state(i, m, torch.full_like(v, 7.0))
+    pb = [x.clone() for x in pa]
+    g = [x.cuda() for x in grads_h[1]]
+    a.step(pa, g, 1, 1e-2)
+    b.step(pb, g, 1, 1e-2)
+    torch.cuda.synchronize()
+    for x, y in zip(pa, pb):
+        assert torch.equal(x, y)
+    a.close()
+    b.close()
