@@ -760,7 +760,7 @@ def main():
                             KERNEL_TRACE_COMMANDS if args.command is None else args.command)
         return
     if args.gpus != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
+        print("bench.py measures one GPU only: the library has no multi-GPU path "
               "(blocks of a sharded matrix are processed as a batch on one GPU).", file=sys.stderr)
         sys.exit(2)
 
