@@ -231,10 +231,10 @@ int32_t choose_variant(const std::vector<Problem>& probs, GemmKind kind, int til
   if (dma) {
     // 256 x 256 tiles run on the 8-wave kernel (two waves per SIMD): 4-19%
     // faster than the 4-wave one on every measured launch, never slower.
-    // The 8-wave 192 x 256 / 256 x 192 kernels (tile policies only) are
-    // 5-6% faster per launch, but on the 2048 x 6144 benchmark the Gram and
-    // A.A launches that follow them ran 3-7% slower, and the step did not
-    // gain.
+    // 192 x 256 and 256 x 192 tiles too, since the two waves of a SIMD swap
+    // issue priority every slice: the 2048 x 768 shards' apply 700 against
+    // 649 TFLOP/s, the 2048 x 6144 step 2.5% faster (before the swap the
+    // launches after them ran slower and the step did not gain).
     static const int32_t sym_cands[] = {kGemmDmaP128x128, kGemmDmaP192x192, kGemmDmaP256x256W8};
     static const int32_t gen_cands[] = {kGemmDmaP128x128, kGemmDmaP256x128, kGemmDmaP192x256,
                                         kGemmDmaP256x192, kGemmDmaP256x256W8};
@@ -249,6 +249,8 @@ int32_t choose_variant(const std::vector<Problem>& probs, GemmKind kind, int til
         best_us = us;
       }
     }
+    if (best == kGemmDmaP192x256) best = kGemmDmaP192x256W8;
+    if (best == kGemmDmaP256x192) best = kGemmDmaP256x192W8;
     return best;
   }
   const int64_t n128 = count_tiles(probs, kind, kGemm128x128);
