@@ -4,10 +4,12 @@ The NS kernels address an operand with 32-bit byte offsets, and the planner
 refuses any unit whose Z, A or B reaches 2^31 bytes.  This test runs a unit
 just under that limit: one 264 x 4065000 bf16 matrix (Z is 2.146e9 bytes;
 the column count is near the planner's tile-index limit of 65535 tiles of
-64).  264 rows is no multiple of any tile height, so the last tile row of
-every product holds rows past M, and the apply's K loop (K = S = 264) ends
-in a partial slice followed by slices past K: the offsets those take must
-not be row products past 2^31.
+64) on the DMA kernels, and one 124 x 4065000 fp32 matrix on the
+register-loop kernels (its Z^T is 2.08e9 bytes).  Eight more rows are
+refused in either case.  Neither row count is a multiple of a tile height,
+so the last tile row of every product holds rows past M, and the bf16
+apply's K loop (K = S = 264) ends in a partial slice followed by slices
+past K: the offsets those take must not be row products past 2^31.
 
 One full step (P = 1) from zero momentum on seeded inputs (drawn on the GPU
 with a seeded generator): the momentum must equal the bf16 gradient bit for
@@ -25,9 +27,18 @@ from tests.gpu_harness import announce, rel, ulp_distance, update_reference
 
 pytestmark = pytest.mark.gpu
 
-ROWS, COLS = 264, 4065000
-TOL = 2e-2
+COLS = 4065000
 LR, MU, WD = 0.02, 0.95, 0.1
+# (dtype, rows, relative bar): bf16 on the DMA kernels, fp32 on the
+# register-loop kernels (4-byte operands, and Z^T of L x 128 kept as well).
+# Eight more rows are refused in either case.  The fp32 bar: each Gram
+# entry is one fp32 accumulator over K = 4065000 products, each product
+# only a few units in the last place of the running sum (a diagonal term is
+# about 1 / (124 K) against a sum of 1 / 124), so additions lose most of
+# their bits.  Measured U error against the fp64 oracle at K = 40650,
+# 406500, 4065000: 1.1e-6, 2.2e-5, 6.9e-4 (the 1e-4 bar of the fp32 parity
+# cases assumes K of a few thousand), so 1e-3 here.
+CASES = [("bf16", 264, 2e-2), ("f32", 124, 1e-3)]
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -61,23 +72,28 @@ def _tile_errors(u, ref, tile=64, chunk=1 << 18):
     return float(np.max(np.sqrt(d2) / den))
 
 
-def test_largest_accepted_operand_against_oracle():
+@pytest.mark.parametrize("dtype,ROWS,TOL", CASES, ids=[c[0] for c in CASES])
+def test_largest_accepted_operand_against_oracle(dtype, ROWS, TOL):
     import torch
     from paper_2510_16981_amd import muonbp as mb
 
+    es = 2 if dtype == "bf16" else 4
+    code = mb.BF16 if dtype == "bf16" else mb.F32
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    opts = mb.options_default(param_dtype=code, state_dtype=code, ns_dtype=code)
     mats = [(ROWS, COLS, 1, 1)]
-    info = mb.describe_plan(mats, True)
-    assert ROWS * COLS * 2 < 2 ** 31 <= ROWS * (COLS + 8 * 1024) * 2
-    announce(f"largest operand {ROWS} x {COLS} bf16: Z {ROWS * COLS * 2} bytes, tiles "
+    info = mb.describe_plan(mats, True, opts)
+    with pytest.raises(mb.MuonBPError):
+        mb.describe_plan([(ROWS + 8, COLS, 1, 1)], True, opts)
+    announce(f"largest operand {ROWS} x {COLS} {dtype}: Z {ROWS * COLS * es} bytes, tiles "
              f"{[(info.gemm_tile_rows[k], info.gemm_tile_cols[k], info.gemm_tiles[k]) for k in range(3)]}")
-    # Seeded inputs drawn on the GPU (1.07 G elements each); the checks copy
-    # back what they compare.
+    # Seeded inputs drawn on the GPU; the checks copy back what they compare.
     gen = torch.Generator(device="cuda").manual_seed(2026)
-    g_dev = (torch.randn((ROWS, COLS), generator=gen, device="cuda") * 0.01).to(torch.bfloat16)
-    x_dev = (torch.randn((ROWS, COLS), generator=gen, device="cuda") * 0.02).to(torch.bfloat16)
+    g_dev = (torch.randn((ROWS, COLS), generator=gen, device="cuda") * 0.01).to(tdt)
+    x_dev = (torch.randn((ROWS, COLS), generator=gen, device="cuda") * 0.02).to(tdt)
     cols = [slice(0, 100000), slice(COLS - 100000, COLS)]
     x0 = [x_dev[:, cs].double().cpu().numpy() for cs in cols]
-    opt = mb.MuonBP(mats, 1, LR, LR, MU, WD)
+    opt = mb.MuonBP(mats, 1, LR, LR, MU, WD, options=opts)
     opt.step([x_dev], [g_dev], 0)
     m_dev = opt.get_momentum(0)
     u_dev = opt.get_update(0)
@@ -99,7 +115,7 @@ def test_largest_accepted_operand_against_oracle():
     del ref
 
     # Update on the first and last 100000 columns: one step of Alg. 1 from
-    # x0 with the GPU's U, at most one bf16 unit in the last place apart.
+    # x0 with the GPU's U, at most one unit in the last place apart.
     for cs, a, b in zip(cols, x0, x1):
-        want = update_reference(a, u[:, cs], LR, WD, 1.0, "bf16")
-        assert ulp_distance(b, want, "bf16") <= 1.0
+        want = update_reference(a, u[:, cs], LR, WD, 1.0, dtype)
+        assert ulp_distance(b, want, dtype) <= 1.0
