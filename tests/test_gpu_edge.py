@@ -4,8 +4,8 @@ The NS kernels address an operand with 32-bit byte offsets, and the planner
 refuses any unit whose Z, A or B reaches 2^31 bytes.  This test runs a unit
 just under that limit: one 264 x 4065000 bf16 matrix (Z is 2.146e9 bytes;
 the column count is near the planner's tile-index limit of 65535 tiles of
-64) on the DMA kernels, and one 124 x 4065000 fp32 matrix on the
-register-loop kernels (its Z^T is 2.08e9 bytes).  Eight more rows are
+64) on the DMA kernels, and one 1020 x 524280 fp32 matrix on the
+register-loop kernels (its Z^T is 2.1474e9 bytes).  Eight more rows are
 refused in either case.  Neither row count is a multiple of a tile height,
 so the last tile row of every product holds rows past M, and the bf16
 apply's K loop (K = S = 264) ends in a partial slice followed by slices
@@ -27,18 +27,13 @@ from tests.gpu_harness import announce, rel, ulp_distance, update_reference
 
 pytestmark = pytest.mark.gpu
 
-COLS = 4065000
 LR, MU, WD = 0.02, 0.95, 0.1
-# (dtype, rows, relative bar): bf16 on the DMA kernels, fp32 on the
-# register-loop kernels (4-byte operands, and Z^T of L x 128 kept as well).
-# Eight more rows are refused in either case.  The fp32 bar: each Gram
-# entry is one fp32 accumulator over K = 4065000 products, each product
-# only a few units in the last place of the running sum (a diagonal term is
-# about 1 / (124 K) against a sum of 1 / 124), so additions lose most of
-# their bits.  Measured U error against the fp64 oracle at K = 40650,
-# 406500, 4065000: 1.1e-6, 2.2e-5, 6.9e-4 (the 1e-4 bar of the fp32 parity
-# cases assumes K of a few thousand), so 1e-3 here.
-CASES = [("bf16", 264, 2e-2), ("f32", 124, 1e-3)]
+# (dtype, rows, cols, relative bar): bf16 on the DMA kernels (Z of 2.146e9
+# bytes, the column count near the planner's tile-index limit), fp32 on the
+# register-loop kernels (4-byte operands, and Z^T of L x 1024 kept as well:
+# 2.1474e9 bytes, 32 bytes under 2^31).  Eight more rows are refused in
+# either case.
+CASES = [("bf16", 264, 4065000, 2e-2), ("f32", 1020, 524280, 1e-4)]
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -72,8 +67,8 @@ def _tile_errors(u, ref, tile=64, chunk=1 << 18):
     return float(np.max(np.sqrt(d2) / den))
 
 
-@pytest.mark.parametrize("dtype,ROWS,TOL", CASES, ids=[c[0] for c in CASES])
-def test_largest_accepted_operand_against_oracle(dtype, ROWS, TOL):
+@pytest.mark.parametrize("dtype,ROWS,COLS,TOL", CASES, ids=[c[0] for c in CASES])
+def test_largest_accepted_operand_against_oracle(dtype, ROWS, COLS, TOL):
     import torch
     from paper_2510_16981_amd import muonbp as mb
 
