@@ -51,9 +51,11 @@ constexpr int64_t kFuseScaleMaxReads = int64_t(1) << 20;
 // their tiles' K loops as the tile table says; ksum holds the fp32 partial
 // sums (tiles x nsplit x tile area floats) and kcount one zeroed counter per
 // tile (left zeroed on return).
+// long_k (fp32 register-loop 128 x 128 variants): sums restarted every
+// 2048 terms, for products over very long K.
 hipError_t launch_ns_gemm(DType ns_t, int variant, bool nn, int n_tiles, const GemmDesc* probs,
                           const TileRef* tiles, int nsplit, float* ksum, int* kcount,
-                          hipStream_t s);
+                          hipStream_t s, bool long_k = false);
 
 // X <- X (1 - eta lambda) - eta s_b U_b over every block segment.
 hipError_t launch_update(DType param_t, DType ns_t, bool vec, bool nt, int n_segs,

@@ -571,7 +571,7 @@ struct GemmShape {
 // K loop over every KS-th slice with their own LDS buffers, and the partial
 // sums are added in LDS (a fixed order) before the epilogue.  Used when a
 // launch has too few tiles to give every CU two workgroups.
-template <typename T, int BM, int BN, int KS>
+template <typename T, int BM, int BN, int KS, bool TWO = false>
 __global__ __launch_bounds__(kThreads * KS) void k_ns_gemm(const GemmDesc* __restrict__ probs,
                                                            const TileRef* __restrict__ tiles) {
   using G = GemmShape<T, BM, BN, KS>;
@@ -649,6 +649,25 @@ __global__ __launch_bounds__(kThreads * KS) void k_ns_gemm(const GemmDesc* __res
     for (int j = 0; j < TN; ++j)
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+  // TWO (fp32, launches over a very long K): the accumulators are added
+  // into a second set every kFlush iterations (kFlush x 32 K) and
+  // restarted, so that no fp32 sum runs over more than 2048 products.  Over
+  // a long K one accumulator per output loses most of each product's bits
+  // once the products are a few units in the last place of the running sum
+  // (a 124-row unit's U was 6.9e-4 from the fp64 result at K = 4065000).
+  // The second set costs 64 registers (one workgroup per CU instead of
+  // two), so shorter launches keep the single set.
+  constexpr bool kTwoLevel = TWO && std::is_same<T, float>::value && TM * TN <= 4;
+  constexpr int kFlush = 64;
+  f32x16_t hi[kTwoLevel ? TM : 1][kTwoLevel ? TN : 1];
+  if constexpr (kTwoLevel) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) hi[i][j][v] = 0.f;
+  }
 
   // Group grp handles K slices kt = KS it + grp, it < niter (the same count
   // in every group, so all threads meet every barrier); slices past K load
@@ -692,8 +711,26 @@ __global__ __launch_bounds__(kThreads * KS) void k_ns_gemm(const GemmDesc* __res
         for (int j = 0; j < TN; ++j) acc[i][j] = Mfma<T>::step(a[s & 1][i], b[s & 1][j], acc[i][j]);
       __builtin_amdgcn_sched_barrier(0);
     }
+    if constexpr (kTwoLevel) {
+      if (it % kFlush == kFlush - 1) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j) {
+            hi[i][j] += acc[i][j];
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+          }
+      }
+    }
     if (it + 1 < niter) lstore(buf ^ 1);
     __syncthreads();
+  }
+  if constexpr (kTwoLevel) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j) acc[i][j] = hi[i][j] + acc[i][j];
   }
   if (KS > 1) {
     // Groups 1.. hand their partial sums to group 0 through LDS, register by
@@ -1438,7 +1475,7 @@ hipError_t launch_pack(DType mom_t, DType grad_t, DType ns_t, bool vec, int n_ti
 
 hipError_t launch_ns_gemm(DType ns_t, int variant, bool nn, int n_tiles, const GemmDesc* probs,
                           const TileRef* tiles, int nsplit, float* ksum, int* kcount,
-                          hipStream_t s) {
+                          hipStream_t s, bool long_k) {
   if (nsplit > 1 && (!ksum || !kcount || !gemm_is_dmap(variant))) return hipErrorInvalidValue;
   if (nn && !gemm_is_dmap(variant)) return hipErrorInvalidValue;
   if (n_tiles <= 0) return hipSuccess;
@@ -1446,8 +1483,12 @@ hipError_t launch_ns_gemm(DType ns_t, int variant, bool nn, int n_tiles, const G
     using TN = decltype(n);
     switch (variant) {
       case kGemm128x128:
-        hipLaunchKernelGGL((k_ns_gemm<TN, 128, 128, 1>), dim3(n_tiles), dim3(kThreads), 0, s, probs,
-                           tiles);
+        if (long_k && std::is_same<TN, float>::value)
+          hipLaunchKernelGGL((k_ns_gemm<TN, 128, 128, 1, true>), dim3(n_tiles), dim3(kThreads), 0, s,
+                             probs, tiles);
+        else
+          hipLaunchKernelGGL((k_ns_gemm<TN, 128, 128, 1>), dim3(n_tiles), dim3(kThreads), 0, s, probs,
+                             tiles);
         break;
       case kGemm256x128:
         hipLaunchKernelGGL((k_ns_gemm<TN, 256, 128, 1>), dim3(n_tiles), dim3(kThreads), 0, s, probs,
@@ -1458,8 +1499,12 @@ hipError_t launch_ns_gemm(DType ns_t, int variant, bool nn, int n_tiles, const G
                            tiles);
         break;
       case kGemm128x128Split2:
-        hipLaunchKernelGGL((k_ns_gemm<TN, 128, 128, 2>), dim3(n_tiles), dim3(2 * kThreads), 0, s,
-                           probs, tiles);
+        if (long_k && std::is_same<TN, float>::value)
+          hipLaunchKernelGGL((k_ns_gemm<TN, 128, 128, 2, true>), dim3(n_tiles), dim3(2 * kThreads), 0,
+                             s, probs, tiles);
+        else
+          hipLaunchKernelGGL((k_ns_gemm<TN, 128, 128, 2>), dim3(n_tiles), dim3(2 * kThreads), 0, s,
+                             probs, tiles);
         break;
       case kGemmDmaP128x128:
       case kGemmDmaP256x128:

@@ -107,7 +107,7 @@ int32_t slot_of(GemmKind kind, int iter, int ns_steps, int poly_slots) {
 
 // Launch schedule of the K NS iterations: three launches per iteration
 // (every problem's Gram, then polynomial, then apply).
-void build_phases(Plan* plan, int ns_steps, int poly_slots, int desc_per_problem) {
+void build_phases(Plan* plan, int ns_steps, int poly_slots, int desc_per_problem, int ns_elem_bytes) {
   plan->phases.clear();
   plan->split_floats = plan->split_slots = 0;
   const int32_t np = int32_t(plan->probs.size());
@@ -118,6 +118,12 @@ void build_phases(Plan* plan, int ns_steps, int poly_slots, int desc_per_problem
       phase.kind = kind;
       phase.nsplit = plan->nsplit[kind];
       phase.nn = kind == kApply && plan->nn_apply;
+      if (ns_elem_bytes == 4 && !gemm_is_dmap(phase.variant))
+        for (const Problem& p : plan->probs) {
+          int64_t m, n, k;
+          gemm_dims(p, GemmKind(kind), &m, &n, &k);
+          phase.long_k = phase.long_k || k > kLongK;
+        }
       std::vector<TileRef> logical;
       for (int32_t pi = 0; pi < np; ++pi)
         append_tiles(plan->probs[pi], GemmKind(kind), phase.variant,
@@ -433,7 +439,7 @@ std::string build_layout(const MatrixShape* mats, int32_t n_mats,
       plan.ns_dense_flops += ns_unit_dense_flops(p.S, p.L, ns_steps);
     }
     plan.ws_elems = cursor;
-    build_phases(&plan, ns_steps, poly_slots, kSlotPoly0 + poly_slots);
+    build_phases(&plan, ns_steps, poly_slots, kSlotPoly0 + poly_slots, ns_elem_bytes);
     if (plan.pack_tiles.size() > size_t(std::numeric_limits<int32_t>::max() / 2))
       return "too many tiles";
   }

@@ -73,8 +73,13 @@ struct GemmPhase {
   int32_t kind = 0;            // GemmKind
   int32_t nsplit = 1;          // workgroups per tile, each on a share of K
   bool nn = false;             // apply reading Z row-major (no Z^T operand)
+  // fp32 register-loop kernel with a product over more than kLongK terms:
+  // the variant that restarts its sums every 2048 terms (see k_ns_gemm).
+  bool long_k = false;
   std::vector<TileRef> tiles;  // workgroup order
 };
+
+constexpr int64_t kLongK = 65536;
 
 struct Plan {
   bool full = false;

@@ -141,7 +141,7 @@ hipError_t enqueue_after_momentum(const muonbp_options& o, const Plan& plan, con
     const GemmPhase& P = plan.phases[ph];
     e = wrap(kKindGram + P.kind, [&] {
       return launch_ns_gemm(tn, P.variant, P.nn, int(P.tiles.size()), pv.descs, pv.phase_tiles[ph],
-                            P.nsplit, b.ksum, b.kcount, s);
+                            P.nsplit, b.ksum, b.kcount, s, P.long_k);
     });
     if (e != hipSuccess) return e;
   }

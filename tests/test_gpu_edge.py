@@ -33,7 +33,10 @@ LR, MU, WD = 0.02, 0.95, 0.1
 # register-loop kernels (4-byte operands, and Z^T of L x 1024 kept as well:
 # 2.1474e9 bytes, 32 bytes under 2^31).  Eight more rows are refused in
 # either case.
-CASES = [("bf16", 264, 4065000, 2e-2), ("f32", 1020, 524280, 1e-4)]
+CASES = [("bf16", 264, 4065000, 2e-2), ("f32", 1020, 524280, 1e-4),
+         # fp32 over the longest K: the Gram's sums restart every 2048 terms
+         # (one fp32 sum over all 4065000 was 6.9e-4 from the fp64 U).
+         ("f32", 124, 4065000, 1e-4)]
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -67,7 +70,7 @@ def _tile_errors(u, ref, tile=64, chunk=1 << 18):
     return float(np.max(np.sqrt(d2) / den))
 
 
-@pytest.mark.parametrize("dtype,ROWS,COLS,TOL", CASES, ids=[c[0] for c in CASES])
+@pytest.mark.parametrize("dtype,ROWS,COLS,TOL", CASES, ids=[f"{c[0]}-{c[1]}x{c[2]}" for c in CASES])
 def test_largest_accepted_operand_against_oracle(dtype, ROWS, COLS, TOL):
     import torch
     from paper_2510_16981_amd import muonbp as mb
@@ -78,8 +81,9 @@ def test_largest_accepted_operand_against_oracle(dtype, ROWS, COLS, TOL):
     opts = mb.options_default(param_dtype=code, state_dtype=code, ns_dtype=code)
     mats = [(ROWS, COLS, 1, 1)]
     info = mb.describe_plan(mats, True, opts)
-    with pytest.raises(mb.MuonBPError):
-        mb.describe_plan([(ROWS + 8, COLS, 1, 1)], True, opts)
+    if ROWS * COLS * es > 2 ** 30:  # the two cases at the operand limit
+        with pytest.raises(mb.MuonBPError):
+            mb.describe_plan([(ROWS + 8, COLS, 1, 1)], True, opts)
     announce(f"largest operand {ROWS} x {COLS} {dtype}: Z {ROWS * COLS * es} bytes, tiles "
              f"{[(info.gemm_tile_rows[k], info.gemm_tile_cols[k], info.gemm_tiles[k]) for k in range(3)]}")
     # Seeded inputs drawn on the GPU; the checks copy back what they compare.
