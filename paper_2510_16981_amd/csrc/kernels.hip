@@ -20,6 +20,23 @@ typedef __bf16 bf16;
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+
+// Global-address-space views of device pointers: accesses through them
+// compile to global_load / global_store.  A generic (flat) access counts
+// against the LDS wait counter as well as the memory one, so every LDS wait
+// issued after it (the GEMM epilogue's staged reads, the pack's transpose,
+// the K loop's fragment reads) would also wait for that memory access to
+// complete.  The integer round trip makes the compiler take the address
+// space.
+typedef __attribute__((address_space(1))) u32x4_t g_u32x4_t;
+__device__ __forceinline__ g_u32x4_t* gvec(const void* p) {
+  return (g_u32x4_t*)(reinterpret_cast<uintptr_t>(p));
+}
+template <typename T>
+__device__ __forceinline__ void gstore1(T* p, T v) {
+  *(__attribute__((address_space(1))) T*)(reinterpret_cast<uintptr_t>(p)) = v;
+}
 
 constexpr int kThreads = 256;
 
@@ -40,7 +57,7 @@ template <typename T> __device__ __forceinline__ float rt(float x) {
 
 // Eight consecutive elements <-> floats (pointer 16-byte aligned).
 __device__ __forceinline__ void load8(const bf16* p, float f[8]) {
-  const uint4 v = *reinterpret_cast<const uint4*>(p);
+  const u32x4_t v = *gvec(p);
   const uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -49,23 +66,30 @@ __device__ __forceinline__ void load8(const bf16* p, float f[8]) {
   }
 }
 __device__ __forceinline__ void load8(const float* p, float f[8]) {
-  const float4 a = reinterpret_cast<const float4*>(p)[0];
-  const float4 b = reinterpret_cast<const float4*>(p)[1];
-  f[0] = a.x; f[1] = a.y; f[2] = a.z; f[3] = a.w;
-  f[4] = b.x; f[5] = b.y; f[6] = b.z; f[7] = b.w;
+  const u32x4_t a = gvec(p)[0], b = gvec(p)[1];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    f[i] = __uint_as_float(a[i]);
+    f[4 + i] = __uint_as_float(b[i]);
+  }
 }
 __device__ __forceinline__ void store8(bf16* p, const float f[8]) {
   union {
     bf16 h[8];
-    uint4 v;
+    u32x4_t v;
   } u;
 #pragma unroll
   for (int i = 0; i < 8; ++i) u.h[i] = bf16(f[i]);
-  *reinterpret_cast<uint4*>(p) = u.v;
+  *gvec(p) = u.v;
 }
 __device__ __forceinline__ void store8(float* p, const float f[8]) {
-  reinterpret_cast<float4*>(p)[0] = make_float4(f[0], f[1], f[2], f[3]);
-  reinterpret_cast<float4*>(p)[1] = make_float4(f[4], f[5], f[6], f[7]);
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    u32x4_t v;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) v[k] = __float_as_uint(f[4 * i + k]);
+    gvec(p)[i] = v;
+  }
 }
 
 // Eight consecutive elements as raw 16-byte words.  NT: loaded and stored
@@ -73,13 +97,12 @@ __device__ __forceinline__ void store8(float* p, const float f[8]) {
 // written once per step) is far larger than the last-level cache; smaller
 // steps keep plain accesses, whose data stays cache-resident between the
 // kernels of a step.
-typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 template <typename T> struct Raw8 {
   u32x4_t w[sizeof(T) / 2];
 };
 template <bool NT, typename T> __device__ __forceinline__ Raw8<T> load8r(const T* p) {
   Raw8<T> r;
-  const u32x4_t* q = reinterpret_cast<const u32x4_t*>(p);
+  g_u32x4_t* q = gvec(p);
 #pragma unroll
   for (int i = 0; i < int(sizeof(T) / 2); ++i) r.w[i] = NT ? __builtin_nontemporal_load(q + i) : q[i];
   return r;
@@ -97,9 +120,9 @@ __device__ __forceinline__ void unpack8(const Raw8<float>& r, float f[8]) {
 }
 template <bool NT> __device__ __forceinline__ void store_w(u32x4_t* p, u32x4_t v) {
   if (NT)
-    __builtin_nontemporal_store(v, p);
+    __builtin_nontemporal_store(v, gvec(p));
   else
-    *p = v;
+    *gvec(p) = v;
 }
 template <bool NT> __device__ __forceinline__ void store8r(bf16* p, const float f[8]) {
   union {
@@ -315,7 +338,7 @@ __global__ __launch_bounds__(kThreads) void k_pack(
         if (r + 8 <= d.rows) {
           store8(p, y);
         } else {
-          for (int e = 0; e < d.rows - r; ++e) p[e] = from_f<TN>(y[e]);
+          for (int e = 0; e < d.rows - r; ++e) gstore1(p + e, from_f<TN>(y[e]));
         }
       }
     }
@@ -331,7 +354,7 @@ __global__ __launch_bounds__(kThreads) void k_pack(
       y = to_f<TM>(m[o]);
       if (nesterov) y = fmaf(mu, y, to_f<TG>(g[o]));
       y *= s;
-      if (ds) ds[int64_t(r) * d.ld_s + c] = from_f<TN>(y);
+      if (ds) gstore1(ds + int64_t(r) * d.ld_s + c, from_f<TN>(y));
     }
     tile[lr + 4 * i][lc] = y;
   }
@@ -340,7 +363,7 @@ __global__ __launch_bounds__(kThreads) void k_pack(
 #pragma unroll 4
   for (int i = 0; i < 16; ++i) {
     const int c = c0 + lr + 4 * i, r = r0 + lc;
-    if (r < d.rows && c < d.cols) dt[int64_t(c) * d.ld_t + r] = from_f<TN>(tile[lc][lr + 4 * i]);
+    if (r < d.rows && c < d.cols) gstore1(dt + int64_t(c) * d.ld_t + r, from_f<TN>(tile[lc][lr + 4 * i]));
   }
 }
 
@@ -376,15 +399,10 @@ template <> struct Mfma<float> {
   }
 };
 
-typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(1))) const u32x4_t gu32x4_t;
-
-// 16-byte load through the global address space (global_load rather than
-// flat_load: flat loads also count against the LDS wait counter, so every
-// LDS wait in the K loop would also wait for the prefetch).  The integer
-// round trip makes the compiler emit an address-space-1 access.
+// 16-byte load through the global address space (the register-staged K
+// loop's prefetch: a flat load would make its LDS waits wait for it).
 __device__ __forceinline__ uint4 gld16(const void* p) {
-  const u32x4_t v = *(gu32x4_t*)(reinterpret_cast<uintptr_t>(p));
+  const u32x4_t v = *gvec(p);
   return make_uint4(v.x, v.y, v.z, v.w);
 }
 
@@ -453,7 +471,7 @@ __device__ __forceinline__ void store_chunk(T* out, int ld, int row, int col, in
   if (col + 8 <= nc) {
     store8(p, f);
   } else {
-    for (int e = 0; e < nc - col; ++e) p[e] = from_f<T>(f[e]);
+    for (int e = 0; e < nc - col; ++e) gstore1(p + e, from_f<T>(f[e]));
   }
 }
 
@@ -463,8 +481,11 @@ __device__ __forceinline__ void store_chunk(T* out, int ld, int row, int col, in
 // modulo WM WN so that the second K group of a split workgroup mirrors the
 // first).  st: this wave's free LDS block of 32 * (32 TN + 1) floats.
 // gamma is added on the diagonal of C (row == column).  Waves with
-// active == false only take part in the workgroup barriers.
-template <typename T, int TM, int TN, int WM = 2, int WN = 2>
+// active == false only take part in the workgroup barriers.  WG_SYNC =
+// false: no workgroup barrier between the passes (every wave stages in its
+// own block and the LDS runs one wave's accesses in order, so a wave needs
+// no other wave to reach a pass boundary).
+template <typename T, int TM, int TN, int WM = 2, int WN = 2, bool WG_SYNC = true>
 __device__ __forceinline__ void gemm_epilogue(f32x16_t (&acc)[TM][TN], float* st,
                                               const GemmDesc& d, int m0, int n0, bool diag,
                                               float alpha, float beta, float gamma,
@@ -518,7 +539,7 @@ __device__ __forceinline__ void gemm_epilogue(f32x16_t (&acc)[TM][TN], float* st
       for (int v = 0; v < 16; ++v)
         st[(8 * (v >> 2) + 4 * (lane >> 5) + (v & 3)) * P + j * 32 + (lane & 31)] = alpha * acc[i][j][v];
     if (i + 1 < TM && has_d && active) load_d(i + 1, dv[(i + 1) & 1]);
-    __syncthreads();
+    if constexpr (WG_SYNC) __syncthreads();
 #pragma unroll
     for (int c = 0; c < CPL && active; ++c) {
       const int q = lane + 64 * c, r = q / NCH, ch = q - r * NCH;
@@ -533,7 +554,7 @@ __device__ __forceinline__ void gemm_epilogue(f32x16_t (&acc)[TM][TN], float* st
         for (int e = 0; e < 8; ++e) st[r * P + 8 * ch + e] = f[e];
       }
     }
-    if (mirror && has_d) __syncthreads();
+    if (WG_SYNC && mirror && has_d) __syncthreads();
     if (mirror && active) {
 #pragma unroll
       for (int c = 0; c < CPL; ++c) {
@@ -544,7 +565,133 @@ __device__ __forceinline__ void gemm_epilogue(f32x16_t (&acc)[TM][TN], float* st
         store_chunk<T>(Ct, d.ldct, wc0 + rr, r0 + 8 * cc, d.N, d.M, f);
       }
     }
-    __syncthreads();
+    if constexpr (WG_SYNC) __syncthreads();
+  }
+}
+
+// 16-byte buffer store at byte offset voff; a store at or past the
+// descriptor's byte count is dropped.
+__device__ __forceinline__ void bst16(__amdgpu_buffer_rsrc_t r, u32x4_t v, uint32_t voff) {
+  __builtin_amdgcn_raw_buffer_store_b128(v, r, voff, 0, 0);
+}
+
+__device__ __forceinline__ u32x4_t pack_bf16x8(const float f[8]) {
+  union {
+    bf16 h[8];
+    u32x4_t v;
+  } u;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) u.h[i] = bf16(f[i]);
+  return u.v;
+}
+
+// Epilogue of the LDS-DMA kernel (bf16 C and Ct): the arithmetic of
+// gemm_epilogue in the same order (alpha acc, then + beta D, then + gamma
+// on the diagonal, one rounding to bf16), with the per-chunk work cut
+// down for tiles whose rows of C (and of Ct) are whole 8-element chunks:
+// buffer stores whose offset splits into a per-lane part fixed for the
+// tile and a wave-uniform part per pass, rows past the matrix sent past
+// the descriptor's byte count (the hardware drops them), the diagonal
+// term only on passes that cross the diagonal, and no workgroup barriers
+// (every wave stages in its own block, and the LDS runs one wave's
+// accesses in order).  Other tiles take gemm_epilogue.
+template <int TM, int TN, int WM, int WN>
+__device__ __forceinline__ void dma_epilogue(f32x16_t (&acc)[TM][TN], float* st, const GemmDesc& d, int m0,
+                                             int n0, bool diag) {
+  constexpr int ES = 2;
+  constexpr int P = 32 * TN + 1;
+  constexpr int NCH = 4 * TN;         // 8-element chunks per staged row
+  constexpr int CPL = 32 * NCH / 64;  // chunks per lane, C and Ct alike
+  const int lane = threadIdx.x & 63, wave = (threadIdx.x >> 6) % (WM * WN);
+  const int wm = wave / WN, wn = wave % WN;
+  const int wr0 = m0 + wm * 32 * TM, wc0 = n0 + wn * 32 * TN;
+  const bool mirror = d.Ct != nullptr && !diag;
+  const bool has_d = d.D != nullptr;
+  const float alpha = d.alpha, beta = d.beta, gamma = d.gamma;
+  if (d.N % 8 != 0 || (mirror && d.M % 8 != 0)) {
+    gemm_epilogue<bf16, TM, TN, WM, WN, false>(acc, st, d, m0, n0, diag, alpha, beta, gamma);
+    return;
+  }
+  // Byte offsets as the sum of a per-lane part fixed for the tile (row and
+  // column within the wave block) and a wave-uniform part per pass (the
+  // block's origin).  A chunk outside the matrix takes the byte count
+  // itself as its offset, so that no offset reaches 2^31 (the bounds check
+  // does not drop offsets from 2^31 up).
+  const uint32_t cbytes = d.C ? uint32_t(d.M) * uint32_t(d.ldc) * ES : 0u;
+  const uint32_t tbytes = mirror ? uint32_t(d.N) * uint32_t(d.ldct) * ES : 0u;
+  const uint32_t dbytes = has_d ? uint32_t(d.M) * uint32_t(d.ldd) * ES : 0u;
+  const __amdgpu_buffer_rsrc_t cr = __builtin_amdgcn_make_buffer_rsrc(d.C ? d.C : d.Ct, 0, cbytes, kBufferWord3);
+  const __amdgpu_buffer_rsrc_t tr = __builtin_amdgcn_make_buffer_rsrc(d.Ct ? d.Ct : d.C, 0, tbytes, kBufferWord3);
+  const __amdgpu_buffer_rsrc_t dr = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<void*>(has_d ? d.D : d.X), 0, dbytes, kBufferWord3);
+  // Per lane: row and column of each C chunk within the 32-row block of a
+  // pass, and of each Ct chunk within the wave's block of Ct; whether a C
+  // chunk's columns (a Ct chunk's rows) lie inside the matrix.
+  int crow[CPL], ccol[CPL], trow[CPL], tcol[CPL];
+  bool cin[CPL], tin[CPL];
+  uint32_t coff[CPL], doff[CPL], toff[CPL];
+#pragma unroll
+  for (int c = 0; c < CPL; ++c) {
+    const int q = lane + 64 * c;
+    crow[c] = q / NCH;
+    ccol[c] = 8 * (q - crow[c] * NCH);
+    trow[c] = q >> 2;
+    tcol[c] = 8 * (q & 3);
+    cin[c] = wc0 + ccol[c] < d.N;
+    tin[c] = wc0 + trow[c] < d.N;
+    coff[c] = uint32_t(crow[c] * d.ldc + ccol[c]) * ES;
+    doff[c] = uint32_t(crow[c] * d.ldd + ccol[c]) * ES;
+    toff[c] = uint32_t(trow[c] * d.ldct + tcol[c]) * ES;
+  }
+  uint4 dv[2][CPL];
+  auto load_d = [&](int i, uint4 (&buf)[CPL]) {
+    const int r0 = wr0 + 32 * i;
+    const uint32_t so = r0 < d.M ? uint32_t(r0 * d.ldd + wc0) * ES : 0u;
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) {
+      const bool in = cin[c] && r0 + crow[c] < d.M;
+      const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(dr, in ? doff[c] + so : dbytes, 0, 0);
+      buf[c] = make_uint4(v.x, v.y, v.z, v.w);
+    }
+  };
+  if (has_d) load_d(0, dv[0]);
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+    const int r0 = wr0 + 32 * i;
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v)
+        st[(8 * (v >> 2) + 4 * (lane >> 5) + (v & 3)) * P + j * 32 + (lane & 31)] = alpha * acc[i][j][v];
+    if (i + 1 < TM && has_d) load_d(i + 1, dv[(i + 1) & 1]);
+    // The diagonal crosses this pass's 32 x 32 TN block.
+    const bool dg = gamma != 0.f && r0 < wc0 + 32 * TN && wc0 < r0 + 32;
+    if (d.C || (mirror && (has_d || dg))) {
+      const uint32_t so = r0 < d.M ? uint32_t(r0 * d.ldc + wc0) * ES : 0u;
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) {
+        float f[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) f[e] = st[crow[c] * P + ccol[c] + e];
+        if (has_d) add8<bf16>(f, &dv[i & 1][c], beta);
+        if (dg) add_diag(f, r0 + crow[c], wc0 + ccol[c], gamma);
+        if (d.C) bst16(cr, pack_bf16x8(f), cin[c] && r0 + crow[c] < d.M ? coff[c] + so : cbytes);
+        if (mirror && (has_d || dg)) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) st[crow[c] * P + ccol[c] + e] = f[e];
+        }
+      }
+    }
+    if (mirror) {
+      const uint32_t so = wc0 < d.N ? uint32_t(wc0 * d.ldct + r0) * ES : 0u;
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) {
+        float f[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) f[e] = st[(tcol[c] + e) * P + trow[c]];
+        bst16(tr, pack_bf16x8(f), tin[c] && r0 + tcol[c] < d.M ? toff[c] + so : tbytes);
+      }
+    }
   }
 }
 
@@ -1199,8 +1346,8 @@ __global__ __launch_bounds__(64 * WM * WN) void k_ns_gemm_dmap(const GemmDesc* _
     if (tid == 0) __hip_atomic_store(kcount + t.slot, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
   __syncthreads();
-  gemm_epilogue<T, TM, TN, WM, WN>(acc, reinterpret_cast<float*>(lds) + wave * 32 * (32 * TN + 1), d,
-                                   m0, n0, ti == tj && d.sym, d.alpha, d.beta, d.gamma);
+  dma_epilogue<TM, TN, WM, WN>(acc, reinterpret_cast<float*>(lds) + wave * 32 * (32 * TN + 1), d, m0, n0,
+                              ti == tj && d.sym);
 }
 
 // ---------------------------------------------------------------- update
