@@ -54,33 +54,35 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def ns_unit_flops(S, L, K):
-    """Algorithmic NS flops of one S x L unit: Gram and A A counted on their
-    distinct (symmetric) entries, B Z in full."""
-    return K * (S * (S + 1) * L + S * S * (S + 1) + 2 * S * S * L)
+def gram_space_unit(S, L, K, mode, apply_nn):
+    """Whether the library runs an S x L unit's K iterations in Gram space
+    (the planner's rule for bf16 NS; mode is the gram_iteration option)."""
+    if mode == 1 or not apply_nn or K < 2:
+        return False
+    return mode == 2 or (S >= 1024 and 4 * L >= 5 * S)
 
 
-def plan_flops(mats, full, K):
-    tot = 0.0
-    for r, c, gr, gc in mats:
-        units = [(r, c)] if full else [(r // gr, c // gc)] * (gr * gc)
-        for p, q in units:
-            tot += ns_unit_flops(min(p, q), max(p, q), K)
-    return tot
+GRAM_SEGMENT = 3  # Gram-space iterations per segment (the library's kGramSegment)
 
 
-def kind_flops(mats, full, K):
-    """Algorithmic flops of each NS product kind per step (symmetric
-    products counted once per distinct entry, as ns_unit_flops)."""
+def kind_flops(mats, full, K, mode=0, apply_nn=True):
+    """Flops of each NS product kind per step as the library computes them
+    (symmetric products counted once per distinct entry).  A unit that
+    iterates as printed: K Grams, K A A, K applies; a Gram-space unit, per
+    segment of n <= 3 iterations: one Gram, 4n - 3 symmetric S x S x S
+    products (launched, and profiled, with the polynomial) and one apply."""
     out = {"gram": 0.0, "poly": 0.0, "apply": 0.0}
+    segs = [min(GRAM_SEGMENT, K - k0) for k0 in range(0, K, GRAM_SEGMENT)]
     for r, c, gr, gc in mats:
         units = [(r, c)] if full else [(r // gr, c // gc)] * (gr * gc)
         for p, q in units:
             S, L = float(min(p, q)), float(max(p, q))
-            out["gram"] += K * S * (S + 1) * L
-            out["poly"] += K * S * S * (S + 1)
-            out["apply"] += K * 2 * S * S * L
+            g = gram_space_unit(S, L, K, mode, apply_nn)
+            out["gram"] += (len(segs) if g else K) * S * (S + 1) * L
+            out["poly"] += (sum(4 * n - 3 for n in segs) if g else K) * S * S * (S + 1)
+            out["apply"] += (len(segs) if g else K) * 2 * S * S * L
     return out
+
 
 
 # Dominant product shapes of the 8B-shaped model: MLP shards 1792 x 4096 on
@@ -730,6 +732,9 @@ def main():
                     help="skip timing the vendor library's GEMM on the dominant shapes")
     ap.add_argument("--tile-policy", type=int, default=0,
                     help="library option tile_policy (0: planner's choice)")
+    ap.add_argument("--gram-iteration", type=int, default=0,
+                    help="library option gram_iteration (0: Gram-space iteration where it saves "
+                         "time, 1: every iteration as printed, 2: Gram-space wherever allowed)")
     ap.add_argument("--copy-probe", type=int, metavar="MIB", default=None,
                     help="only run a plain copy of MIB MiB (counter calibration) and exit")
     ap.add_argument("--mfma-probe", action="store_true",
@@ -792,7 +797,8 @@ def main():
     params, grads, data = make_inputs(mats, rank)
     opt = mb.MuonBP(mats, period, lr_block, LR_FULL, MU, WD,
                     options=mb.options_default(ns_steps=K_NS, apply_mode=args.apply_mode,
-                                               k_split=args.k_split, tile_policy=args.tile_policy))
+                                               k_split=args.k_split, tile_policy=args.tile_policy,
+                                               gram_iteration=args.gram_iteration))
     torch.cuda.synchronize()
 
     t = 0
@@ -856,8 +862,10 @@ def main():
         detail = opt.profile_read()
         opt.profile_enable(0)
         span_ms, span_n = timed_prof[kind]["ns_span"]
-        flops = plan_flops(mats, full, K_NS)
         info = mb.describe_plan(mats, full, opt.options)
+        flops = info.ns_flops
+        kf = kind_flops(mats, full, K_NS, args.gram_iteration, bool(info.apply_nn))
+        assert abs(sum(kf.values()) - flops) <= 1e-9 * flops, "flop model out of step with the planner"
         per[kind] = {
             "steps_in_timed_region": nk,
             "ms_per_step": ms_step,
@@ -872,8 +880,8 @@ def main():
                                           if k != "ns_span"},
             "detail_launches": {k: v[1] for k, v in detail.items() if k != "ns_span"},
             "detail_gemm_tflops": {k: f * reps / (detail[k][0] * 1e-3) / 1e12
-                                   for k, f in kind_flops(mats, full, K_NS).items()
-                                   if detail[k][0] > 0},
+                                   for k, f in kf.items() if detail[k][0] > 0},
+            "gram_space_units": int(info.gram_units),
             "gemm_tiles": [f"{info.gemm_tile_rows[i]}x{info.gemm_tile_cols[i]}:{info.gemm_tiles[i]}"
                            for i in range(3)],
         }
@@ -896,7 +904,7 @@ def main():
 
     # Dominant kernel: the grouped NS GEMM (all three NS products) over the
     # launches of the timed region (block and full steps as scheduled).
-    tot_flops = sum(plan_flops(mats, k == "full", K_NS) * n_of[k] for k in kinds)
+    tot_flops = sum(per[k]["ns_flops_per_step"] * n_of[k] for k in kinds)
     tot_ms = sum(timed_prof[k]["ns_span"][0] for k in kinds)
     launches = sum(timed_prof[k]["ns_span"][1] for k in kinds)
     achieved = tot_flops / (tot_ms * 1e-3) / 1e12

@@ -134,6 +134,25 @@ typedef struct {
                                before any HIP call; 0 = no limit (default).
                                muonbp_plan_info.device_bytes is the size of
                                those three. */
+  int32_t gram_iteration;   /* how the K NS iterations of a unit run (the
+                               result is Alg. 2's, up to rounding).  Every
+                               polynomial of Alg. 2 is a polynomial in
+                               A_0 = Z_0 Z_0^T, so the iterations can run on
+                               S x S matrices only: P_k = a_k I + b_k A_k +
+                               c_k A_k^2, A_{k+1} = A_k P_k^2, Q_k = P_k
+                               Q_{k-1}, and one apply U = Q_{K-1} Z_0 ends
+                               them (4K - 3 symmetric S x S x S products, one
+                               S x S x L Gram and one S x L x S apply, against
+                               K of each of the three as printed).
+                               0 = that Gram-space iteration on the units
+                               where it saves time (bf16 NS, the row-major
+                               apply, K >= 2, S >= 1024 and L >= 1.25 S;
+                               below S = 1024 its bf16 rounding error grows),
+                               as printed elsewhere (default); 1 = as
+                               printed everywhere; 2 = the Gram-space
+                               iteration on every unit that allows it (bf16,
+                               row-major apply, K >= 2), whatever its shape.
+                               It keeps two more S x S buffers per unit. */
 } muonbp_options;
 
 /* Fill *opt with the defaults above.  NULL is ignored. */
@@ -214,13 +233,17 @@ muonbp_status muonbp_synchronize(muonbp_ctx* ctx);
 typedef struct {
   int64_t n_problems;      /* orthogonalized units (blocks or matrices)     */
   int64_t n_elements;      /* parameters covered                            */
-  int64_t gemm_tiles[3];   /* workgroup tiles per NS iteration: Gram, poly,
-                              apply                                         */
+  int64_t gemm_tiles[3];   /* workgroup tiles per NS iteration as printed
+                              (every unit): Gram, poly, apply               */
   int32_t gemm_tile_rows[3], gemm_tile_cols[3]; /* their tile shapes         */
-  int64_t gemm_launches;   /* grouped GEMM launches per step (3 K)          */
-  double ns_flops;         /* algorithmic NS flops per step: per S x L unit
-                              and iteration S(S+1)L + S^2(S+1) + 2S^2 L
-                              (symmetric products counted once)             */
+  int64_t gemm_launches;   /* grouped GEMM launches per step (3 K as
+                              printed; up to 5 per iteration with Gram-space
+                              units, see gram_iteration)                    */
+  double ns_flops;         /* NS flops per step of the products as computed
+                              (symmetric products counted once): per S x L
+                              unit and iteration S(S+1)L + S^2(S+1) + 2S^2 L
+                              as printed; S(S+1)L + (4K-3) S^2(S+1) + 2S^2 L
+                              in all for a Gram-space unit                  */
   double ns_dense_flops;   /* Sec. 2.2 cost 2K(2 L S^2 + S^3), S <= L        */
   double elementwise_bytes;/* algorithmic HBM bytes of the non-NS kernels    */
   int64_t workspace_bytes; /* NS workspace this plan needs                  */
@@ -231,6 +254,8 @@ typedef struct {
                               MUONBP_STATIC_SCRATCH_BYTES)                    */
   int64_t device_bytes;    /* momentum + NS workspace + K-split sums of a
                               context for these matrices (both plans)       */
+  int64_t gram_units;      /* units that run the Gram-space iteration (see
+                              muonbp_options.gram_iteration)                */
 } muonbp_plan_info;
 
 /* Plan description for a set of matrices without creating a context

@@ -307,6 +307,7 @@ muonbp_status muonbp_describe_plan(const muonbp_matrix* mats, int32_t n_mats,
   out->workspace_bytes = p.ws_elems * int64_t(nb);
   out->static_scratch_bytes = scratch_plan(lay, full, o).total;
   out->device_bytes = context_bulk_bytes(lay, o);
+  for (const Problem& q : p.probs) out->gram_units += q.gram ? 1 : 0;
   return MUONBP_OK;
 }
 

@@ -5,6 +5,7 @@
 
 #include <algorithm>
 #include <limits>
+#include <utility>
 
 namespace muonbp {
 
@@ -26,7 +27,7 @@ constexpr int64_t kMaxOperandBytes = int64_t(1) << 31;
 // Lp or L x Sp); U of a transposed unit is written as Z^T into the buffer
 // the last apply would otherwise fill (off_zt aliases off_z).  Otherwise
 // (the transposed-copy apply, or the register-loop kernels): Z[2], Z^T[2],
-// A, B.
+// A, B.  A Gram-space unit adds Q[2] and T (S x Sp each).
 bool place_problem(Problem* p, int64_t* cursor, int64_t align_elems, bool nn) {
   auto take = [&](int64_t n) {
     int64_t at = *cursor;
@@ -46,6 +47,11 @@ bool place_problem(Problem* p, int64_t* cursor, int64_t align_elems, bool nn) {
   }
   p->off_a = take(as);
   p->off_b = take(as);
+  if (p->gram) {
+    p->off_q[0] = take(as);
+    p->off_q[1] = take(as);
+    p->off_t = take(as);
+  }
   return *cursor > 0 && *cursor < (int64_t(1) << 46);
 }
 
@@ -105,47 +111,84 @@ int32_t slot_of(GemmKind kind, int iter, int ns_steps, int poly_slots) {
                                 : kSlotApply0 + q;
 }
 
-// Launch schedule of the K NS iterations: three launches per iteration
-// (every problem's Gram, then polynomial, then apply).
+// Launch schedule of the K NS iterations.  Per iteration: the Gram (every
+// unit that iterates as printed; a Gram-space unit at the start of each
+// segment), the polynomial (every unit; a segment's first into Q[0]), then
+// for the Gram-space units the products Q_j = P_j Q_{j-1} and T = A_j P_j
+// together, and A_{j+1} = T P_j (none in a segment's last iteration), then
+// the apply (every unit that iterates as printed; a Gram-space unit's Z <-
+// Q Z at the end of each segment).  The Gram-space products take the
+// polynomial's tile shape (all are S x S x S).
 void build_phases(Plan* plan, int ns_steps, int poly_slots, int desc_per_problem, int ns_elem_bytes) {
   plan->phases.clear();
   plan->split_floats = plan->split_slots = 0;
   const int32_t np = int32_t(plan->probs.size());
-  for (int iter = 0; iter < ns_steps; ++iter)
-    for (int kind = 0; kind < 3; ++kind) {
-      GemmPhase phase;
-      phase.variant = plan->variant[kind];
-      phase.kind = kind;
-      phase.nsplit = plan->nsplit[kind];
-      phase.nn = kind == kApply && plan->nn_apply;
-      if (ns_elem_bytes == 4 && !gemm_is_dmap(phase.variant))
-        for (const Problem& p : plan->probs) {
-          int64_t m, n, k;
-          gemm_dims(p, GemmKind(kind), &m, &n, &k);
-          phase.long_k = phase.long_k || k > kLongK;
-        }
-      std::vector<TileRef> logical;
-      for (int32_t pi = 0; pi < np; ++pi)
-        append_tiles(plan->probs[pi], GemmKind(kind), phase.variant,
-                     pi * desc_per_problem + slot_of(GemmKind(kind), iter, ns_steps, poly_slots),
-                     &logical);
-      if (phase.nsplit > 1) {
-        // The shares of one tile are adjacent, so that the XCD order below
-        // keeps them on one XCD (one L2) as a rule.
-        std::vector<TileRef> parts;
-        parts.reserve(logical.size() * size_t(phase.nsplit));
-        for (size_t ti = 0; ti < logical.size(); ++ti)
-          for (int32_t q = 0; q < phase.nsplit; ++q)
-            parts.push_back(TileRef{logical[ti].prob, logical[ti].ij, int32_t(ti), q});
-        plan->split_slots = std::max<int64_t>(plan->split_slots, int64_t(logical.size()));
-        plan->split_floats = std::max<int64_t>(
-            plan->split_floats, int64_t(logical.size()) * phase.nsplit *
-                                    kGemmTileRows[phase.variant] * kGemmTileCols[phase.variant]);
-        logical.swap(parts);
+  using Item = std::pair<int32_t, int32_t>;  // (problem, descriptor slot)
+  auto add_phase = [&](GemmKind kind, const std::vector<Item>& items) {
+    if (items.empty()) return;
+    GemmPhase phase;
+    phase.variant = plan->variant[kind];
+    phase.kind = kind;
+    phase.nsplit = plan->nsplit[kind];
+    phase.nn = kind == kApply && plan->nn_apply;
+    std::vector<TileRef> logical;
+    for (const Item& it : items) {
+      const Problem& p = plan->probs[size_t(it.first)];
+      if (ns_elem_bytes == 4 && !gemm_is_dmap(phase.variant)) {
+        int64_t m, n, k;
+        gemm_dims(p, kind, &m, &n, &k);
+        phase.long_k = phase.long_k || k > kLongK;
       }
-      phase.tiles = xcd_order(logical);
-      plan->phases.push_back(std::move(phase));
+      append_tiles(p, kind, phase.variant, it.first * desc_per_problem + it.second, &logical);
     }
+    if (phase.nsplit > 1) {
+      // The shares of one tile are adjacent, so that the XCD order below
+      // keeps them on one XCD (one L2) as a rule.
+      std::vector<TileRef> parts;
+      parts.reserve(logical.size() * size_t(phase.nsplit));
+      for (size_t ti = 0; ti < logical.size(); ++ti)
+        for (int32_t q = 0; q < phase.nsplit; ++q)
+          parts.push_back(TileRef{logical[ti].prob, logical[ti].ij, int32_t(ti), q});
+      plan->split_slots = std::max<int64_t>(plan->split_slots, int64_t(logical.size()));
+      plan->split_floats = std::max<int64_t>(
+          plan->split_floats, int64_t(logical.size()) * phase.nsplit *
+                                  kGemmTileRows[phase.variant] * kGemmTileCols[phase.variant]);
+      logical.swap(parts);
+    }
+    phase.tiles = xcd_order(logical);
+    plan->phases.push_back(std::move(phase));
+  };
+  for (int iter = 0; iter < ns_steps; ++iter) {
+    std::vector<Item> gram, poly, qt, upd, apply;
+    for (int32_t pi = 0; pi < np; ++pi) {
+      const Problem& p = plan->probs[size_t(pi)];
+      if (!p.gram) {
+        gram.push_back({pi, slot_of(kGram, iter, ns_steps, poly_slots)});
+        poly.push_back({pi, slot_of(kPoly, iter, ns_steps, poly_slots)});
+        apply.push_back({pi, slot_of(kApply, iter, ns_steps, poly_slots)});
+        continue;
+      }
+      // Segment sg of n iterations, j-th of them.
+      const int sg = iter / kGramSegment, j = iter % kGramSegment;
+      const int n = std::min(kGramSegment, ns_steps - sg * kGramSegment);
+      const int nseg = (ns_steps + kGramSegment - 1) / kGramSegment;
+      const int32_t poly_b = slot_of(kPoly, iter, ns_steps, poly_slots);
+      if (j == 0) gram.push_back({pi, kSlotGram0 + (sg & 1)});
+      poly.push_back({pi, j == 0 ? poly_b + poly_slots : poly_b});
+      if (j > 0) qt.push_back({pi, (j & 1) ? kSlotQ1 : kSlotQ0});
+      if (j < n - 1) {
+        qt.push_back({pi, j == 0 ? kSlotT0 : kSlotT});
+        upd.push_back({pi, j == 0 ? kSlotA0 : kSlotA});
+      } else {
+        apply.push_back({pi, kSlotGApply0 + (sg & 1) + 2 * ((n - 1) & 1) + 4 * (sg == nseg - 1)});
+      }
+    }
+    add_phase(kGram, gram);
+    add_phase(kPoly, poly);
+    add_phase(kPoly, qt);
+    add_phase(kPoly, upd);
+    add_phase(kApply, apply);
+  }
 }
 
 }  // namespace
@@ -290,11 +333,21 @@ int32_t choose_split(const std::vector<Problem>& probs, GemmKind kind, int32_t v
   return 3;
 }
 
-double ns_unit_flops(int64_t S, int64_t L, int K) {
+double ns_unit_flops(int64_t S, int64_t L, int K, bool gram) {
   const double s = double(S), l = double(L);
-  // Gram Z Z^T: S(S+1)/2 distinct entries x 2L; A A: S(S+1)/2 x 2S;
-  // B Z: S x L entries x 2S.
-  return double(K) * (s * (s + 1) * l + s * s * (s + 1) + 2 * s * s * l);
+  // Gram Z Z^T: S(S+1)/2 distinct entries x 2L; a symmetric S x S x S
+  // product (A A, and the Gram-space Q, T and A products): S(S+1)/2 x 2S;
+  // B Z (the apply): S x L entries x 2S.
+  const double gram_zz = s * (s + 1) * l, sym = s * s * (s + 1), apply = 2 * s * s * l;
+  if (!gram || K == 0) return double(K) * (gram_zz + sym + apply);
+  // Per segment of n iterations: one Gram, n polynomials, n - 1 Q products,
+  // 2 (n - 1) A updates, one apply.
+  double f = 0;
+  for (int k0 = 0; k0 < K; k0 += kGramSegment) {
+    const int n = std::min(kGramSegment, K - k0);
+    f += gram_zz + (4.0 * n - 3.0) * sym + apply;
+  }
+  return f;
 }
 
 double ns_unit_dense_flops(int64_t S, int64_t L, int K) {
@@ -304,13 +357,14 @@ double ns_unit_dense_flops(int64_t S, int64_t L, int K) {
 
 std::string build_layout(const MatrixShape* mats, int32_t n_mats,
                          int ns_elem_bytes, int ns_steps, int poly_slots, int tile_policy,
-                         int k_split, int apply_mode, Layout* out, bool* shape_error) {
+                         int k_split, int apply_mode, Layout* out, bool* shape_error, int gram_mode) {
   *shape_error = false;
   if (!mats || n_mats <= 0) return "mats must be a non-empty array";
   if (ns_steps < 0) return "ns_steps must be >= 0";
   if (poly_slots < 1 || poly_slots > 64) return "poly_slots out of range";
   if (tile_policy < 0 || tile_policy > kNumGemmVariants) return "tile_policy out of range";
   if (k_split < 0 || k_split > kMaxKSplit) return "k_split out of range";
+  if (gram_mode < 0 || gram_mode > 2) return "gram_mode out of range";
   Layout L;
   L.mats.assign(mats, mats + n_mats);
   int64_t elems = 0;
@@ -332,7 +386,7 @@ std::string build_layout(const MatrixShape* mats, int32_t n_mats,
   }
   L.total_elems = elems;
   L.poly_slots = poly_slots;
-  L.desc_per_problem = kSlotPoly0 + poly_slots;
+  L.desc_per_problem = kSlotPoly0 + 2 * poly_slots;
 
   // Blocks in matrix order, row-major inside each grid; segments per block.
   for (int32_t k = 0; k < n_mats; ++k) {
@@ -433,13 +487,15 @@ std::string build_layout(const MatrixShape* mats, int32_t n_mats,
     int64_t cursor = 0;
     for (int32_t pi = 0; pi < int32_t(plan.probs.size()); ++pi) {
       Problem& p = plan.probs[pi];
+      p.gram = gram_mode != 1 && ns_elem_bytes == 2 && plan.nn_apply && ns_steps >= 2 &&
+               (gram_mode == 2 || (p.S >= kGramMinS && 4 * p.L >= 5 * p.S));
       if (!place_problem(&p, &cursor, align_elems, plan.nn_apply)) return "workspace too large";
       add_pack_tiles(&plan, pi);
-      plan.ns_flops += ns_unit_flops(p.S, p.L, ns_steps);
+      plan.ns_flops += ns_unit_flops(p.S, p.L, ns_steps, p.gram);
       plan.ns_dense_flops += ns_unit_dense_flops(p.S, p.L, ns_steps);
     }
     plan.ws_elems = cursor;
-    build_phases(&plan, ns_steps, poly_slots, kSlotPoly0 + poly_slots, ns_elem_bytes);
+    build_phases(&plan, ns_steps, poly_slots, L.desc_per_problem, ns_elem_bytes);
     if (plan.pack_tiles.size() > size_t(std::numeric_limits<int32_t>::max() / 2))
       return "too many tiles";
   }

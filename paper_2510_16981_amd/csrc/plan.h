@@ -48,6 +48,16 @@ struct Problem {
   int64_t off_b;      // B = b A + c A^2 (S x Sp)
   int32_t seg_begin, seg_end;
   int32_t first_block, n_blocks;
+  // Gram-space iteration: every polynomial of Alg. 2 is a polynomial in
+  // the Gram matrix of the iterate it starts from, so n iterations can run
+  // on S x S matrices only -- P_j = a I + b A_j + c A_j^2, A_{j+1} = A_j
+  // P_j^2 (as (A_j P_j) P_j), Q_j = P_j Q_{j-1} -- and one apply Z <- Q_{n-1}
+  // Z ends them.  The K iterations run in segments of at most
+  // kGramSegment such iterations, each starting from a fresh Gram of the
+  // current Z (segment s reads Z[s mod 2] and writes Z[(s + 1) mod 2]).
+  bool gram = false;
+  int64_t off_q[2] = {0, 0};  // Q ping-pong (S x Sp), Gram-space units only
+  int64_t off_t = 0;          // A_j P_j (S x Sp), Gram-space units only
 };
 
 // The three grouped products of one NS iteration.
@@ -55,8 +65,9 @@ enum GemmKind { kGram = 0, kPoly = 1, kApply = 2 };
 
 // GEMM descriptors per problem: Gram reading Z[0] / Z[1], apply reading
 // Z[0] / Z[1], the apply of the last iteration (which writes U where the
-// update reads it), then one polynomial per distinct iteration coefficient
-// set (kSlotPoly0 + k for iteration k, the last one repeated).
+// update reads it), the products of the Gram-space iteration (Problem::gram;
+// T is the Z[1] buffer), then one polynomial per distinct iteration
+// coefficient set (kSlotPoly0 + k for iteration k, the last one repeated).
 // TileRef::prob of a GEMM tile is problem * Layout::desc_per_problem + slot.
 enum DescSlot {
   kSlotGram0 = 0,
@@ -64,8 +75,33 @@ enum DescSlot {
   kSlotApply0 = 2,
   kSlotApply1 = 3,
   kSlotApplyLast = 4,
-  kSlotPoly0 = 5
+  kSlotT0 = 5,       // Gram-space: T = A Q[0] (first iteration of a segment, P_0 in Q[0])
+  kSlotT = 6,        // T = A B
+  kSlotA0 = 7,       // A = T Q[0]
+  kSlotA = 8,        // A = T B
+  kSlotQ0 = 9,       // Q[0] = B Q[1]
+  kSlotQ1 = 10,      // Q[1] = B Q[0]
+  // Z[1 - z] = Q[q] Z[z] at slot kSlotGApply0 + z + 2 q + 4 last (last: the
+  // final segment, which writes Z^T, i.e. U, for a transposed unit).
+  kSlotGApply0 = 11,
+  kSlotPoly0 = 19    // then poly_slots polynomials into B, poly_slots into Q[0]
 };
+
+// Gram-space iterations per segment: with longer runs the product chain's
+// bf16 rounding outgrows the iteration as printed (emulated, 1792 x 4096
+// after 48 momentum steps: 1.16% for one run of 5 against 0.75% as
+// printed), with runs of at most 3 it stays below it (0.63%).
+constexpr int kGramSegment = 3;
+
+// Gram-space iteration where it saves work (bf16 NS, the row-major apply,
+// K >= 2): on units with S >= kGramMinS and L >= 1.25 S.  A segment of n
+// iterations costs one Gram (S x S x L), 4n - 3 symmetric S x S x S
+// products and one apply (S x L x S) against n of each of the Gram, the
+// polynomial and the apply; with segments of 3 the measured kernel rates
+// break even at L = 1.26 S.  Below kGramMinS its bf16 error grows
+// (emulated, rank-128 gradients, one segment of 5: 1.0% at S = 512, 1.9%
+// at S = 128).
+constexpr int64_t kGramMinS = 1024;
 
 // One grouped GEMM launch of a step.
 struct GemmPhase {
@@ -106,7 +142,7 @@ struct Layout {
   std::vector<SegDesc> segs;
   int64_t total_elems = 0;
   int32_t poly_slots = 1;        // distinct polynomial descriptors per problem
-  int32_t desc_per_problem = 6;  // kSlotPoly0 + poly_slots
+  int32_t desc_per_problem = kSlotPoly0 + 2;  // kSlotPoly0 + 2 poly_slots
   Plan plan[2];  // [0] block plan, [1] full plan
 };
 
@@ -117,10 +153,13 @@ struct Layout {
 // the symmetric products; the register K loop where DMA is not allowed).
 // Returns "" on success, else a message (with *shape_error telling shape
 // vs. argument).
+// gram_mode: 0 = the Gram-space iteration where it saves work (above),
+// 1 = never, 2 = on every unit that allows it (bf16, row-major apply,
+// K >= 2) whatever its shape.
 std::string build_layout(const MatrixShape* mats, int32_t n_mats,
                          int ns_elem_bytes, int ns_steps, int poly_slots, int tile_policy,
                          int k_split, int apply_mode,
-                         Layout* out, bool* shape_error);
+                         Layout* out, bool* shape_error, int gram_mode = 0);
 
 // Tile shape the planner picks for one grouped product.
 int32_t choose_variant(const std::vector<Problem>& probs, GemmKind kind, int tile_policy,
@@ -135,7 +174,7 @@ int32_t choose_split(const std::vector<Problem>& probs, GemmKind kind, int32_t v
 std::vector<TileRef> xcd_order(const std::vector<TileRef>& logical);
 
 // Per-step flops of NS on one S x L unit for K iterations.
-double ns_unit_flops(int64_t S, int64_t L, int K);        // symmetric-aware
+double ns_unit_flops(int64_t S, int64_t L, int K, bool gram = false);  // symmetric-aware, as computed
 double ns_unit_dense_flops(int64_t S, int64_t L, int K);  // Sec. 2.2 model
 
 }  // namespace muonbp

@@ -46,6 +46,7 @@ std::string validate_opts(const muonbp_options& o) {
   if (o.apply_mode < 0 || o.apply_mode > 1) return "apply_mode out of range";
   if (o.check_finite != 0 && o.check_finite != 1) return "check_finite must be 0 or 1";
   if (o.device_memory_limit < 0) return "device_memory_limit must be >= 0";
+  if (o.gram_iteration < 0 || o.gram_iteration > 2) return "gram_iteration must be 0, 1 or 2";
   for (int i = 0; i < 3 * o.coeff_count; ++i)
     if (!std::isfinite(o.coeff_table[i])) return "coefficients must be finite";
   return "";
@@ -70,7 +71,8 @@ std::string check_mats(const muonbp_matrix* mats, int32_t n_mats, std::vector<Ma
 std::string layout_for(const std::vector<MatrixShape>& shapes, const muonbp_options& o, Layout* out,
                        bool* shape_error) {
   return build_layout(shapes.data(), int32_t(shapes.size()), int(dtype_size(o.ns_dtype)), o.ns_steps,
-                      poly_slots(o), o.tile_policy, o.k_split, o.apply_mode, out, shape_error);
+                      poly_slots(o), o.tile_policy, o.k_split, o.apply_mode, out, shape_error,
+                      o.gram_iteration);
 }
 
 void build_plan_host_tables(const Layout& lay, const muonbp_options& o, int full, void* ws_base,
@@ -137,21 +139,62 @@ void build_plan_host_tables(const Layout& lay, const muonbp_options& o, int full
     };
     for (int q = 0; q < 2; ++q) out->descs.push_back(apply_desc(q, false));
     out->descs.push_back(apply_desc((o.ns_steps + 1) & 1, true));  // iteration K - 1 reads Z_{(K-1) mod 2}
+    // Gram-space products (kSlotT0 .. kSlotGApply0 + 7; placeholders that
+    // no tile refers to on a unit that iterates as printed).  All but the
+    // applies are S x S x S products of symmetric matrices that commute
+    // (polynomials in the Gram matrix a segment starts from), so the result
+    // is symmetric and only its upper tiles are computed.
+    {
+      const int32_t ld = Sp;
+      auto sym_desc = [&](int64_t x, int64_t y, int64_t c) {
+        return GemmDesc{at(x), at(y), nullptr, at(c), at(c), S, S, S, ld, ld, 0, ld, ld, 1.f, 0.f, 0.f, 1};
+      };
+      if (!p.gram) {
+        const GemmDesc unused = out->descs.front();
+        for (int k = kSlotT0; k < kSlotPoly0; ++k) out->descs.push_back(unused);
+      } else {
+        const int64_t q0 = p.off_q[0], q1 = p.off_q[1], t = p.off_t;
+        out->descs.push_back(sym_desc(p.off_a, q0, t));       // kSlotT0
+        out->descs.push_back(sym_desc(p.off_a, p.off_b, t));  // kSlotT
+        out->descs.push_back(sym_desc(t, q0, p.off_a));       // kSlotA0
+        out->descs.push_back(sym_desc(t, p.off_b, p.off_a));  // kSlotA
+        out->descs.push_back(sym_desc(p.off_b, q1, q0));      // kSlotQ0
+        out->descs.push_back(sym_desc(p.off_b, q0, q1));      // kSlotQ1
+        // Z[1 - z] = Q[q] Z[z]; the final segment of a transposed unit writes
+        // Z^T[1 - z] instead (U in the matrix's orientation, where the update
+        // reads it).
+        for (int last = 0; last < 2; ++last)
+          for (int q = 0; q < 2; ++q)
+            for (int z = 0; z < 2; ++z) {
+              const bool t_only = last && p.trans;
+              out->descs.push_back(GemmDesc{at(p.off_q[q]), at(p.off_z[z]), nullptr,
+                                            t_only ? nullptr : at(p.off_z[1 - z]),
+                                            t_only ? at(p.off_zt[1 - z]) : nullptr, S, Lr, S, Sp, Lp, 0,
+                                            Lp, Sp, 1.f, 0.f, 0.f, 0});  // kSlotGApply0 + z + 2 q + 4 last
+            }
+      }
+    }
     // Polynomial of iteration k: B = c_k A A^T + b_k A + a_k I (A symmetric;
     // the a I term carries Algorithm 2's a X into the apply).
-    for (int k = 0; k < lay.poly_slots; ++k) {
-      float a, b, cc;
-      ns_coeffs(o, k, &a, &b, &cc);
-      out->descs.push_back(GemmDesc{at(p.off_a), at(p.off_a), at(p.off_a), at(p.off_b), at(p.off_b), S,
-                                    S, S, Sp, Sp, Sp, Sp, Sp, cc, b, a, 1});
-    }
+    // Then the same polynomials into Q[0] (a Gram-space segment's first;
+    // placeholders on a unit that iterates as printed).
+    for (int into_q = 0; into_q < 2; ++into_q)
+      for (int k = 0; k < lay.poly_slots; ++k) {
+        float a, b, cc;
+        ns_coeffs(o, k, &a, &b, &cc);
+        const int64_t dst = into_q && p.gram ? p.off_q[0] : p.off_b;
+        out->descs.push_back(GemmDesc{at(p.off_a), at(p.off_a), at(p.off_a), at(dst), at(dst), S, S, S, Sp,
+                                      Sp, Sp, Sp, Sp, cc, b, a, 1});
+      }
   }
   // Update table: U of every block after K iterations (buffer K mod 2).
   const int fin = o.ns_steps & 1;
   for (const Problem& p : plan.probs) {
     float s = 1.f;
     if (o.scale_mode == 1) s = o.rms_beta * std::sqrt(float(std::max(p.rows, p.cols)));
-    const int64_t base = p.trans ? p.off_zt[fin] : p.off_z[fin];
+    // A Gram-space unit's last segment writes Z[number of segments mod 2].
+    const int u = p.gram ? ((o.ns_steps + kGramSegment - 1) / kGramSegment) & 1 : fin;
+    const int64_t base = p.trans ? p.off_zt[u] : p.off_z[u];
     const int64_t ldu = p.trans ? p.Sp : p.Lp;
     for (int32_t b = p.first_block; b < p.first_block + p.n_blocks; ++b) {
       const BlockPlan& bp = lay.blocks[b];

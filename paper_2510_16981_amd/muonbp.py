@@ -45,7 +45,7 @@ class Options(ctypes.Structure):
                 ("k_split", ctypes.c_int32), ("coeff_count", ctypes.c_int32),
                 ("coeff_table", ctypes.c_float * (3 * 16)), ("stream_hint", ctypes.c_int32),
                 ("apply_mode", ctypes.c_int32), ("check_finite", ctypes.c_int32),
-                ("device_memory_limit", ctypes.c_int64)]
+                ("device_memory_limit", ctypes.c_int64), ("gram_iteration", ctypes.c_int32)]
 
 
 class PlanInfo(ctypes.Structure):
@@ -57,7 +57,8 @@ class PlanInfo(ctypes.Structure):
                 ("elementwise_bytes", ctypes.c_double),
                 ("workspace_bytes", ctypes.c_int64),
                 ("gemm_split", ctypes.c_int32 * 3), ("apply_nn", ctypes.c_int32),
-                ("static_scratch_bytes", ctypes.c_int64), ("device_bytes", ctypes.c_int64)]
+                ("static_scratch_bytes", ctypes.c_int64), ("device_bytes", ctypes.c_int64),
+                ("gram_units", ctypes.c_int64)]
 
 
 class AdamwOptions(ctypes.Structure):

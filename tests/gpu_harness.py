@@ -147,6 +147,7 @@ class Case:
     stream_hint: int = 0
     apply_mode: int = 0
     coeffs: Optional[Sequence[tuple]] = None  # per-iteration (a, b, c) table
+    gram_iteration: int = 0  # 0 = planner's choice, 1 = as printed, 2 = Gram-space wherever allowed
     period_schedule: Optional[Dict[int, int]] = None  # step -> new period (set before it)
     check_steps: Optional[Sequence[int]] = None  # None = every step
 
@@ -202,7 +203,7 @@ def run_case(case: Case, keep_updates: bool = False) -> Result:
                               param_dtype=DT[case.param], state_dtype=DT[case.state],
                               ns_dtype=DT[case.ns], tile_policy=case.tile_policy,
                               k_split=case.k_split, stream_hint=case.stream_hint,
-                              apply_mode=case.apply_mode, **extra)
+                              apply_mode=case.apply_mode, gram_iteration=case.gram_iteration, **extra)
     opt = mb.MuonBP(case.mats, case.period, case.lr_block, case.lr_full, case.momentum,
                     case.weight_decay, options=opts)
     orc = O.MuonBPOracle([O.MatrixSpec(*m) for m in case.mats],

@@ -176,25 +176,47 @@ def test_describe_plan_counts_and_flops(lib, name):
         gram = poly = apply = 0
         (gr_, pr_, ar_), (gc_, pc_, ac_) = info.gemm_tile_rows, info.gemm_tile_cols
         assert gr_ == gc_ and pr_ == pc_  # symmetric products use square tiles
+        n_gram = 0
         for p, q in units:
             S, L = min(p, q), max(p, q)
-            sym += 5 * (S * (S + 1) * L + S * S * (S + 1) + 2 * S * S * L)
+            # Gram-space iteration (bf16, row-major apply, K = 5): S >= 1024
+            # and L >= 1.25 S.  Segments of 3 and 2 iterations, each one
+            # Gram, 4n - 3 symmetric S x S x S products and one apply,
+            # instead of K of each of three.
+            g = bool(info.apply_nn) and S >= 1024 and 4 * L >= 5 * S
+            n_gram += g
+            zz, ss, ap = S * (S + 1) * L, S * S * (S + 1), 2 * S * S * L
+            sym += (2 * zz + (9 + 5) * ss + 2 * ap) if g else 5 * (zz + ss + ap)
             tg, tp = -(-S // gr_), -(-S // pr_)
             gram += tg * (tg + 1) // 2
             poly += tp * (tp + 1) // 2
             apply += -(-S // ar_) * -(-L // ac_)
+        assert info.gram_units == n_gram
         assert abs(info.ns_flops - sym) <= 1e-9 * sym
         assert info.gemm_tiles[0] == gram and info.gemm_tiles[1] == poly
         assert info.gemm_tiles[2] == apply
         assert info.workspace_bytes > 0
+        # Launches per iteration: Gram, poly, apply for units as printed; with
+        # Gram-space units also the Q / T and the A products (none in the
+        # last iteration), and no Gram after the first iteration when every
+        # unit is a Gram-space one.
+        # K = 5: 3 K as printed; with both kinds of unit 5, 5, 4 (segment of
+        # 3: no A update in its last iteration) then 5, 4; with Gram-space
+        # units only 4, 3, 3, 4, 3 (a Gram only where a segment starts).
+        if n_gram == 0:
+            assert info.gemm_launches == 15
+        else:
+            assert info.gemm_launches == (17 if n_gram == len(units) else 23)
         # The apply reads Z row-major on every bf16 workload: per unit two Z
-        # buffers (either layout) plus A and B, nothing else.
+        # buffers (either layout) plus A and B, and Q[2] and T on a Gram-space
+        # unit.
         if info.apply_nn:
             ws = 0
             for p, q in units:
                 S, L = min(p, q), max(p, q)
                 Sp, Lp = -(-S // 8) * 8, -(-L // 8) * 8
-                for n_el in (max(S * Lp, L * Sp),) * 2 + (S * Sp,) * 2:
+                g = S >= 1024 and 4 * L >= 5 * S
+                for n_el in (max(S * Lp, L * Sp),) * 2 + (S * Sp,) * (5 if g else 2):
                     ws = -(-(ws + n_el) // 128) * 128  # 256-byte aligned bf16 buffers
             assert info.workspace_bytes == 2 * ws
 
@@ -207,7 +229,13 @@ def test_describe_plan_qkv_numbers(lib):
     assert abs(blk.ns_dense_flops / 1e12 - 0.2295) < 5e-4
     assert abs(full.ns_dense_flops / 1e12 - 0.6013) < 5e-4
     assert abs(blk.ns_flops / 1e12 - 0.1632) < 5e-4
-    assert abs(full.ns_flops / 1e12 - 0.4296) < 5e-4
+    # The whole matrix (S = 2048, L = 3 S) runs the Gram-space iteration in
+    # segments of 3 and 2: 2 S(S+1)L + 14 S^2(S+1) + 4 S^2 L; as printed,
+    # 5 (S(S+1)L + S^2(S+1) + 2 S^2 L).
+    assert full.gram_units == 1 and blk.gram_units == 0
+    assert abs(full.ns_flops / 1e12 - 0.2750) < 5e-4
+    printed = mb.describe_plan(mats, True, mb.options_default(gram_iteration=1))
+    assert printed.gram_units == 0 and abs(printed.ns_flops / 1e12 - 0.4296) < 5e-4
 
 
 @pytest.mark.parametrize("policy,shape,square", [
@@ -247,12 +275,35 @@ def test_describe_plan_rejects_bad_grid(lib):
 
 
 def test_three_launches_per_iteration(lib):
+    """Three grouped launches per iteration as printed (gram_iteration = 1);
+    the Gram-space schedule of the other modes is counted in
+    test_describe_plan_counts_and_flops."""
+    opt = mb.options_default(gram_iteration=1)
     for name in ("qkv-2048x6144-bf16", "llama-32L-d4096-bf16"):
         for full in (False, True):
-            info = mb.describe_plan(W.workload_matrices(name), full)
+            info = mb.describe_plan(W.workload_matrices(name), full, opt)
             assert info.gemm_launches == 3 * 5
     info = mb.describe_plan([(64, 64, 1, 1)], False, mb.options_default(ns_steps=0))
     assert info.gemm_launches == 0
+
+
+def test_gram_iteration_modes(lib):
+    """Which units run the Gram-space iteration: mode 0 from S >= 1024 and
+    L >= 1.25 S, mode 1 none, mode 2 every unit that allows it; never with
+    K < 2, fp32 NS or the transposed-copy apply; an out-of-range mode is
+    refused."""
+    mats = [(1024, 1280, 1, 1), (1024, 1272, 1, 1), (1016, 4096, 1, 1), (4096, 1024, 1, 1), (296, 704, 1, 1)]
+    info = lambda **kw: mb.describe_plan(mats, True, mb.options_default(**kw))
+    assert info().gram_units == 2  # 1024 x 1280 and 4096 x 1024 (transposed); 1272 < 1.25 S
+    assert info(gram_iteration=1).gram_units == 0
+    assert info(gram_iteration=2).gram_units == 5
+    assert info(gram_iteration=2, ns_steps=1).gram_units == 0
+    assert info(gram_iteration=2, ns_dtype=mb.F32).gram_units == 0
+    assert info(gram_iteration=2, apply_mode=1).gram_units == 0
+    # Three more S x Sp bf16 buffers (Q[2], T) per Gram-space unit.
+    assert info().workspace_bytes - info(gram_iteration=1).workspace_bytes == 2 * 3 * (1024 * 1024 + 1024 * 1024)
+    with pytest.raises(mb.MuonBPError):
+        info(gram_iteration=3)
 
 
 def test_k_split_applies_to_dma_pipeline_only(lib):
