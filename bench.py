@@ -59,7 +59,7 @@ def gram_space_unit(S, L, K, mode, apply_nn):
     (the planner's rule for bf16 NS; mode is the gram_iteration option)."""
     if mode == 1 or not apply_nn or K < 2:
         return False
-    return mode == 2 or (S >= 1024 and 4 * L >= 5 * S)
+    return mode == 2 or (S >= 256 and 4 * L >= 5 * S)
 
 
 GRAM_SEGMENT = 3  # Gram-space iterations per segment (the library's kGramSegment)
@@ -321,9 +321,39 @@ def mfma_probe():
     print(json.dumps({"mfma_probe_flops": 2 * n ** 3, "reps": 3}), flush=True)
 
 
-def _pmc_dispatches(run_dir):
+def launch_products(mats, full, K, mode=0, apply_nn=True):
+    """The library's grouped NS GEMM launches of one step, in order, named
+    after their products: per iteration the Gram (units as printed; a
+    Gram-space unit where its segment starts), the polynomial, the
+    Gram-space Q / T products and the A update (Gram-space units), the apply
+    (units as printed; a Gram-space unit at its segment's end).  Empty
+    launches are skipped, as the library does."""
+    flags = []
+    for r, c, gr, gc in mats:
+        units = [(r, c)] if full else [(r // gr, c // gc)] * (gr * gc)
+        flags += [gram_space_unit(min(p, q), max(p, q), K, mode, apply_nn) for p, q in units]
+    has_std, has_g = not all(flags), any(flags)
+    out = []
+    for it in range(K):
+        j = it % GRAM_SEGMENT
+        n = min(GRAM_SEGMENT, K - it + j)
+        if has_std or (has_g and j == 0):
+            out.append("gram")
+        out.append("poly")
+        if has_g and (j > 0 or j < n - 1):
+            out.append("gram-space")
+        if has_g and j < n - 1:
+            out.append("gram-space")
+        if has_std or (has_g and j == n - 1):
+            out.append("apply")
+    return out
+
+
+def _pmc_dispatches(run_dir, products=None):
     """Dispatches of a rocprofv3 --pmc csv run: {dispatch id: {"name", "ns"
-    (duration), counter: value, ...}}."""
+    (duration), counter: value, ...}}.  products: the NS GEMM launches of
+    one step in order (launch_products); by default Gram, polynomial and
+    apply per iteration."""
     import csv
     import glob
     out = {}
@@ -338,13 +368,14 @@ def _pmc_dispatches(run_dir):
         raise SystemExit(f"no counter_collection.csv under {run_dir}")
     rows = [out[k] for k in sorted(out)]
     # Name each NS GEMM dispatch after its product: a step launches pack,
-    # then (Gram, polynomial, apply) once per iteration, then the update.
+    # then its NS GEMM launches in a fixed order, then the update.
+    seq = products or ("gram", "poly", "apply")
     i = 0
     for r in rows:
         if "k_pack" in r["name"]:
             i = 0
         elif "k_ns_gemm" in r["name"]:
-            r["product"] = ("gram", "poly", "apply")[i % 3]
+            r["product"] = seq[i % len(seq)]
             i += 1
     return rows
 
@@ -429,6 +460,8 @@ def ingest_counters(workload, dirs, command):
     against the probe's known flops) and TFLOP/s; MFMA utilisation (busy
     MFMA cycles over active cycles times SIMDs, rocprofv3's MfmaUtil).
     Durations are those of the counter runs' own dispatches."""
+    from paper_2510_16981_amd import muonbp as mb
+    from paper_2510_16981_amd import workload as W
     d = dict(zip(INGEST_DIRS, dirs))
     copy_kib = _json_line(os.path.join(d["copy_fetch"], "copy_probe.json"),
                           "copy_probe_bytes")["copy_probe_bytes"] / 1024.0
@@ -456,9 +489,14 @@ def ingest_counters(workload, dirs, command):
         n_el = bj["config"]["params"]
         kstats = bj[kind]
         alg_flops_launch = kstats["ns_flops_per_step"] / kstats["ns_gemm_launches_per_step"]
-        fetch = _by_label(_pmc_dispatches(d[f"{kind}_fetch"]), "FETCH_SIZE")
-        write = _by_label(_pmc_dispatches(d[f"{kind}_write"]), "WRITE_SIZE")
-        mrows = _pmc_dispatches(d[f"{kind}_mfma"])
+        mats = W.workload_matrices(workload)
+        info = mb.describe_plan(mats, kind == "full", mb.options_default(ns_steps=K_NS))
+        prods = launch_products(mats, kind == "full", K_NS, 0, bool(info.apply_nn))
+        if len(prods) != info.gemm_launches:
+            raise SystemExit("launch order model out of step with the planner")
+        fetch = _by_label(_pmc_dispatches(d[f"{kind}_fetch"], prods), "FETCH_SIZE")
+        write = _by_label(_pmc_dispatches(d[f"{kind}_write"], prods), "WRITE_SIZE")
+        mrows = _pmc_dispatches(d[f"{kind}_mfma"], prods)
         mops = _by_label(mrows, "SQ_INSTS_VALU_MFMA_MOPS_BF16")
         util = _by_label(mrows, "MfmaUtil")
         gui = _by_label(mrows, "GRBM_GUI_ACTIVE")

@@ -135,24 +135,26 @@ typedef struct {
                                muonbp_plan_info.device_bytes is the size of
                                those three. */
   int32_t gram_iteration;   /* how the K NS iterations of a unit run (the
-                               result is Alg. 2's, up to rounding).  Every
-                               polynomial of Alg. 2 is a polynomial in
-                               A_0 = Z_0 Z_0^T, so the iterations can run on
-                               S x S matrices only: P_k = a_k I + b_k A_k +
-                               c_k A_k^2, A_{k+1} = A_k P_k^2, Q_k = P_k
-                               Q_{k-1}, and one apply U = Q_{K-1} Z_0 ends
-                               them (4K - 3 symmetric S x S x S products, one
-                               S x S x L Gram and one S x L x S apply, against
-                               K of each of the three as printed).
+                               result is Alg. 2's, up to rounding).  Each
+                               iteration multiplies Z by a polynomial of its
+                               Gram matrix, so n of them can run on S x S
+                               matrices only: from A_0 = Z Z^T, P_j = a I +
+                               b A_j + c A_j^2, A_{j+1} = A_j P_j^2, Q_j =
+                               P_j Q_{j-1}, then Z <- Q_{n-1} Z (4n - 3
+                               symmetric S x S x S products, one S x S x L
+                               Gram and one S x L x S apply, against n of
+                               each of the three as printed).  The K
+                               iterations then run in segments of at most 3,
+                               each from a fresh Gram of the current Z.
                                0 = that Gram-space iteration on the units
                                where it saves time (bf16 NS, the row-major
-                               apply, K >= 2, S >= 1024 and L >= 1.25 S;
-                               below S = 1024 its bf16 rounding error grows),
-                               as printed elsewhere (default); 1 = as
-                               printed everywhere; 2 = the Gram-space
-                               iteration on every unit that allows it (bf16,
-                               row-major apply, K >= 2), whatever its shape.
-                               It keeps two more S x S buffers per unit. */
+                               apply, K >= 2, S >= 256 and L >= 1.25 S), as
+                               printed elsewhere (default); 1 = as printed
+                               everywhere; 2 = the Gram-space iteration on
+                               every unit that allows it (bf16, row-major
+                               apply, K >= 2), whatever its shape.  A
+                               Gram-space unit keeps three more S x S
+                               buffers. */
 } muonbp_options;
 
 /* Fill *opt with the defaults above.  NULL is ignored. */

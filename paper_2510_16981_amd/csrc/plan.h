@@ -98,10 +98,12 @@ constexpr int kGramSegment = 3;
 // iterations costs one Gram (S x S x L), 4n - 3 symmetric S x S x S
 // products and one apply (S x L x S) against n of each of the Gram, the
 // polynomial and the apply; with segments of 3 the measured kernel rates
-// break even at L = 1.26 S.  Below kGramMinS its bf16 error grows
-// (emulated, rank-128 gradients, one segment of 5: 1.0% at S = 512, 1.9%
-// at S = 128).
-constexpr int64_t kGramMinS = 1024;
+// break even at L = 1.26 S.  In segments of at most 3 its bf16 error is at
+// or below the printed iteration's from S = 128 to 4096 (emulated, rank-128
+// gradients, 48 momentum steps: 0.91 / 0.80 / 0.63% at S = 128 / 512 /
+// 1792 against 1.06 / 0.95 / 0.75%); the floor keeps the smallest units,
+// whose products are mostly tile padding, as printed.
+constexpr int64_t kGramMinS = 256;
 
 // One grouped GEMM launch of a step.
 struct GemmPhase {

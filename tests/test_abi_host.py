@@ -179,11 +179,11 @@ def test_describe_plan_counts_and_flops(lib, name):
         n_gram = 0
         for p, q in units:
             S, L = min(p, q), max(p, q)
-            # Gram-space iteration (bf16, row-major apply, K = 5): S >= 1024
+            # Gram-space iteration (bf16, row-major apply, K = 5): S >= 256
             # and L >= 1.25 S.  Segments of 3 and 2 iterations, each one
             # Gram, 4n - 3 symmetric S x S x S products and one apply,
             # instead of K of each of three.
-            g = bool(info.apply_nn) and S >= 1024 and 4 * L >= 5 * S
+            g = bool(info.apply_nn) and S >= 256 and 4 * L >= 5 * S
             n_gram += g
             zz, ss, ap = S * (S + 1) * L, S * S * (S + 1), 2 * S * S * L
             sym += (2 * zz + (9 + 5) * ss + 2 * ap) if g else 5 * (zz + ss + ap)
@@ -215,7 +215,7 @@ def test_describe_plan_counts_and_flops(lib, name):
             for p, q in units:
                 S, L = min(p, q), max(p, q)
                 Sp, Lp = -(-S // 8) * 8, -(-L // 8) * 8
-                g = S >= 1024 and 4 * L >= 5 * S
+                g = S >= 256 and 4 * L >= 5 * S
                 for n_el in (max(S * Lp, L * Sp),) * 2 + (S * Sp,) * (5 if g else 2):
                     ws = -(-(ws + n_el) // 128) * 128  # 256-byte aligned bf16 buffers
             assert info.workspace_bytes == 2 * ws
@@ -228,14 +228,17 @@ def test_describe_plan_qkv_numbers(lib):
     full = mb.describe_plan(mats, True)
     assert abs(blk.ns_dense_flops / 1e12 - 0.2295) < 5e-4
     assert abs(full.ns_dense_flops / 1e12 - 0.6013) < 5e-4
-    assert abs(blk.ns_flops / 1e12 - 0.1632) < 5e-4
-    # The whole matrix (S = 2048, L = 3 S) runs the Gram-space iteration in
-    # segments of 3 and 2: 2 S(S+1)L + 14 S^2(S+1) + 4 S^2 L; as printed,
-    # 5 (S(S+1)L + S^2(S+1) + 2 S^2 L).
-    assert full.gram_units == 1 and blk.gram_units == 0
+    # Every unit (the shards: S = 768, L = 2.7 S; the whole matrix: S = 2048,
+    # L = 3 S) runs the Gram-space iteration in segments of 3 and 2:
+    # 2 S(S+1)L + 14 S^2(S+1) + 4 S^2 L per unit; as printed, 5 (S(S+1)L +
+    # S^2(S+1) + 2 S^2 L).
+    assert full.gram_units == 1 and blk.gram_units == 8
+    assert abs(blk.ns_flops / 1e12 - 0.1088) < 5e-4
     assert abs(full.ns_flops / 1e12 - 0.2750) < 5e-4
-    printed = mb.describe_plan(mats, True, mb.options_default(gram_iteration=1))
-    assert printed.gram_units == 0 and abs(printed.ns_flops / 1e12 - 0.4296) < 5e-4
+    opt = mb.options_default(gram_iteration=1)
+    pb, pf = mb.describe_plan(mats, False, opt), mb.describe_plan(mats, True, opt)
+    assert pb.gram_units == pf.gram_units == 0
+    assert abs(pb.ns_flops / 1e12 - 0.1632) < 5e-4 and abs(pf.ns_flops / 1e12 - 0.4296) < 5e-4
 
 
 @pytest.mark.parametrize("policy,shape,square", [
@@ -288,20 +291,24 @@ def test_three_launches_per_iteration(lib):
 
 
 def test_gram_iteration_modes(lib):
-    """Which units run the Gram-space iteration: mode 0 from S >= 1024 and
+    """Which units run the Gram-space iteration: mode 0 from S >= 256 and
     L >= 1.25 S, mode 1 none, mode 2 every unit that allows it; never with
     K < 2, fp32 NS or the transposed-copy apply; an out-of-range mode is
     refused."""
-    mats = [(1024, 1280, 1, 1), (1024, 1272, 1, 1), (1016, 4096, 1, 1), (4096, 1024, 1, 1), (296, 704, 1, 1)]
+    mats = [(1024, 1280, 1, 1), (1024, 1272, 1, 1), (1016, 4096, 1, 1), (4096, 1024, 1, 1), (296, 704, 1, 1),
+            (200, 800, 1, 1)]
+    gram = [0, 2, 3, 4]  # 1272 < 1.25 S; 200 < 256
     info = lambda **kw: mb.describe_plan(mats, True, mb.options_default(**kw))
-    assert info().gram_units == 2  # 1024 x 1280 and 4096 x 1024 (transposed); 1272 < 1.25 S
+    assert info().gram_units == len(gram)
     assert info(gram_iteration=1).gram_units == 0
-    assert info(gram_iteration=2).gram_units == 5
+    assert info(gram_iteration=2).gram_units == 6
     assert info(gram_iteration=2, ns_steps=1).gram_units == 0
     assert info(gram_iteration=2, ns_dtype=mb.F32).gram_units == 0
     assert info(gram_iteration=2, apply_mode=1).gram_units == 0
-    # Three more S x Sp bf16 buffers (Q[2], T) per Gram-space unit.
-    assert info().workspace_bytes - info(gram_iteration=1).workspace_bytes == 2 * 3 * (1024 * 1024 + 1024 * 1024)
+    # Three more S x Sp bf16 buffers (Q[2], T) per Gram-space unit, each
+    # rounded up to 256 bytes.
+    extra = sum(-(-min(mats[i][:2]) ** 2 // 128) * 128 for i in gram)
+    assert info().workspace_bytes - info(gram_iteration=1).workspace_bytes == 2 * 3 * extra
     with pytest.raises(mb.MuonBPError):
         info(gram_iteration=3)
 

@@ -4,7 +4,7 @@ Every polynomial of Alg. 2 (App. B) is a polynomial in the Gram matrix of
 the iterate it starts from, so the library may run up to three iterations
 at a time on S x S matrices only (P_j, then Q_j = P_j Q_{j-1} and A_{j+1} =
 (A_j P_j) P_j) and end each such segment with one apply Z <- Q Z: the same
-U up to rounding.  The planner does so for bf16 units with S >= 1024 and
+U up to rounding.  The planner does so for bf16 units with S >= 256 and
 L >= 1.25 S (option gram_iteration = 0); mode 2 forces it on every unit that
 allows it, mode 1 turns it off.  The cases cover transposed and
 untransposed units, units that iterate as printed in the same launches,
@@ -45,10 +45,10 @@ def _check(case, want_gram_units):
     assert w["m_ulp"] <= 1.0 and w["x_ulp"] <= 1.0, w
 
 
-# 1024 x 1280 (S = 1024), its transpose, a 512 x 2048 unit that iterates as
-# printed (S < 1024), and 2048 x 2560 in two column blocks (blocks 2048 x
+# 1024 x 1280 (S = 1024), its transpose, a 768 x 896 unit that iterates as
+# printed (L < 1.25 S), and 2048 x 2560 in two column blocks (blocks 2048 x
 # 1280 transposed: S = 1280, L = 2048; the whole matrix: S = 2048, L = 1.25 S).
-MIXED = [(1024, 1280, 1, 1), (1280, 1024, 1, 1), (512, 2048, 1, 1), (2048, 2560, 1, 2)]
+MIXED = [(1024, 1280, 1, 1), (1280, 1024, 1, 1), (768, 896, 1, 1), (2048, 2560, 1, 2)]
 
 
 def test_mixed_units_block_and_full():
