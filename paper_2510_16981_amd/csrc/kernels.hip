@@ -1248,66 +1248,95 @@ __global__ __launch_bounds__(64 * WM * WN) void k_ns_gemm_dmap(const GemmDesc* _
                               acc[i][j]);
   };
 
-  // Prologue: fill the ring, publish slice kb, read its first K step.
-#pragma unroll
-  for (int s = 0; s < NS; ++s)
-#pragma unroll
-    for (int jj = 0; jj < LPW; ++jj) copy(kb + s, jj);
-  __builtin_amdgcn_s_waitcnt(vmcnt_imm((NS - 1) * LPW));
-  barrier_no_fence();
+  // Idle waves run the K loop's copies, waits and barriers but no MFMAs or
+  // fragment reads, and store nothing.  In a diagonal tile of a symmetric
+  // product those are the waves whose sub-tile lies strictly below the
+  // diagonal, and the waves whose sub-tile lies strictly above it write
+  // their block's transpose there (Ct = C): with 2 x 4 or 2 x 2 waves on a
+  // square tile the blocks below are exactly the transposes of the blocks
+  // above.  (Not where the epilogue takes the general path: rows of C not
+  // whole 8-element chunks.)
+  constexpr bool kDiagSkip = BM == BN && WM == 2 && (WN == 4 || WN == 2);
+  const bool dtile = kDiagSkip && ti == tj && d.sym && d.Ct == d.C && d.M % 8 == 0 && d.N % 8 == 0;
+  const int lr0 = wm * 32 * TM, lc0 = wn * 32 * TN;  // the wave's sub-tile inside the tile
+  const bool below = dtile && lr0 >= lc0 + 32 * TN;
+  const bool above = dtile && lc0 >= lr0 + 32 * TM;
+  // So is a wave whose whole sub-tile lies past M or N (a unit smaller than
+  // the tile), whose rows or columns of C are never stored.
+  const bool idle = below || m0 + lr0 >= d.M || n0 + lc0 >= d.N;
+
   u32x4_t f0[NF], f1[NF];
   u32x2_t y0l[YH], y0h[YH], y1l[YH], y1h[YH];
+  auto kloop = [&](auto math) {
+    constexpr bool MATH = decltype(math)::value;
+    // Prologue: fill the ring, publish slice kb, read its first K step.
 #pragma unroll
-  for (int o = 0; o < NR; ++o) read_op(f0, y0l, y0h, kb, 0, o);
-  frag_wait(f0, y0l, y0h);
-
-  for (int kt = kb; kt < ke; ++kt) {
-    // 8 waves: waves w and w + 4 share a SIMD.  Their issue priority swaps
-    // every slice, so that neither falls behind the other on every slice
-    // and holds up the barrier (measured: Gram 2%, step 0.7-0.9% faster
-    // than equal priorities; swapping every K step was 2% slower).
-    if constexpr (W == 8) {
-      if (((kt + (wave >> 2)) & 1) != 0)
-        __builtin_amdgcn_s_setprio(1);
-      else
-        __builtin_amdgcn_s_setprio(0);
-    }
-    // Step 0 of slice kt, with the reads of its step 1.
+    for (int s = 0; s < NS; ++s)
 #pragma unroll
-    for (int q = 0; q < NM; ++q) {
-      mfma(f0, q);
-#pragma unroll
-      for (int o = q * RPM; o < (q + 1) * RPM && o < NR; ++o) read_op(f1, y1l, y1h, kt, 1, o);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    frag_wait(f1, y1l, y1h);
-    // Step 1, first part.
-#pragma unroll
-    for (int q = 0; q < H; ++q) {
-      mfma(f1, q);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    // Slice kt + 1 has landed for this wave (two later slices may still be
-    // in flight); after the barrier it has landed for every wave, and no
-    // wave reads slice kt any more, so its slot takes slice kt + NS.
-    __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * LPW));
+      for (int jj = 0; jj < LPW; ++jj) copy(kb + s, jj);
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm((NS - 1) * LPW));
     barrier_no_fence();
-    // Step 1, rest, with the reads of slice kt + 1 and the refill copies.
-    constexpr int OPS = LPW + NR;
+    if constexpr (MATH)
 #pragma unroll
-    for (int q = H; q < NM; ++q) {
-      mfma(f1, q);
-      constexpr int R = NM - H;
-      const int lo = (q - H) * OPS / R, hi = (q - H + 1) * OPS / R;
-#pragma unroll
-      for (int o = lo; o < hi; ++o) {
-        if (o < NR) read_op(f0, y0l, y0h, kt + 1, 0, o);
-        else copy(kt + NS, o - NR);
-      }
-      __builtin_amdgcn_sched_barrier(0);
-    }
+      for (int o = 0; o < NR; ++o) read_op(f0, y0l, y0h, kb, 0, o);
     frag_wait(f0, y0l, y0h);
-  }
+
+    for (int kt = kb; kt < ke; ++kt) {
+      // 8 waves: waves w and w + 4 share a SIMD.  Their issue priority swaps
+      // every slice, so that neither falls behind the other on every slice
+      // and holds up the barrier (measured: Gram 2%, step 0.7-0.9% faster
+      // than equal priorities; swapping every K step was 2% slower).
+      if constexpr (W == 8) {
+        if (((kt + (wave >> 2)) & 1) != 0)
+          __builtin_amdgcn_s_setprio(1);
+        else
+          __builtin_amdgcn_s_setprio(0);
+      }
+      // Step 0 of slice kt, with the reads of its step 1.
+#pragma unroll
+      for (int q = 0; q < NM; ++q) {
+        if constexpr (MATH) {
+          mfma(f0, q);
+#pragma unroll
+          for (int o = q * RPM; o < (q + 1) * RPM && o < NR; ++o) read_op(f1, y1l, y1h, kt, 1, o);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      frag_wait(f1, y1l, y1h);
+      // Step 1, first part.
+#pragma unroll
+      for (int q = 0; q < H; ++q) {
+        if constexpr (MATH) mfma(f1, q);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      // Slice kt + 1 has landed for this wave (two later slices may still be
+      // in flight); after the barrier it has landed for every wave, and no
+      // wave reads slice kt any more, so its slot takes slice kt + NS.
+      __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * LPW));
+      barrier_no_fence();
+      // Step 1, rest, with the reads of slice kt + 1 and the refill copies.
+      constexpr int OPS = LPW + NR;
+#pragma unroll
+      for (int q = H; q < NM; ++q) {
+        if constexpr (MATH) mfma(f1, q);
+        constexpr int R = NM - H;
+        const int lo = (q - H) * OPS / R, hi = (q - H + 1) * OPS / R;
+#pragma unroll
+        for (int o = lo; o < hi; ++o) {
+          if (o < NR) {
+            if constexpr (MATH) read_op(f0, y0l, y0h, kt + 1, 0, o);
+          } else
+            copy(kt + NS, o - NR);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      frag_wait(f0, y0l, y0h);
+    }
+  };
+  if (idle)
+    kloop(std::false_type{});
+  else
+    kloop(std::true_type{});
   // Zero-filled copies past the share may still be in flight: let them land
   // before the epilogue reuses the ring.
   __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
@@ -1346,8 +1375,9 @@ __global__ __launch_bounds__(64 * WM * WN) void k_ns_gemm_dmap(const GemmDesc* _
     if (tid == 0) __hip_atomic_store(kcount + t.slot, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
   __syncthreads();
+  if (idle) return;
   dma_epilogue<TM, TN, WM, WN>(acc, reinterpret_cast<float*>(lds) + wave * 32 * (32 * TN + 1), d, m0, n0,
-                              ti == tj && d.sym);
+                              ti == tj && d.sym && !above);
 }
 
 // ---------------------------------------------------------------- update
