@@ -422,7 +422,8 @@ INGEST_DIRS = ("copy_fetch", "copy_write", "mfma_probe", "block_fetch", "block_w
 MFMA_COUNTERS = ("SQ_INSTS_VALU_MFMA_MOPS_BF16", "MfmaUtil", "GRBM_GUI_ACTIVE")
 # Bytes per element the elementwise kernels must move (bf16 storage):
 # momentum reads M and G and writes M; pack reads M and writes Z (the apply
-# reads Z row-major, so no Z^T); update reads X and U and writes X.
+# reads Z row-major, so no Z^T; only the units not read in place, the plan's
+# pack_elements); update reads X and U and writes X.
 ELEMENTWISE_BYTES = {"k_momentum": 6, "k_pack": 4, "k_update": 6}
 
 
@@ -507,7 +508,8 @@ def ingest_counters(workload, dirs, command):
             us = f["us"] if f else mops[lab]["us"]
             flops = mops[lab]["value"] * mops_unit if lab in mops else None
             base = lab.split("<")[0]
-            alg = (n_el * ELEMENTWISE_BYTES[base]) if base in ELEMENTWISE_BYTES else None
+            n_moved = info.pack_elements if base == "k_pack" else n_el
+            alg = (n_moved * ELEMENTWISE_BYTES[base]) if base in ELEMENTWISE_BYTES else None
             rows.append({
                 "kernel": lab, "dispatches": f["n"] if f else mops[lab]["n"], "us": us,
                 "hbm_bytes": byt, "hbm_gbs": byt / (us * 1e3) if byt else None,

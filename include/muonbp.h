@@ -190,7 +190,9 @@ muonbp_status muonbp_create(const muonbp_matrix* mats, int32_t n_mats,
  *  grads   host array of n_mats device pointers (param_dtype), read only.
  *  step    t >= 0.  Full step iff period > 0 and step % period == 0.
  * Enqueues: momentum (+ per-segment sum of squares), per-unit scale,
- * operand pack, K x (Gram, polynomial, apply) grouped MFMA launches, update.
+ * operand pack (units not read in place, see
+ * muonbp_plan_info.pack_elements), K x (Gram, polynomial, apply) grouped
+ * MFMA launches, update.
  * The step may be captured into a HIP graph on the context's stream when
  * profiling is off and the pointers equal those of the step before (their
  * device table is then not re-uploaded); a replay repeats the captured step
@@ -258,6 +260,14 @@ typedef struct {
                               context for these matrices (both plans)       */
   int64_t gram_units;      /* units that run the Gram-space iteration (see
                               muonbp_options.gram_iteration)                */
+  int64_t pack_elements;   /* elements the pack copies into the NS workspace
+                              per step (4 bytes each in bf16).  An
+                              untransposed unit whose NS input is the bf16
+                              momentum itself (bf16 state and NS, no
+                              Nesterov, K >= 1) is not packed: its first Gram
+                              and apply read the momentum in place with the
+                              Frobenius scale of Alg. 2 applied to their
+                              sums                                          */
 } muonbp_plan_info;
 
 /* Plan description for a set of matrices without creating a context

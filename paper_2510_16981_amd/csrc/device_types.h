@@ -56,6 +56,9 @@ struct PackDesc {
 // D must be symmetric (the transposed tile reuses D's tile).
 // sym: the product is symmetric; its tile list holds upper tiles only and
 // the mirror write (Ct = C) is skipped on diagonal tiles.
+// scale: when set, alpha is multiplied by scale[0] (by scale[0]^2 with
+// scale_sq) -- Alg. 2's Frobenius normalisation folded into the first Gram
+// and apply of a unit that reads its NS input (the momentum) in place.
 struct GemmDesc {
   const void* X;
   const void* Y;
@@ -66,6 +69,8 @@ struct GemmDesc {
   int32_t ldx, ldy, ldd, ldc, ldct;
   float alpha, beta, gamma;
   int32_t sym;
+  const float* scale;
+  int32_t scale_sq;
 };
 
 // Workgroup tile shapes of the NS GEMM (rows x columns of C per workgroup):

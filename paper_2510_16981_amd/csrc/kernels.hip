@@ -585,6 +585,15 @@ __device__ __forceinline__ u32x4_t pack_bf16x8(const float f[8]) {
   return u.v;
 }
 
+// alpha of a product, with the unit's Frobenius scale when the descriptor
+// carries one (a scalar load; read at the start of a tile, so that its
+// latency is hidden by the K loop).
+__device__ __forceinline__ float desc_alpha(const GemmDesc& d) {
+  if (d.scale == nullptr) return d.alpha;
+  const float s = d.scale[0];
+  return d.alpha * (d.scale_sq ? s * s : s);
+}
+
 // Epilogue of the LDS-DMA kernel (bf16 C and Ct): the arithmetic of
 // gemm_epilogue in the same order (alpha acc, then + beta D, then + gamma
 // on the diagonal, one rounding to bf16), with the per-chunk work cut
@@ -597,7 +606,7 @@ __device__ __forceinline__ u32x4_t pack_bf16x8(const float f[8]) {
 // accesses in order).  Other tiles take gemm_epilogue.
 template <int TM, int TN, int WM, int WN>
 __device__ __forceinline__ void dma_epilogue(f32x16_t (&acc)[TM][TN], float* st, const GemmDesc& d, int m0,
-                                             int n0, bool diag) {
+                                             int n0, bool diag, float alpha) {
   constexpr int ES = 2;
   constexpr int P = 32 * TN + 1;
   constexpr int NCH = 4 * TN;         // 8-element chunks per staged row
@@ -607,7 +616,7 @@ __device__ __forceinline__ void dma_epilogue(f32x16_t (&acc)[TM][TN], float* st,
   const int wr0 = m0 + wm * 32 * TM, wc0 = n0 + wn * 32 * TN;
   const bool mirror = d.Ct != nullptr && !diag;
   const bool has_d = d.D != nullptr;
-  const float alpha = d.alpha, beta = d.beta, gamma = d.gamma;
+  const float beta = d.beta, gamma = d.gamma;
   if (d.N % 8 != 0 || (mirror && d.M % 8 != 0)) {
     gemm_epilogue<bf16, TM, TN, WM, WN, false>(acc, st, d, m0, n0, diag, alpha, beta, gamma);
     return;
@@ -727,6 +736,7 @@ __global__ __launch_bounds__(kThreads * KS) void k_ns_gemm(const GemmDesc* __res
 
   const TileRef t = tiles[blockIdx.x];
   const GemmDesc d = probs[t.prob];
+  const float alpha = desc_alpha(d);
   const int ti = t.ij >> 16, tj = t.ij & 0xffff;
   const int m0 = ti * BM, n0 = tj * BN;
   const int grp = threadIdx.x >> 8;       // K group
@@ -908,7 +918,7 @@ __global__ __launch_bounds__(kThreads * KS) void k_ns_gemm(const GemmDesc* __res
   }
 
   gemm_epilogue<T, TM, TN>(acc, reinterpret_cast<float*>(lds) + (threadIdx.x >> 6) * 32 * (32 * TN + 1),
-                           d, m0, n0, ti == tj && d.sym, d.alpha, d.beta, d.gamma, grp == 0);
+                           d, m0, n0, ti == tj && d.sym, alpha, d.beta, d.gamma, grp == 0);
 }
 
 // ---------------------------------------------------------------- NS GEMM, LDS-DMA staging
@@ -1092,6 +1102,7 @@ __global__ __launch_bounds__(64 * WM * WN) void k_ns_gemm_dmap(const GemmDesc* _
 
   const TileRef t = tiles[blockIdx.x];
   const GemmDesc d = probs[t.prob];
+  const float alpha = desc_alpha(d);
   const int ti = t.ij >> 16, tj = t.ij & 0xffff;
   const int m0 = ti * BM, n0 = tj * BN;
   const int tid = threadIdx.x, lane = tid & 63;
@@ -1377,7 +1388,7 @@ __global__ __launch_bounds__(64 * WM * WN) void k_ns_gemm_dmap(const GemmDesc* _
   __syncthreads();
   if (idle) return;
   dma_epilogue<TM, TN, WM, WN>(acc, reinterpret_cast<float*>(lds) + wave * 32 * (32 * TN + 1), d, m0, n0,
-                              ti == tj && d.sym && !above);
+                              ti == tj && d.sym && !above, alpha);
 }
 
 // ---------------------------------------------------------------- update

@@ -143,7 +143,7 @@ hipError_t build_plan_tables(muonbp_ctx* c, int full) {
   const Plan& plan = c->lay.plan[full];
   PlanDev& pd = c->pd[full];
   PlanHostTables h;
-  build_plan_host_tables(c->lay, c->opt, full, c->ws, &h);
+  build_plan_host_tables(c->lay, c->opt, full, c->ws, c->mom, c->scales, &h);
   pd.fuse_scale = h.fuse_scale;
   pd.upd_host = h.upd;
   const std::vector<ScaleDesc>& sd = h.scale;
@@ -307,7 +307,10 @@ muonbp_status muonbp_describe_plan(const muonbp_matrix* mats, int32_t n_mats,
   out->workspace_bytes = p.ws_elems * int64_t(nb);
   out->static_scratch_bytes = scratch_plan(lay, full, o).total;
   out->device_bytes = context_bulk_bytes(lay, o);
-  for (const Problem& q : p.probs) out->gram_units += q.gram ? 1 : 0;
+  for (const Problem& q : p.probs) {
+    out->gram_units += q.gram ? 1 : 0;
+    out->pack_elements += q.in_place ? 0 : q.rows * q.cols;
+  }
   return MUONBP_OK;
 }
 

@@ -162,10 +162,12 @@ void build_phases(Plan* plan, int ns_steps, int poly_slots, int desc_per_problem
     std::vector<Item> gram, poly, qt, upd, apply;
     for (int32_t pi = 0; pi < np; ++pi) {
       const Problem& p = plan->probs[size_t(pi)];
+      // An in-place unit's first Gram and first apply read the momentum.
+      const bool first_m = p.in_place && iter == 0;
       if (!p.gram) {
-        gram.push_back({pi, slot_of(kGram, iter, ns_steps, poly_slots)});
+        gram.push_back({pi, first_m ? kSlotGramM : slot_of(kGram, iter, ns_steps, poly_slots)});
         poly.push_back({pi, slot_of(kPoly, iter, ns_steps, poly_slots)});
-        apply.push_back({pi, slot_of(kApply, iter, ns_steps, poly_slots)});
+        apply.push_back({pi, first_m ? kSlotApplyM : slot_of(kApply, iter, ns_steps, poly_slots)});
         continue;
       }
       // Segment sg of n iterations, j-th of them.
@@ -173,14 +175,16 @@ void build_phases(Plan* plan, int ns_steps, int poly_slots, int desc_per_problem
       const int n = std::min(kGramSegment, ns_steps - sg * kGramSegment);
       const int nseg = (ns_steps + kGramSegment - 1) / kGramSegment;
       const int32_t poly_b = slot_of(kPoly, iter, ns_steps, poly_slots);
-      if (j == 0) gram.push_back({pi, kSlotGram0 + (sg & 1)});
+      if (j == 0) gram.push_back({pi, first_m ? kSlotGramM : kSlotGram0 + (sg & 1)});
       poly.push_back({pi, j == 0 ? poly_b + poly_slots : poly_b});
       if (j > 0) qt.push_back({pi, (j & 1) ? kSlotQ1 : kSlotQ0});
       if (j < n - 1) {
         qt.push_back({pi, j == 0 ? kSlotT0 : kSlotT});
         upd.push_back({pi, j == 0 ? kSlotA0 : kSlotA});
       } else {
-        apply.push_back({pi, kSlotGApply0 + (sg & 1) + 2 * ((n - 1) & 1) + 4 * (sg == nseg - 1)});
+        apply.push_back({pi, p.in_place && sg == 0
+                                 ? kSlotApplyM
+                                 : kSlotGApply0 + (sg & 1) + 2 * ((n - 1) & 1) + 4 * (sg == nseg - 1)});
       }
     }
     add_phase(kGram, gram);
@@ -357,7 +361,8 @@ double ns_unit_dense_flops(int64_t S, int64_t L, int K) {
 
 std::string build_layout(const MatrixShape* mats, int32_t n_mats,
                          int ns_elem_bytes, int ns_steps, int poly_slots, int tile_policy,
-                         int k_split, int apply_mode, Layout* out, bool* shape_error, int gram_mode) {
+                         int k_split, int apply_mode, Layout* out, bool* shape_error, int gram_mode,
+                         bool in_place_input) {
   *shape_error = false;
   if (!mats || n_mats <= 0) return "mats must be a non-empty array";
   if (ns_steps < 0) return "ns_steps must be >= 0";
@@ -489,8 +494,14 @@ std::string build_layout(const MatrixShape* mats, int32_t n_mats,
       Problem& p = plan.probs[pi];
       p.gram = gram_mode != 1 && ns_elem_bytes == 2 && plan.nn_apply && ns_steps >= 2 &&
                (gram_mode == 2 || (p.S >= kGramMinS && 4 * p.L >= 5 * p.S));
+      // The momentum window as a GEMM operand: rows of 16-byte chunks (the
+      // arena is 16-byte aligned), within the kernels' 32-bit byte offsets.
+      const MatrixShape& mm = mats[p.mat];
+      const int64_t mom_off = L.mat_off[p.mat] + p.row0 * mm.cols + p.col0;
+      p.in_place = in_place_input && ns_elem_bytes == 2 && ns_steps >= 1 && plan.nn_apply && !p.trans &&
+                   mm.cols % 8 == 0 && mom_off % 8 == 0 && p.rows * mm.cols * ns_elem_bytes < kMaxOperandBytes;
       if (!place_problem(&p, &cursor, align_elems, plan.nn_apply)) return "workspace too large";
-      add_pack_tiles(&plan, pi);
+      if (!p.in_place) add_pack_tiles(&plan, pi);
       plan.ns_flops += ns_unit_flops(p.S, p.L, ns_steps, p.gram);
       plan.ns_dense_flops += ns_unit_dense_flops(p.S, p.L, ns_steps);
     }

@@ -58,6 +58,11 @@ struct Problem {
   bool gram = false;
   int64_t off_q[2] = {0, 0};  // Q ping-pong (S x Sp), Gram-space units only
   int64_t off_t = 0;          // A_j P_j (S x Sp), Gram-space units only
+  // NS input read in place: an untransposed unit whose input is the bf16
+  // momentum itself (no Nesterov blend) skips the pack; its first Gram and
+  // first apply read the momentum window (leading dimension = the matrix's
+  // columns) and fold the Frobenius scale s into alpha (s^2 and s).
+  bool in_place = false;
 };
 
 // The three grouped products of one NS iteration.
@@ -84,7 +89,9 @@ enum DescSlot {
   // Z[1 - z] = Q[q] Z[z] at slot kSlotGApply0 + z + 2 q + 4 last (last: the
   // final segment, which writes Z^T, i.e. U, for a transposed unit).
   kSlotGApply0 = 11,
-  kSlotPoly0 = 19    // then poly_slots polynomials into B, poly_slots into Q[0]
+  kSlotGramM = 19,   // Problem::in_place: the first Gram, reading the momentum
+  kSlotApplyM = 20,  // Problem::in_place: the first apply, reading the momentum
+  kSlotPoly0 = 21    // then poly_slots polynomials into B, poly_slots into Q[0]
 };
 
 // Gram-space iterations per segment: with longer runs the product chain's
@@ -158,10 +165,15 @@ struct Layout {
 // gram_mode: 0 = the Gram-space iteration where it saves work (above),
 // 1 = never, 2 = on every unit that allows it (bf16, row-major apply,
 // K >= 2) whatever its shape.
+// in_place_input: the NS input is the momentum itself, stored as the NS
+// dtype (bf16 state, bf16 NS, no Nesterov blend); untransposed units whose
+// momentum window is 16-byte aligned then read it in place
+// (Problem::in_place).
 std::string build_layout(const MatrixShape* mats, int32_t n_mats,
                          int ns_elem_bytes, int ns_steps, int poly_slots, int tile_policy,
                          int k_split, int apply_mode,
-                         Layout* out, bool* shape_error, int gram_mode = 0);
+                         Layout* out, bool* shape_error, int gram_mode = 0,
+                         bool in_place_input = false);
 
 // Tile shape the planner picks for one grouped product.
 int32_t choose_variant(const std::vector<Problem>& probs, GemmKind kind, int tile_policy,

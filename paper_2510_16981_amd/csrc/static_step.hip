@@ -100,7 +100,7 @@ extern "C" muonbp_status muonbp_step_static(const muonbp_matrix* mats, int32_t n
   std::vector<BlockDesc> bd;
   try {
     bool shape_err = false;
-    if (!layout_for(shapes, o, &lay, &shape_err).empty())
+    if (!layout_for(shapes, o, &lay, &shape_err, reinterpret_cast<uintptr_t>(momentum) % 16 == 0).empty())
       return shape_err ? MUONBP_E_SHAPE : MUONBP_E_INVALID;
     sp = scratch_plan(lay, full, o);
     if (sp.total > kStaticScratchBytes) return MUONBP_E_TOO_LARGE;
@@ -120,7 +120,8 @@ extern "C" muonbp_status muonbp_step_static(const muonbp_matrix* mats, int32_t n
   std::vector<MatPtrs> ptrs(static_cast<size_t>(n_mats));
   std::vector<const TileRef*> phase_tiles(plan.phases.size());
   try {
-    build_plan_host_tables(lay, o, full, base + sp.ws, &h);
+    build_plan_host_tables(lay, o, full, base + sp.ws, momentum, reinterpret_cast<const float*>(base + sp.scales),
+                           &h);
   } catch (const std::bad_alloc&) {
     return MUONBP_E_NOMEM;
   }

@@ -69,14 +69,18 @@ std::string check_mats(const muonbp_matrix* mats, int32_t n_mats, std::vector<Ma
 }
 
 std::string layout_for(const std::vector<MatrixShape>& shapes, const muonbp_options& o, Layout* out,
-                       bool* shape_error) {
+                       bool* shape_error, bool momentum_aligned) {
+  // The NS input is the momentum itself when it is stored as the NS dtype
+  // and no Nesterov blend is formed.
+  const bool in_place = momentum_aligned && o.state_dtype == MUONBP_BF16 && o.ns_dtype == MUONBP_BF16 &&
+                        o.nesterov == 0;
   return build_layout(shapes.data(), int32_t(shapes.size()), int(dtype_size(o.ns_dtype)), o.ns_steps,
                       poly_slots(o), o.tile_policy, o.k_split, o.apply_mode, out, shape_error,
-                      o.gram_iteration);
+                      o.gram_iteration, in_place);
 }
 
 void build_plan_host_tables(const Layout& lay, const muonbp_options& o, int full, void* ws_base,
-                            PlanHostTables* out) {
+                            const void* mom_base, const float* scales, PlanHostTables* out) {
   const Plan& plan = lay.plan[full];
   const size_t es = dtype_size(o.ns_dtype);
   char* ws = static_cast<char*>(ws_base);
@@ -86,10 +90,16 @@ void build_plan_host_tables(const Layout& lay, const muonbp_options& o, int full
   std::vector<int64_t> pack_tiles_of(plan.probs.size(), 0);
   for (const TileRef& t : plan.pack_tiles) ++pack_tiles_of[size_t(t.prob)];
   int64_t fused_reads = 0;
-  for (size_t i = 0; i < plan.probs.size(); ++i)
+  bool any_in_place = false;
+  for (size_t i = 0; i < plan.probs.size(); ++i) {
     fused_reads += pack_tiles_of[i] * (plan.probs[i].seg_end - plan.probs[i].seg_begin);
-  out->fuse_scale = fused_reads <= kFuseScaleMaxReads;
-  for (const Problem& p : plan.probs) {
+    any_in_place = any_in_place || plan.probs[i].in_place;
+  }
+  // Units read in place have no pack tiles to compute their scale.
+  out->fuse_scale = !any_in_place && fused_reads <= kFuseScaleMaxReads;
+  for (size_t pi = 0; pi < plan.probs.size(); ++pi) {
+    const Problem& p = plan.probs[pi];
+    const size_t desc0 = out->descs.size();
     out->scale.push_back(ScaleDesc{p.seg_begin, p.seg_end});
     const MatrixShape& m = lay.mats[p.mat];
     PackDesc d{};
@@ -151,7 +161,7 @@ void build_plan_host_tables(const Layout& lay, const muonbp_options& o, int full
       };
       if (!p.gram) {
         const GemmDesc unused = out->descs.front();
-        for (int k = kSlotT0; k < kSlotPoly0; ++k) out->descs.push_back(unused);
+        for (int k = kSlotT0; k < kSlotGramM; ++k) out->descs.push_back(unused);
       } else {
         const int64_t q0 = p.off_q[0], q1 = p.off_q[1], t = p.off_t;
         out->descs.push_back(sym_desc(p.off_a, q0, t));       // kSlotT0
@@ -173,6 +183,40 @@ void build_plan_host_tables(const Layout& lay, const muonbp_options& o, int full
                                             Lp, Sp, 1.f, 0.f, 0.f, 0});  // kSlotGApply0 + z + 2 q + 4 last
             }
       }
+    }
+    // The first Gram and the first apply of a unit read in place: the slots
+    // they replace, with the momentum window as Z_0 and alpha scaled by s^2
+    // (Gram) and s (apply).  Placeholders on other units.
+    if (!p.in_place) {
+      const GemmDesc unused = out->descs.front();
+      out->descs.push_back(unused);
+      out->descs.push_back(unused);
+    } else {
+      const MatrixShape& m = lay.mats[p.mat];
+      const void* mw = static_cast<const char*>(mom_base) +
+                       (lay.mat_off[p.mat] + p.row0 * m.cols + p.col0) * int64_t(es);
+      const int32_t ldm = int32_t(m.cols);
+      GemmDesc g = out->descs[desc0 + kSlotGram0];
+      g.X = g.Y = mw;
+      g.ldx = g.ldy = ldm;
+      g.scale = scales + pi;
+      g.scale_sq = 1;
+      out->descs.push_back(g);  // kSlotGramM
+      // The apply the first iteration (segment) would run on Z_0.
+      int slot;
+      if (!p.gram) {
+        slot = o.ns_steps == 1 ? kSlotApplyLast : kSlotApply0;
+      } else {
+        const int n = std::min(kGramSegment, o.ns_steps);
+        const int nseg = (o.ns_steps + kGramSegment - 1) / kGramSegment;
+        slot = kSlotGApply0 + 2 * ((n - 1) & 1) + 4 * (nseg == 1);
+      }
+      GemmDesc a = out->descs[desc0 + size_t(slot)];
+      a.Y = mw;
+      a.ldy = ldm;
+      a.scale = scales + pi;
+      a.scale_sq = 0;
+      out->descs.push_back(a);  // kSlotApplyM
     }
     // Polynomial of iteration k: B = c_k A A^T + b_k A + a_k I (A symmetric;
     // the a I term carries Algorithm 2's a X into the apply).

@@ -33,11 +33,16 @@ int64_t context_bulk_bytes(const Layout& lay, const muonbp_options& o);
 // Copies the shapes (E_INVALID text on a NULL array or a bad count).
 std::string check_mats(const muonbp_matrix* mats, int32_t n_mats, std::vector<MatrixShape>* out);
 
-// build_layout with the NS settings of the options.
+// build_layout with the NS settings of the options.  momentum_aligned: the
+// momentum arena starts on a 16-byte boundary (always for a context's own
+// arena), a condition for reading it in place as the NS input.
 std::string layout_for(const std::vector<MatrixShape>& shapes, const muonbp_options& o, Layout* out,
-                       bool* shape_error);
+                       bool* shape_error, bool momentum_aligned = true);
 
-// Host form of one plan's device tables, the NS workspace starting at `ws`.
+// Host form of one plan's device tables, the NS workspace starting at `ws`,
+// the momentum arena at `mom` and the per-problem scales at `scales` (both
+// device addresses; the units read in place point their first products
+// there).
 struct PlanHostTables {
   std::vector<ScaleDesc> scale;  // one per problem
   std::vector<PackDesc> pack;    // one per problem
@@ -46,7 +51,7 @@ struct PlanHostTables {
   bool fuse_scale = false;       // the pack computes the scales (no k_scale launch)
 };
 void build_plan_host_tables(const Layout& lay, const muonbp_options& o, int full, void* ws,
-                            PlanHostTables* out);
+                            const void* mom, const float* scales, PlanHostTables* out);
 
 std::vector<BlockDesc> block_descs(const Layout& lay);
 

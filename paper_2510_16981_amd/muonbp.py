@@ -58,7 +58,7 @@ class PlanInfo(ctypes.Structure):
                 ("workspace_bytes", ctypes.c_int64),
                 ("gemm_split", ctypes.c_int32 * 3), ("apply_nn", ctypes.c_int32),
                 ("static_scratch_bytes", ctypes.c_int64), ("device_bytes", ctypes.c_int64),
-                ("gram_units", ctypes.c_int64)]
+                ("gram_units", ctypes.c_int64), ("pack_elements", ctypes.c_int64)]
 
 
 class AdamwOptions(ctypes.Structure):

@@ -44,7 +44,7 @@ bool one(const std::vector<MatrixShape>& mats, const muonbp_options& o, bool exp
   static char fake_ws[256];
   for (int full = 0; full < 2; ++full) {
     PlanHostTables h;
-    build_plan_host_tables(lay, o, full, fake_ws, &h);
+    build_plan_host_tables(lay, o, full, fake_ws, fake_ws, reinterpret_cast<const float*>(fake_ws), &h);
     const ScratchPlan sp = scratch_plan(lay, full, o);
     checksum += int64_t(h.descs.size()) + int64_t(h.upd.size()) + sp.total;
     for (const GemmPhase& ph : lay.plan[full].phases)

@@ -313,6 +313,33 @@ def test_gram_iteration_modes(lib):
         info(gram_iteration=3)
 
 
+def test_in_place_units_skip_the_pack(lib):
+    """Untransposed units whose NS input is the bf16 momentum itself are not
+    packed (their first Gram and apply read the momentum in place); a
+    transposed unit, a Nesterov blend, fp32 state or NS, K = 0, the
+    transposed-copy apply or a column count off the 16-byte grid keeps the
+    pack."""
+    mats = [(512, 4096, 1, 1), (4096, 512, 1, 1), (1024, 1024, 1, 1), (1792, 4096, 8, 1), (4096, 1792, 1, 8)]
+    elems = [r * c for r, c, _, _ in mats]
+    packed_full = elems[1] + elems[4]  # the transposed ones
+    info = lambda full=True, **kw: mb.describe_plan(mats, full, mb.options_default(**kw))
+    assert info().pack_elements == packed_full
+    # Block plan: the 8x1 grid's 224 x 4096 blocks are untransposed, the 1x8
+    # grid's 4096 x 224 blocks transposed.
+    assert info(False).pack_elements == packed_full
+    for kw in (dict(nesterov=1), dict(state_dtype=mb.F32), dict(ns_dtype=mb.F32), dict(ns_steps=0),
+               dict(apply_mode=1)):
+        assert info(**kw).pack_elements == sum(elems), kw
+    # In place from one iteration up, with or without the Gram-space iteration.
+    assert info(ns_steps=1).pack_elements == packed_full
+    assert info(gram_iteration=1).pack_elements == packed_full
+    # Same launches and workspace: only the first products' operands move.
+    assert info().gemm_launches == info(nesterov=1).gemm_launches
+    assert info().workspace_bytes == info(nesterov=1).workspace_bytes
+    # Rows of the momentum not on 16-byte boundaries (1004 columns).
+    assert mb.describe_plan([(256, 1004, 1, 1)], True, mb.options_default()).pack_elements == 256 * 1004
+
+
 def test_k_split_applies_to_dma_pipeline_only(lib):
     """A forced K split reaches the interleaved DMA kernels (bf16, K a
     multiple of 8); other kernels never split."""
