@@ -59,7 +59,7 @@ def gram_space_unit(S, L, K, mode, apply_nn):
     (the planner's rule for bf16 NS; mode is the gram_iteration option)."""
     if mode == 1 or not apply_nn or K < 2:
         return False
-    return mode == 2 or (S >= 256 and 4 * L >= 5 * S)
+    return mode == 2 or (S >= 128 and 4 * L >= 5 * S)
 
 
 GRAM_SEGMENT = 3  # Gram-space iterations per segment (the library's kGramSegment)

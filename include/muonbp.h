@@ -148,7 +148,7 @@ typedef struct {
                                each from a fresh Gram of the current Z.
                                0 = that Gram-space iteration on the units
                                where it saves time (bf16 NS, the row-major
-                               apply, K >= 2, S >= 256 and L >= 1.25 S), as
+                               apply, K >= 2, S >= 128 and L >= 1.25 S), as
                                printed elsewhere (default); 1 = as printed
                                everywhere; 2 = the Gram-space iteration on
                                every unit that allows it (bf16, row-major

@@ -108,9 +108,11 @@ constexpr int kGramSegment = 3;
 // break even at L = 1.26 S.  In segments of at most 3 its bf16 error is at
 // or below the printed iteration's from S = 128 to 4096 (emulated, rank-128
 // gradients, 48 momentum steps: 0.91 / 0.80 / 0.63% at S = 128 / 512 /
-// 1792 against 1.06 / 0.95 / 0.75%); the floor keeps the smallest units,
-// whose products are mostly tile padding, as printed.
-constexpr int64_t kGramMinS = 256;
+// 1792 against 1.06 / 0.95 / 0.75%).  Below the floor a unit's products
+// are mostly tile padding; from S = 128 (the 8B-shaped model's k / v
+// shards) the fewer Gram and apply launches still win (block step 0.8%
+// faster than with the floor at 256).
+constexpr int64_t kGramMinS = 128;
 
 // One grouped GEMM launch of a step.
 struct GemmPhase {

@@ -179,11 +179,11 @@ def test_describe_plan_counts_and_flops(lib, name):
         n_gram = 0
         for p, q in units:
             S, L = min(p, q), max(p, q)
-            # Gram-space iteration (bf16, row-major apply, K = 5): S >= 256
+            # Gram-space iteration (bf16, row-major apply, K = 5): S >= 128
             # and L >= 1.25 S.  Segments of 3 and 2 iterations, each one
             # Gram, 4n - 3 symmetric S x S x S products and one apply,
             # instead of K of each of three.
-            g = bool(info.apply_nn) and S >= 256 and 4 * L >= 5 * S
+            g = bool(info.apply_nn) and S >= 128 and 4 * L >= 5 * S
             n_gram += g
             zz, ss, ap = S * (S + 1) * L, S * S * (S + 1), 2 * S * S * L
             sym += (2 * zz + (9 + 5) * ss + 2 * ap) if g else 5 * (zz + ss + ap)
@@ -215,7 +215,7 @@ def test_describe_plan_counts_and_flops(lib, name):
             for p, q in units:
                 S, L = min(p, q), max(p, q)
                 Sp, Lp = -(-S // 8) * 8, -(-L // 8) * 8
-                g = S >= 256 and 4 * L >= 5 * S
+                g = S >= 128 and 4 * L >= 5 * S
                 for n_el in (max(S * Lp, L * Sp),) * 2 + (S * Sp,) * (5 if g else 2):
                     ws = -(-(ws + n_el) // 128) * 128  # 256-byte aligned bf16 buffers
             assert info.workspace_bytes == 2 * ws
@@ -291,13 +291,13 @@ def test_three_launches_per_iteration(lib):
 
 
 def test_gram_iteration_modes(lib):
-    """Which units run the Gram-space iteration: mode 0 from S >= 256 and
+    """Which units run the Gram-space iteration: mode 0 from S >= 128 and
     L >= 1.25 S, mode 1 none, mode 2 every unit that allows it; never with
     K < 2, fp32 NS or the transposed-copy apply; an out-of-range mode is
     refused."""
     mats = [(1024, 1280, 1, 1), (1024, 1272, 1, 1), (1016, 4096, 1, 1), (4096, 1024, 1, 1), (296, 704, 1, 1),
-            (200, 800, 1, 1)]
-    gram = [0, 2, 3, 4]  # 1272 < 1.25 S; 200 < 256
+            (120, 800, 1, 1)]
+    gram = [0, 2, 3, 4]  # 1272 < 1.25 S; 120 < 128
     info = lambda **kw: mb.describe_plan(mats, True, mb.options_default(**kw))
     assert info().gram_units == len(gram)
     assert info(gram_iteration=1).gram_units == 0

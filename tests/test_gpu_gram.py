@@ -4,7 +4,7 @@ Every polynomial of Alg. 2 (App. B) is a polynomial in the Gram matrix of
 the iterate it starts from, so the library may run up to three iterations
 at a time on S x S matrices only (P_j, then Q_j = P_j Q_{j-1} and A_{j+1} =
 (A_j P_j) P_j) and end each such segment with one apply Z <- Q Z: the same
-U up to rounding.  The planner does so for bf16 units with S >= 256 and
+U up to rounding.  The planner does so for bf16 units with S >= 128 and
 L >= 1.25 S (option gram_iteration = 0); mode 2 forces it on every unit that
 allows it, mode 1 turns it off.  The cases cover transposed and
 untransposed units, units that iterate as printed in the same launches,
