@@ -255,7 +255,10 @@ typedef struct {
   int32_t apply_nn;        /* 1: the apply products read Z row-major (no Z^T) */
   int64_t static_scratch_bytes; /* scratch muonbp_step_static needs for a step
                               of this plan (MUONBP_E_TOO_LARGE above
-                              MUONBP_STATIC_SCRATCH_BYTES)                    */
+                              MUONBP_STATIC_SCRATCH_BYTES), with a 16-byte
+                              aligned momentum (otherwise every unit is
+                              packed, see pack_elements, and the pack's
+                              tile list is longer)                            */
   int64_t device_bytes;    /* momentum + NS workspace + K-split sums of a
                               context for these matrices (both plans)       */
   int64_t gram_units;      /* units that run the Gram-space iteration (see
