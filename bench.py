@@ -221,7 +221,7 @@ def cpu_baseline_sampled(workload, mats, period, rank):
 
 
 PROFILES = os.path.join(ROOT, "profiles")
-KERNEL_SOURCES = ("kernels.hip", "plan.cpp", "plan.h", "device_types.h", "muonbp_api.cpp")
+KERNEL_SOURCES = ("kernels.hip", "plan.cpp", "plan.h", "device_types.h", "muonbp_api.cpp", "step_core.cpp")
 
 
 def kernel_source_digest():
