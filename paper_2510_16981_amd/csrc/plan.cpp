@@ -103,6 +103,21 @@ void append_tiles(const Problem& p, GemmKind kind, int v, int32_t desc,
         if (kind == kApply || i <= j) out->push_back(TileRef{desc, int32_t((i << 16) | j)});
 }
 
+}  // namespace
+
+int32_t gram_apply_slot(int ns_steps, int sg) {
+  const int n = std::min(kGramSegment, ns_steps - sg * kGramSegment);
+  const int nseg = (ns_steps + kGramSegment - 1) / kGramSegment;
+  return kSlotGApply0 + (sg & 1) + 2 * ((n - 1) & 1) + 4 * (sg == nseg - 1);
+}
+
+int32_t first_apply_slot(const Problem& p, int ns_steps) {
+  if (p.gram) return gram_apply_slot(ns_steps, 0);
+  return ns_steps == 1 ? kSlotApplyLast : kSlotApply0;
+}
+
+namespace {
+
 int32_t slot_of(GemmKind kind, int iter, int ns_steps, int poly_slots) {
   const int q = iter & 1;
   return kind == kGram   ? kSlotGram0 + q
@@ -173,7 +188,6 @@ void build_phases(Plan* plan, int ns_steps, int poly_slots, int desc_per_problem
       // Segment sg of n iterations, j-th of them.
       const int sg = iter / kGramSegment, j = iter % kGramSegment;
       const int n = std::min(kGramSegment, ns_steps - sg * kGramSegment);
-      const int nseg = (ns_steps + kGramSegment - 1) / kGramSegment;
       const int32_t poly_b = slot_of(kPoly, iter, ns_steps, poly_slots);
       if (j == 0) gram.push_back({pi, first_m ? kSlotGramM : kSlotGram0 + (sg & 1)});
       poly.push_back({pi, j == 0 ? poly_b + poly_slots : poly_b});
@@ -182,9 +196,7 @@ void build_phases(Plan* plan, int ns_steps, int poly_slots, int desc_per_problem
         qt.push_back({pi, j == 0 ? kSlotT0 : kSlotT});
         upd.push_back({pi, j == 0 ? kSlotA0 : kSlotA});
       } else {
-        apply.push_back({pi, p.in_place && sg == 0
-                                 ? kSlotApplyM
-                                 : kSlotGApply0 + (sg & 1) + 2 * ((n - 1) & 1) + 4 * (sg == nseg - 1)});
+        apply.push_back({pi, p.in_place && sg == 0 ? kSlotApplyM : gram_apply_slot(ns_steps, sg)});
       }
     }
     add_phase(kGram, gram);

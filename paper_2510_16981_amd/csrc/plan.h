@@ -177,6 +177,12 @@ std::string build_layout(const MatrixShape* mats, int32_t n_mats,
                          Layout* out, bool* shape_error, int gram_mode = 0,
                          bool in_place_input = false);
 
+// Descriptor slot of segment sg's apply on a Gram-space unit (Z[1 - z] =
+// Q[q] Z[z] with z = sg mod 2, q the buffer of the segment's last Q, and
+// the final segment writing U), and the slot of a unit's first apply.
+int32_t gram_apply_slot(int ns_steps, int sg);
+int32_t first_apply_slot(const Problem& p, int ns_steps);
+
 // Tile shape the planner picks for one grouped product.
 int32_t choose_variant(const std::vector<Problem>& probs, GemmKind kind, int tile_policy,
                        int ns_elem_bytes);

@@ -192,9 +192,8 @@ void build_plan_host_tables(const Layout& lay, const muonbp_options& o, int full
       out->descs.push_back(unused);
       out->descs.push_back(unused);
     } else {
-      const MatrixShape& m = lay.mats[p.mat];
       const void* mw = static_cast<const char*>(mom_base) +
-                       (lay.mat_off[p.mat] + p.row0 * m.cols + p.col0) * int64_t(es);
+                       (lay.mat_off[p.mat] + p.row0 * m.cols + p.col0) * int64_t(dtype_size(o.state_dtype));
       const int32_t ldm = int32_t(m.cols);
       GemmDesc g = out->descs[desc0 + kSlotGram0];
       g.X = g.Y = mw;
@@ -203,15 +202,7 @@ void build_plan_host_tables(const Layout& lay, const muonbp_options& o, int full
       g.scale_sq = 1;
       out->descs.push_back(g);  // kSlotGramM
       // The apply the first iteration (segment) would run on Z_0.
-      int slot;
-      if (!p.gram) {
-        slot = o.ns_steps == 1 ? kSlotApplyLast : kSlotApply0;
-      } else {
-        const int n = std::min(kGramSegment, o.ns_steps);
-        const int nseg = (o.ns_steps + kGramSegment - 1) / kGramSegment;
-        slot = kSlotGApply0 + 2 * ((n - 1) & 1) + 4 * (nseg == 1);
-      }
-      GemmDesc a = out->descs[desc0 + size_t(slot)];
+      GemmDesc a = out->descs[desc0 + size_t(first_apply_slot(p, o.ns_steps))];
       a.Y = mw;
       a.ldy = ldm;
       a.scale = scales + pi;
