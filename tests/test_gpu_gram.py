@@ -55,6 +55,18 @@ def test_mixed_units_block_and_full():
     _check(Case(mats=MIXED, period=2, steps=4, rank=128, seed=11), [4, 3])
 
 
+# Units at and just above the Gram-space floor (S = 128 .. 256): 128 x 1024
+# and 200 x 600 read the momentum in place, 1024 x 136 is transposed (and
+# packed), 120 x 800 lies below the floor (as printed), 256 x 2048 in two
+# column blocks reads its 256 x 1024 blocks in place with the matrix's row
+# pitch.
+SMALL = [(128, 1024, 1, 1), (1024, 136, 1, 1), (200, 600, 1, 1), (120, 800, 1, 1), (256, 2048, 1, 2)]
+
+
+def test_units_at_the_floor():
+    _check(Case(mats=SMALL, period=2, steps=4, rank=32, seed=31), [5, 4])
+
+
 def test_fp32_weights_and_coefficient_table():
     _check(Case(mats=MIXED[:2], period=1, steps=3, rank=128, seed=12, param="f32", state="f32",
                 coeffs=[(3.4445, -4.7750, 2.0315), (3.0, -3.2, 1.2), (2.0, -1.5, 0.5)]), [2, 2])
