@@ -1211,10 +1211,20 @@ __global__ __launch_bounds__(64 * WM * WN) void k_ns_gemm_dmap(const GemmDesc* _
                    8 * (si & 1);
     }
   }
-  auto read1 = [&](int kt, int s, int f) {
+  // A diagonal tile of a product whose two operands are the same rows of
+  // the same matrix (the Gram Z Z^T, the polynomial's A A) needs only the X
+  // panel: the Y fragments are read from the X rows (fas), and the slice's
+  // copies are the X copies alone (the first XG / W of every wave).
+  constexpr bool kShareXY = !NN && EVEN && XG % W == 0;
+  const bool share_xy = kShareXY && ti == tj && d.X == d.Y && d.ldx == d.ldy && d.M == d.N;
+  uint32_t fas[NF];
+#pragma unroll
+  for (int f = 0; f < NF; ++f) fas[f] = f < TM ? fa[f] : fa[f] - BM * kDmaRow;
+  auto read1 = [&](auto sh, int kt, int s, int f) {
     const uint32_t sbase = (kt % NS) * G::STAGE;
     const int c = 2 * s + (lane >> 5);
-    return lds_read16(fa[f] + sbase + ((c ^ fsw[f]) << 4));
+    const uint32_t base = decltype(sh)::value ? fas[f] : fa[f];
+    return lds_read16(base + sbase + ((c ^ fsw[f]) << 4));
   };
   // Fragments of one K step: f (X, and Y when NT) from 16-byte reads; NN Y
   // fragments from two transpose reads each, held as halves (yl, yh) until
@@ -1223,12 +1233,12 @@ __global__ __launch_bounds__(64 * WM * WN) void k_ns_gemm_dmap(const GemmDesc* _
   using Fr = u32x4_t[NF];
   using Yh = u32x2_t[YH];
   // Read instruction o (0 <= o < NR) of K step s of slice kt.
-  auto read_op = [&](Fr& f, Yh& yl, Yh& yh, int kt, int s, int o) {
+  auto read_op = [&](auto sh, Fr& f, Yh& yl, Yh& yh, int kt, int s, int o) {
     if constexpr (!NN) {
-      f[o] = read1(kt, s, o);
+      f[o] = read1(sh, kt, s, o);
     } else {
       if (o < TM) {
-        f[o] = read1(kt, s, o);
+        f[o] = read1(sh, kt, s, o);
       } else {
         const int j = (o - TM) >> 1, r = (o - TM) & 1;
         const uint32_t a = fa[TM + j] + (kt % NS) * G::STAGE + (16 * s + 4 * r) * (2 * BN);
@@ -1278,18 +1288,20 @@ __global__ __launch_bounds__(64 * WM * WN) void k_ns_gemm_dmap(const GemmDesc* _
 
   u32x4_t f0[NF], f1[NF];
   u32x2_t y0l[YH], y0h[YH], y1l[YH], y1h[YH];
-  auto kloop = [&](auto math) {
+  auto kloop = [&](auto math, auto sh) {
     constexpr bool MATH = decltype(math)::value;
+    // Copies per wave and slice: all LPW, or the X copies alone.
+    constexpr int LP = decltype(sh)::value ? XG / W : LPW;
     // Prologue: fill the ring, publish slice kb, read its first K step.
 #pragma unroll
     for (int s = 0; s < NS; ++s)
 #pragma unroll
-      for (int jj = 0; jj < LPW; ++jj) copy(kb + s, jj);
-    __builtin_amdgcn_s_waitcnt(vmcnt_imm((NS - 1) * LPW));
+      for (int jj = 0; jj < LP; ++jj) copy(kb + s, jj);
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm((NS - 1) * LP));
     barrier_no_fence();
     if constexpr (MATH)
 #pragma unroll
-      for (int o = 0; o < NR; ++o) read_op(f0, y0l, y0h, kb, 0, o);
+      for (int o = 0; o < NR; ++o) read_op(sh, f0, y0l, y0h, kb, 0, o);
     frag_wait(f0, y0l, y0h);
 
     for (int kt = kb; kt < ke; ++kt) {
@@ -1309,7 +1321,7 @@ __global__ __launch_bounds__(64 * WM * WN) void k_ns_gemm_dmap(const GemmDesc* _
         if constexpr (MATH) {
           mfma(f0, q);
 #pragma unroll
-          for (int o = q * RPM; o < (q + 1) * RPM && o < NR; ++o) read_op(f1, y1l, y1h, kt, 1, o);
+          for (int o = q * RPM; o < (q + 1) * RPM && o < NR; ++o) read_op(sh, f1, y1l, y1h, kt, 1, o);
         }
         __builtin_amdgcn_sched_barrier(0);
       }
@@ -1323,10 +1335,10 @@ __global__ __launch_bounds__(64 * WM * WN) void k_ns_gemm_dmap(const GemmDesc* _
       // Slice kt + 1 has landed for this wave (two later slices may still be
       // in flight); after the barrier it has landed for every wave, and no
       // wave reads slice kt any more, so its slot takes slice kt + NS.
-      __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * LPW));
+      __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * LP));
       barrier_no_fence();
       // Step 1, rest, with the reads of slice kt + 1 and the refill copies.
-      constexpr int OPS = LPW + NR;
+      constexpr int OPS = LP + NR;
 #pragma unroll
       for (int q = H; q < NM; ++q) {
         if constexpr (MATH) mfma(f1, q);
@@ -1335,7 +1347,7 @@ __global__ __launch_bounds__(64 * WM * WN) void k_ns_gemm_dmap(const GemmDesc* _
 #pragma unroll
         for (int o = lo; o < hi; ++o) {
           if (o < NR) {
-            if constexpr (MATH) read_op(f0, y0l, y0h, kt + 1, 0, o);
+            if constexpr (MATH) read_op(sh, f0, y0l, y0h, kt + 1, 0, o);
           } else
             copy(kt + NS, o - NR);
         }
@@ -1344,10 +1356,18 @@ __global__ __launch_bounds__(64 * WM * WN) void k_ns_gemm_dmap(const GemmDesc* _
       frag_wait(f0, y0l, y0h);
     }
   };
-  if (idle)
-    kloop(std::false_type{});
-  else
-    kloop(std::true_type{});
+  if (share_xy) {
+    if constexpr (kShareXY) {
+      if (idle)
+        kloop(std::false_type{}, std::true_type{});
+      else
+        kloop(std::true_type{}, std::true_type{});
+    }
+  } else if (idle) {
+    kloop(std::false_type{}, std::false_type{});
+  } else {
+    kloop(std::true_type{}, std::false_type{});
+  }
   // Zero-filled copies past the share may still be in flight: let them land
   // before the epilogue reuses the ring.
   __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
