@@ -90,16 +90,20 @@ int64_t count_tiles(const std::vector<Problem>& probs, GemmKind kind, int v) {
 // rows, each band walked column by column (rows inside a column first).  An
 // XCD's concurrent tiles then form a group x (tiles / group) block of C that
 // shares `group` X panels and as many Y panels as it has columns, instead of
-// one X panel and a Y panel per tile.  Bands of 8 rows of tiles, except
-// for the Gram on tiles taller than 128 rows, which keeps bands of 4
-// (measured on the 8B-shaped model: bands of 8 make the full-step apply
-// 1.7% faster and its Gram 2% slower; bands of 2 make the apply 5% slower).
+// one X panel and a Y panel per tile.  Tiles taller than 128 rows take
+// bands of 4, or of 8 for the polynomial and apply products of a unit with
+// at least 16 rows of tiles (measured on the 8B-shaped model: bands of 8
+// make the full-step apply, 16 x 56 tiles, 1.7% faster; on the block
+// steps' 7-row units they leave the time unchanged and raise the apply's
+// traffic by 60%, and the Gram is 2% slower with them; bands of 2 make the
+// apply 5% slower).
 void append_tiles(const Problem& p, GemmKind kind, int v, int32_t desc,
                   std::vector<TileRef>* out) {
-  const int64_t group = (kGemmTileRows[v] == 128 && v != kGemm128x128Split2) || kind != kGram ? 8 : 4;
   int64_t m, c, k;
   gemm_dims(p, kind, &m, &c, &k);
   const int64_t tm = ceil_div(m, kGemmTileRows[v]), tn = ceil_div(c, kGemmTileCols[v]);
+  const bool small_tiles = kGemmTileRows[v] == 128 && v != kGemm128x128Split2;
+  const int64_t group = small_tiles || (kind != kGram && tm >= 16) ? 8 : 4;
   for (int64_t g0 = 0; g0 < tm; g0 += group)
     for (int64_t j = (kind == kApply ? 0 : g0); j < tn; ++j)
       for (int64_t i = g0; i < std::min(tm, g0 + group); ++i)
